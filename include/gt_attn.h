@@ -1,0 +1,141 @@
+/*
+ * gt_attn.h - topology-biased graph attention on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of libgtattn.so. Plain pointers and sizes only; every tensor pointer
+ * is a DEVICE pointer owned by the caller, dense and row-major in the layout
+ * stated for it. The library never allocates, frees or retains caller memory
+ * and keeps no mutable global state.
+ *
+ * The operation (MegaGraph, Section II-A, Eq. (1)): for every head h,
+ *
+ *     O_h = softmax( scale * Q_h K_h^T + B_h ) V_h,
+ *     B_h[i, j] = table[h, spd[i, j]]   (0 when spd[i, j] >= n_buckets),
+ *
+ * i.e. the structural-encoding bias of the paper realised as one learned
+ * scalar per (head, shortest-path-distance bucket). spd is a uint8 index
+ * matrix shared by all heads. The scale multiplies Q K^T only; the bias is
+ * added unscaled. LSE is the natural-log log-sum-exp of each score row.
+ *
+ * Conventions shared by every entry point
+ *   - dtype GT_BF16: Q, K, V, O, dO, dQ, dK, dV are bfloat16; products run on
+ *     bf16 matrix cores with fp32 accumulation; P and dS are rounded to bf16
+ *     before their products. GT_F32: all of those are fp32 and computed in
+ *     fp32. table, dtable, LSE, partial O and partial LSE are always fp32.
+ *   - d (head dim) must be 32 or 64; 1 <= n_buckets <= 256.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream) and stream-ordered; results are valid once the stream has
+ *     synchronised. Calls on different streams do not interfere except
+ *     through memory the caller shares between them.
+ *   - Errors: arguments are validated on the host BEFORE anything is
+ *     launched; on any error no output is touched. A failed launch returns
+ *     GT_ERR_LAUNCH.
+ *   - Not checked (preconditions): device pointers really are device memory
+ *     of the stated size; outputs do not alias inputs; table entries are
+ *     finite or -inf. A row whose every score is -inf gets O = 0, LSE = -inf
+ *     and zero gradient.
+ */
+#ifndef GT_ATTN_H
+#define GT_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { GT_F32 = 0, GT_BF16 = 1 } gt_dtype_t;
+
+typedef enum {
+  GT_OK = 0,
+  GT_ERR_INVALID = 1,     /* null pointer, bad size, bad offset, bad scale   */
+  GT_ERR_UNSUPPORTED = 2, /* head dim or dtype this build has no kernel for  */
+  GT_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required      */
+  GT_ERR_LAUNCH = 4       /* the HIP runtime rejected a kernel launch        */
+} gt_status_t;
+
+/* Forward over all N nodes (Eq. (1)).
+ *   q, k, v  [H, N, d] dtype          spd    [N, N] uint8, element (i,j) at i*N + j
+ *   table    [H, n_buckets] fp32      o      [H, N, d] dtype (written)
+ *   lse      [H, N] fp32 (written)    scale  > 0 and finite (1/sqrt(d) usual)
+ * Deterministic: the same inputs give bitwise identical O and LSE. */
+gt_status_t gt_attn_fwd(const void* q, const void* k, const void* v,
+                        const uint8_t* spd, const float* table, int32_t n_buckets,
+                        void* o, float* lse,
+                        int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
+                        float scale, void* stream);
+
+/* Bytes of device workspace gt_attn_bwd needs for these sizes. */
+size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dtype);
+
+/* Backward of L = sum(O * dO) (the chain rule through Eq. (1); the paper's
+ * training step needs it but does not write it out):
+ *   dV = P^T dO,  dS = P * (dO V^T - rowsum(dO * O)),
+ *   dQ = scale dS K,  dK = scale dS^T Q,
+ *   dtable[h, b] = sum of dS[h, i, j] over pairs with spd[i, j] == b.
+ *   o, lse   the forward outputs for the same inputs
+ *   d_o      [H, N, d] dtype
+ *   dq,dk,dv [H, N, d] dtype, OVERWRITTEN
+ *   dtable   [H, n_buckets] fp32, OVERWRITTEN (not accumulated)
+ *   workspace at least gt_attn_bwd_workspace_size(H, N, d, dtype) bytes of
+ *            device memory, 256-byte aligned; contents on entry are ignored.
+ * dtable is reduced with floating-point atomics: its last bits may differ
+ * from run to run. No gradient flows to spd. */
+gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v,
+                        const uint8_t* spd, const float* table, int32_t n_buckets,
+                        const void* o, const float* lse, const void* d_o,
+                        void* dq, void* dk, void* dv, float* dtable,
+                        void* workspace, size_t workspace_bytes,
+                        int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
+                        float scale, void* stream);
+
+/* One step of graph-aware context parallelism (Section III-A-1: ring-based
+ * KV rotation, query-dimension bias sharding, Eq. (2)). A rank holding the
+ * query shard q_shard and, at this step, one KV block computes the block's
+ * biased attention with the bias columns sliced to match that block:
+ *
+ *   S[i, j] = scale * q_shard[i] . k_shard[j] + table[h, spd[(row_off+i)*ld_spd + col_off + j]]
+ *
+ * and returns the block-normalised partial O_p = softmax_j(S) v_shard with
+ * its log-sum-exp LSE_p (natural log). Combine partials with gt_attn_merge.
+ *   q_shard  [H, Sq, d] dtype         k_shard, v_shard [H, Sk, d] dtype
+ *   spd      the rank's bias shard; element (r, c) at spd[r*ld_spd + c],
+ *            r = row_off + i, c = col_off + j (typically row_off = 0 and
+ *            col_off = the KV block's first global node id)
+ *   o_part   [H, Sq, d] fp32 (written)  lse_part [H, Sq] fp32 (written)
+ * Sq >= 1, Sk >= 0, row_off >= 0, col_off >= 0, ld_spd >= col_off + Sk.
+ * Sk = 0 gives o_part = 0 and lse_part = -inf (k_shard, v_shard, spd may
+ * then be NULL). Deterministic. */
+gt_status_t gt_attn_ring_step(const void* q_shard, int64_t Sq,
+                              const void* k_shard, const void* v_shard, int64_t Sk,
+                              const uint8_t* spd, int64_t ld_spd,
+                              int64_t row_off, int64_t col_off,
+                              const float* table, int32_t n_buckets,
+                              float* o_part, float* lse_part,
+                              int32_t H, int32_t d, gt_dtype_t dtype,
+                              float scale, void* stream);
+
+/* Combine n_parts block partials into the attention over all of their keys
+ * (Section III-A-1 part 3: every partial's softmax statistics already hold
+ * its bias slice, so the combination is exact):
+ *   LSE = log sum_p exp(LSE_p),  O = sum_p exp(LSE_p - LSE) O_p.
+ * Parts with LSE_p = -inf contribute nothing; if every part is -inf the row
+ * gets O = 0, LSE = -inf.
+ *   o_parts  [n_parts, H, S, d] fp32   lse_parts [n_parts, H, S] fp32
+ *   o        [H, S, d] dtype (written) lse       [H, S] fp32 (written)
+ * n_parts >= 1; n_parts = 1 is a copy/cast. Deterministic. */
+gt_status_t gt_attn_merge(const float* o_parts, const float* lse_parts, int32_t n_parts,
+                          void* o, float* lse,
+                          int32_t H, int64_t S, int32_t d, gt_dtype_t dtype,
+                          void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* gt_status_string(gt_status_t s);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t gt_attn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GT_ATTN_H */

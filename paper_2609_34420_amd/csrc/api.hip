@@ -1,0 +1,151 @@
+// C ABI of libgtattn: host-side validation, then stream-ordered launches.
+// Nothing is launched and no output is touched unless every check passes.
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/gt_attn.h"
+#include "kernels.hpp"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kMaxGrid = 0x7fffffffLL;
+
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline bool dims_ok(int32_t d) { return d == 32 || d == 64; }
+
+inline bool dtype_ok(gt_dtype_t t) { return t == GT_F32 || t == GT_BF16; }
+
+inline bool scale_ok(float s) { return std::isfinite(s) && s > 0.0f; }
+
+// 16-byte spd loads are legal when every 16-key group of every row starts
+// 16-byte aligned.
+inline int spd_vec(const uint8_t* spd, int64_t ld, int64_t row_off, int64_t col_off) {
+  const uintptr_t base = reinterpret_cast<uintptr_t>(spd) + (uintptr_t)(row_off * ld + col_off);
+  return ((base & 15u) == 0 && (ld & 15) == 0) ? 1 : 0;
+}
+
+inline gt_status_t launched(hipError_t e) { return e == hipSuccess ? GT_OK : GT_ERR_LAUNCH; }
+
+}  // namespace
+
+extern "C" {
+
+const char* gt_status_string(gt_status_t s) {
+  switch (s) {
+    case GT_OK: return "GT_OK";
+    case GT_ERR_INVALID: return "GT_ERR_INVALID: invalid argument";
+    case GT_ERR_UNSUPPORTED: return "GT_ERR_UNSUPPORTED: unsupported head dim or dtype";
+    case GT_ERR_WORKSPACE: return "GT_ERR_WORKSPACE: workspace missing or too small";
+    case GT_ERR_LAUNCH: return "GT_ERR_LAUNCH: kernel launch failed";
+  }
+  return "unknown gt_status_t";
+}
+
+int32_t gt_attn_version(void) { return 100; }
+
+gt_status_t gt_attn_ring_step(const void* q_shard, int64_t Sq, const void* k_shard,
+                              const void* v_shard, int64_t Sk, const uint8_t* spd,
+                              int64_t ld_spd, int64_t row_off, int64_t col_off,
+                              const float* table, int32_t n_buckets, float* o_part,
+                              float* lse_part, int32_t H, int32_t d, gt_dtype_t dtype,
+                              float scale, void* stream) {
+  if (!dtype_ok(dtype)) return GT_ERR_UNSUPPORTED;
+  if (!dims_ok(d)) return GT_ERR_UNSUPPORTED;
+  if (H < 1 || Sq < 1 || Sk < 0 || row_off < 0 || col_off < 0) return GT_ERR_INVALID;
+  if (n_buckets < 1 || n_buckets > 256 || !scale_ok(scale)) return GT_ERR_INVALID;
+  if (!q_shard || !table || !o_part || !lse_part) return GT_ERR_INVALID;
+  if (Sk > 0 && (!k_shard || !v_shard || !spd)) return GT_ERR_INVALID;
+  if (Sk > 0 && ld_spd < col_off + Sk) return GT_ERR_INVALID;
+  if (!aligned16(q_shard) || !aligned16(o_part) || (Sk > 0 && (!aligned16(k_shard) || !aligned16(v_shard))))
+    return GT_ERR_INVALID;
+  if ((Sq + 127) / 128 * (int64_t)H > kMaxGrid) return GT_ERR_INVALID;
+  gt::FwdArgs a{};
+  a.q = q_shard; a.k = k_shard; a.v = v_shard;
+  a.spd = spd; a.ld_spd = ld_spd; a.row_off = row_off; a.col_off = col_off;
+  a.table = table; a.n_buckets = n_buckets;
+  a.o = o_part; a.lse = lse_part;
+  a.H = H; a.Sq = Sq; a.Sk = Sk; a.scale = scale;
+  a.spd_vec = Sk > 0 ? spd_vec(spd, ld_spd, row_off, col_off) : 0;
+  return launched(gt::launch_fwd(a, d, dtype == GT_BF16, true, static_cast<hipStream_t>(stream)));
+}
+
+gt_status_t gt_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* spd,
+                        const float* table, int32_t n_buckets, void* o, float* lse,
+                        int32_t H, int64_t N, int32_t d, gt_dtype_t dtype, float scale,
+                        void* stream) {
+  if (!dtype_ok(dtype)) return GT_ERR_UNSUPPORTED;
+  if (!dims_ok(d)) return GT_ERR_UNSUPPORTED;
+  if (H < 1 || N < 1 || n_buckets < 1 || n_buckets > 256 || !scale_ok(scale)) return GT_ERR_INVALID;
+  if (!q || !k || !v || !spd || !table || !o || !lse) return GT_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return GT_ERR_INVALID;
+  if ((N + 127) / 128 * (int64_t)H > kMaxGrid) return GT_ERR_INVALID;
+  gt::FwdArgs a{};
+  a.q = q; a.k = k; a.v = v;
+  a.spd = spd; a.ld_spd = N; a.row_off = 0; a.col_off = 0;
+  a.table = table; a.n_buckets = n_buckets;
+  a.o = o; a.lse = lse;
+  a.H = H; a.Sq = N; a.Sk = N; a.scale = scale;
+  a.spd_vec = spd_vec(spd, N, 0, 0);
+  return launched(gt::launch_fwd(a, d, dtype == GT_BF16, dtype == GT_F32, static_cast<hipStream_t>(stream)));
+}
+
+size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dtype) {
+  (void)d;
+  (void)dtype;
+  if (H < 1 || N < 1) return 0;
+  const size_t rows = (size_t)H * (size_t)N;
+  return 2 * align_up(rows * sizeof(float));
+}
+
+gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v, const uint8_t* spd,
+                        const float* table, int32_t n_buckets, const void* o,
+                        const float* lse, const void* d_o, void* dq, void* dk, void* dv,
+                        float* dtable, void* workspace, size_t workspace_bytes, int32_t H,
+                        int64_t N, int32_t d, gt_dtype_t dtype, float scale, void* stream) {
+  if (!dtype_ok(dtype)) return GT_ERR_UNSUPPORTED;
+  if (!dims_ok(d)) return GT_ERR_UNSUPPORTED;
+  if (H < 1 || N < 1 || n_buckets < 1 || n_buckets > 256 || !scale_ok(scale)) return GT_ERR_INVALID;
+  if (!q || !k || !v || !spd || !table || !o || !lse || !d_o || !dq || !dk || !dv || !dtable)
+    return GT_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(d_o) ||
+      !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+    return GT_ERR_INVALID;
+  if ((N + 127) / 128 * (int64_t)H > kMaxGrid) return GT_ERR_INVALID;
+  const size_t need = gt_attn_bwd_workspace_size(H, N, d, dtype);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return GT_ERR_WORKSPACE;
+  const size_t rows = (size_t)H * (size_t)N;
+  gt::BwdArgs a{};
+  a.q = q; a.k = k; a.v = v;
+  a.spd = spd; a.ld_spd = N;
+  a.table = table; a.n_buckets = n_buckets;
+  a.o = o; a.lse = lse; a.d_o = d_o;
+  a.dq = dq; a.dk = dk; a.dv = dv; a.dtable = dtable;
+  a.lse2 = static_cast<float*>(workspace);
+  a.dlt = reinterpret_cast<float*>(static_cast<char*>(workspace) + align_up(rows * sizeof(float)));
+  a.H = H; a.N = N; a.scale = scale;
+  a.spd_vec = spd_vec(spd, N, 0, 0);
+  return launched(gt::launch_bwd(a, d, dtype == GT_BF16, static_cast<hipStream_t>(stream)));
+}
+
+gt_status_t gt_attn_merge(const float* o_parts, const float* lse_parts, int32_t n_parts,
+                          void* o, float* lse, int32_t H, int64_t S, int32_t d,
+                          gt_dtype_t dtype, void* stream) {
+  if (!dtype_ok(dtype)) return GT_ERR_UNSUPPORTED;
+  if (!dims_ok(d)) return GT_ERR_UNSUPPORTED;
+  if (n_parts < 1 || H < 1 || S < 1) return GT_ERR_INVALID;
+  if (!o_parts || !lse_parts || !o || !lse) return GT_ERR_INVALID;
+  if (!aligned16(o_parts) || !aligned16(o)) return GT_ERR_INVALID;
+  const int64_t rows = (int64_t)H * S;
+  if ((rows * (d / 4) + 255) / 256 > kMaxGrid) return GT_ERR_INVALID;
+  gt::MergeArgs a{};
+  a.o_parts = o_parts; a.lse_parts = lse_parts; a.n_parts = n_parts;
+  a.o = o; a.lse = lse; a.rows = rows; a.d = d;
+  return launched(gt::launch_merge(a, dtype == GT_BF16, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,120 @@
+// Device-side building blocks shared by the gfx950 attention kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gt {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+
+// 32x32x16 bf16 matrix-core product, fp32 accumulate (gfx950).
+//   A operand: lane l supplies row (l & 31), k = (l >> 5) * 8 + [0, 8)
+//   B operand: lane l supplies col (l & 31), k = (l >> 5) * 8 + [0, 8)
+//   C/D:       lane l holds col (l & 31), rows 8u + 4 (l >> 5) + t in
+//              register 4u + t (u, t in [0, 4))
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// 2^x on the transcendental unit (v_exp_f32): exp2(-inf) = 0.
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Operand row permutation inside a 32-row block. If the A operand of a
+// product loads block row perm32(m) into MFMA row m, then the C layout gives
+// lane half g (lane >> 5) the 16 CONSECUTIVE block rows 16 g + r in its
+// registers r = 0..15: C row 8u + 4g + t  <->  block row 16g + 4u + t.
+// Consecutive rows per lane let one 16-byte load fetch the lane's spd bytes
+// and let 8 consecutive registers feed the next product's operand.
+__device__ __forceinline__ int perm32(int m) {
+  return (((m >> 2) & 1) << 4) | ((m >> 3) << 2) | (m & 3);
+}
+
+// XOR swizzle of 16-byte chunks in a row-major LDS tile whose rows hold D
+// bf16 (D / 8 chunks). Chosen so that the 8 lanes of one ds_read_b128 phase
+// reading MFMA rows perm32(0..7) (or perm32(8..15), ...) hit 8 distinct bank
+// groups.
+template <int D>
+__device__ __forceinline__ int swz_rows(int row, int chunk) {
+  if constexpr (D == 64) {
+    return chunk ^ ((row & 3) | ((row >> 2) & 4));
+  } else {
+    return chunk ^ (((row >> 1) & 1) | ((row >> 3) & 2));
+  }
+}
+
+// Swizzle for a transposed tile: row = feature c, 64 keys per row (8 chunks).
+__device__ __forceinline__ int swz_t64(int row, int chunk) { return chunk ^ (row & 7); }
+
+__device__ __forceinline__ bf16x8 lds_b128(const uint16_t* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+
+__device__ __forceinline__ bf16x8 zero_bf16x8() {
+  bf16x8 z;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) z[i] = (__bf16)0.0f;
+  return z;
+}
+
+__device__ __forceinline__ f32x16 zero_f32x16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.0f;
+  return z;
+}
+
+__device__ __forceinline__ bf16x8 cvt_bf16x8(const float* x) {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = (__bf16)x[i];
+  return r;
+}
+
+__device__ __forceinline__ uint16_t f2bf(float x) {
+  __bf16 b = (__bf16)x;
+  return __builtin_bit_cast(uint16_t, b);
+}
+
+__device__ __forceinline__ float bf2f(uint16_t x) {
+  return __uint_as_float(((uint32_t)x) << 16);
+}
+
+// Workgroup id -> logical id so that consecutive logical ids (the H heads of
+// one row block, which share their spd tiles) land on the same XCD at about
+// the same time. Workgroups are handed to the 8 XCDs round robin.
+__device__ __forceinline__ int64_t xcd_remap(int64_t w, int64_t total) {
+  if ((total & 7) != 0) return w;
+  return (w & 7) * (total >> 3) + (w >> 3);
+}
+
+// 16 spd bytes spd_row[j .. j+15] as four dwords; bytes at or past `limit`
+// read as 0. `vec`: the 16 bytes are 16-byte aligned and may be loaded whole.
+__device__ __forceinline__ void load_spd16(const uint8_t* spd_row, int64_t j, int64_t limit,
+                                           bool vec, uint32_t w[4]) {
+  if (spd_row == nullptr) {
+    w[0] = w[1] = w[2] = w[3] = 0u;
+    return;
+  }
+  if (vec && j + 16 <= limit) {
+    const uint4 v = *reinterpret_cast<const uint4*>(spd_row + j);
+    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+    return;
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint32_t x = 0;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int64_t jj = j + 4 * q + t;
+      const uint32_t b = (jj < limit) ? (uint32_t)spd_row[jj] : 0u;
+      x |= b << (8 * t);
+    }
+    w[q] = x;
+  }
+}
+
+}  // namespace gt

@@ -1,0 +1,68 @@
+// Kernel argument blocks and host-side launchers (internal to libgtattn).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gt {
+
+// Biased attention of a query block against a key block with the bias slice
+// aligned by global offsets. Serves both the full forward (offsets 0,
+// ld = N) and one context-parallel ring step.
+struct FwdArgs {
+  const void* q;          // [H, Sq, d]
+  const void* k;          // [H, Sk, d]
+  const void* v;          // [H, Sk, d]
+  const uint8_t* spd;     // element (r, c) at spd[r * ld_spd + c]
+  int64_t ld_spd;
+  int64_t row_off;        // spd row of query 0
+  int64_t col_off;        // spd column of key 0
+  const float* table;     // [H, n_buckets]
+  int32_t n_buckets;
+  void* o;                // [H, Sq, d] (bf16 or fp32)
+  float* lse;             // [H, Sq] natural log
+  int32_t H;
+  int64_t Sq;
+  int64_t Sk;
+  float scale;            // multiplies Q K^T
+  int32_t spd_vec;        // every 16-byte spd group is 16-byte aligned
+};
+
+struct BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const uint8_t* spd;
+  int64_t ld_spd;
+  const float* table;
+  int32_t n_buckets;
+  const void* o;
+  const float* lse;
+  const void* d_o;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* dtable;
+  float* lse2;            // workspace [H, N]: LSE * log2(e), +inf for empty rows
+  float* dlt;             // workspace [H, N]: rowsum(dO * O)
+  int32_t H;
+  int64_t N;
+  float scale;
+  int32_t spd_vec;
+};
+
+struct MergeArgs {
+  const float* o_parts;   // [P, H, S, d]
+  const float* lse_parts; // [P, H, S]
+  int32_t n_parts;
+  void* o;                // [H, S, d]
+  float* lse;             // [H, S]
+  int64_t rows;           // H * S
+  int32_t d;
+};
+
+// Launchers return the hipError_t of the launch.
+hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStream_t s);
+hipError_t launch_bwd(const BwdArgs& a, int d, bool bf16, hipStream_t s);
+hipError_t launch_merge(const MergeArgs& a, bool out_bf16, hipStream_t s);
+
+}  // namespace gt

@@ -1,0 +1,214 @@
+"""GPU parity at sizes the oracle computes in full: the HIP path (through the
+C ABI) against the fp64 oracle, element by element, on the same seeded
+inputs. Sizes span several tiles and ragged tails; edge cases cover N = 1,
+empty KV blocks, fully masked rows, out-of-range buckets, asymmetric spd,
+unaligned spd slices and row/column offsets."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_34420_amd as gt
+import synth
+from gpu_common import (DEV, TOL, check_fwd, check_grads, max_abs, rel_l2, say, tdtype,
+                        to_dev, to_np)
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(H, N, d, nb, seed, dt, hi=None, table_std=0.5, qkv_std=None, neg_inf=False):
+    g = np.random.default_rng(seed)
+    qkv_std = (1.0 / math.sqrt(d)) if qkv_std is None else qkv_std
+    q, k, v = (g.standard_normal((H, N, d)).astype(np.float32) * np.float32(qkv_std) for _ in range(3))
+    do = g.standard_normal((H, N, d)).astype(np.float32)
+    if dt == "bf16":
+        q, k, v, do = (synth.round_bf16(x) for x in (q, k, v, do))
+    table = (g.standard_normal((H, nb)) * table_std).astype(np.float32)
+    if neg_inf:
+        table[:, : max(1, nb // 3)] = -np.inf
+    spd = g.integers(0, hi if hi is not None else nb, size=(N, N)).astype(np.uint8)
+    return q, k, v, do, table, spd
+
+
+def _run_full(q, k, v, do, table, spd, dt, scale):
+    td = tdtype(dt)
+    Q, K, V, dO = (to_dev(x, td) for x in (q, k, v, do))
+    T = to_dev(table)
+    S = to_dev(spd, torch.uint8)
+    O, L = gt.gt_attn_fwd(Q, K, V, S, T, scale=scale)
+    dq, dk, dv, dtab = gt.gt_attn_bwd(Q, K, V, S, T, O, L, dO, scale=scale)
+    torch.cuda.synchronize()
+    return dict(o=to_np(O), lse=to_np(L), dq=to_np(dq), dk=to_np(dk), dv=to_np(dv),
+                dtable=to_np(dtab))
+
+
+def _oracle_full(q, k, v, do, table, spd, scale):
+    O, L = oracle.forward(q, k, v, spd, table, scale)
+    dq, dk, dv, dt = oracle.backward(q, k, v, spd, table, scale, do)
+    return dict(o=O, lse=L, dq=dq, dk=dk, dv=dv, dtable=dt)
+
+
+def test_tiny_workload_fp32():
+    """N=512, H=4, d=32 fp32, Erdos-Renyi spd clipped at 20: full oracle."""
+    w = synth.workload("tiny")
+    q, k, v = w.qkv(0)
+    do = w.d_out(0)
+    table = w.table(0)
+    spd = w.spd_block(0, w.N)
+    say("tiny fp32 N=512 H=4 d=32")
+    got = _run_full(q, k, v, do, table, spd, "f32", w.scale())
+    ref = _oracle_full(q, k, v, do, table, spd, w.scale())
+    check_fwd("tiny", got["o"], got["lse"], ref["o"], ref["lse"], "f32")
+    check_grads("tiny", got, ref, "f32")
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("N", [1, 7, 33, 100, 1000])
+def test_ragged_sizes(N, d, dt):
+    """Ragged N (not a tile multiple), asymmetric random spd with buckets past
+    the table (bias 0, no gradient)."""
+    H, nb = 2, 10
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=N * 7 + d, dt=dt, hi=nb + 4)
+    scale = 1.0 / math.sqrt(d)
+    say(f"ragged {dt} N={N} d={d}")
+    got = _run_full(q, k, v, do, table, spd, dt, scale)
+    ref = _oracle_full(q, k, v, do, table, spd, scale)
+    check_fwd(f"ragged N={N}", got["o"], got["lse"], ref["o"], ref["lse"], dt)
+    if N > 1:
+        check_grads(f"ragged N={N}", got, ref, dt)
+    else:
+        # N = 1: dV = dO and dQ = dK = dtable = 0 (P = 1, so dS = dP - Dlt = 0
+        # up to the rounding of O and LSE)
+        assert max_abs(got["dv"], do) <= TOL[dt]["o"]
+        for name in ("dq", "dk", "dtable"):
+            assert np.abs(got[name]).max() <= 1e-6, name
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_masked_rows_and_neg_inf_table(dt):
+    """-inf table entries; rows 0..9 only see -inf buckets: O = 0, LSE = -inf,
+    zero gradients from those rows, no NaN anywhere."""
+    H, N, d, nb = 2, 300, 64, 9
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=5, dt=dt, neg_inf=True)
+    spd[:10] = np.random.default_rng(6).integers(0, nb // 3, size=(10, N))
+    scale = 0.125
+    say(f"masked rows {dt}")
+    got = _run_full(q, k, v, do, table, spd, dt, scale)
+    ref = _oracle_full(q, k, v, do, table, spd, scale)
+    assert np.isneginf(got["lse"][:, :10]).all() and np.all(got["o"][:, :10] == 0)
+    check_fwd("masked", got["o"], got["lse"], ref["o"], ref["lse"], dt)
+    check_grads("masked", got, ref, dt)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("Sq,Sk,row_off,col_off,ld", [
+    (200, 300, 37, 91, 512),      # unaligned slice: byte loads
+    (256, 320, 64, 128, 512),     # 16-byte aligned slice: vector loads
+    (129, 1, 3, 500, 512),        # single key
+    (64, 77, 0, 0, 77),           # ld not a multiple of 16
+])
+def test_ring_step_offsets(Sq, Sk, row_off, col_off, ld, dt):
+    """One context-parallel step: bias slice spd[row_off + i, col_off + j] of an
+    asymmetric spd; partial O (fp32) and LSE against the oracle's ring step."""
+    H, d, nb = 3, 64, 12
+    g = np.random.default_rng(Sq + Sk)
+    rows = row_off + Sq
+    spd = g.integers(0, nb + 2, size=(rows, ld)).astype(np.uint8)
+    q = g.standard_normal((H, Sq, d)).astype(np.float32) * 0.125
+    k = g.standard_normal((H, Sk, d)).astype(np.float32) * 0.125
+    v = g.standard_normal((H, Sk, d)).astype(np.float32)
+    if dt == "bf16":
+        q, k, v = (synth.round_bf16(x) for x in (q, k, v))
+    table = (g.standard_normal((H, nb)) * 0.5).astype(np.float32)
+    td = tdtype(dt)
+    say(f"ring step {dt} Sq={Sq} Sk={Sk} row_off={row_off} col_off={col_off} ld={ld}")
+    o, l = gt.gt_attn_ring_step(to_dev(q, td), to_dev(k, td), to_dev(v, td),
+                                to_dev(spd, torch.uint8), row_off, col_off, to_dev(table),
+                                scale=0.125)
+    torch.cuda.synchronize()
+    o_ref, l_ref = oracle.ring_step(q, k, v, spd, row_off, col_off, table, 0.125)
+    check_fwd("ring", to_np(o), to_np(l), o_ref, l_ref, dt)
+
+
+def test_ring_step_empty_kv_block():
+    """Sk = 0: the partial is O = 0, LSE = -inf (null K/V/spd allowed)."""
+    q = torch.randn(2, 70, 32, device=DEV).to(torch.bfloat16)
+    t = torch.randn(2, 5, device=DEV)
+    o, l = gt.gt_attn_ring_step(q, None, None, None, 0, 0, t)
+    torch.cuda.synchronize()
+    assert torch.all(o == 0) and torch.all(torch.isneginf(l))
+
+
+@pytest.mark.parametrize("out", ["bf16", "f32"])
+@pytest.mark.parametrize("P", [1, 3, 8])
+def test_merge(P, out):
+    """Merge of partials against the oracle, with some -inf parts and a row
+    whose every part is -inf."""
+    H, S, d = 3, 333, 64
+    g = np.random.default_rng(P)
+    o = g.standard_normal((P, H, S, d)).astype(np.float32)
+    lse = (g.standard_normal((P, H, S)) * 3).astype(np.float32)
+    lse[0, :, ::7] = -np.inf
+    lse[:, 0, 5] = -np.inf
+    say(f"merge P={P} out={out}")
+    O, L = gt.gt_attn_merge(to_dev(o), to_dev(lse), dtype=tdtype(out))
+    torch.cuda.synchronize()
+    O_ref, L_ref = oracle.merge(o, lse)
+    tol = TOL["bf16" if out == "bf16" else "f32"]["o"]
+    assert max_abs(to_np(O), O_ref) <= tol
+    assert max_abs(to_np(L), L_ref) <= 1e-5
+    assert np.isneginf(to_np(L)[0, 5]) and np.all(to_np(O)[0, 5] == 0)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_context_parallel_ring_small(dt):
+    """P = 4 uneven shards of N = 1000: every rank runs its ring steps on its
+    own spd row shard (row_off = 0, col_off = the block's first node), then
+    merges; the result equals the unsharded oracle forward."""
+    H, N, d, nb = 2, 1000, 64, 16
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=11, dt=dt)
+    bounds = [0, 240, 500, 777, 1000]
+    td = tdtype(dt)
+    Q, K, V, T = to_dev(q, td), to_dev(k, td), to_dev(v, td), to_dev(table)
+    O_ref, L_ref = oracle.forward(q, k, v, spd, table, 0.125)
+    P = len(bounds) - 1
+    for r in range(P):
+        r0, r1 = bounds[r], bounds[r + 1]
+        shard = to_dev(spd[r0:r1], torch.uint8)
+        parts_o, parts_l = [], []
+        for t in range(P):
+            b = (r - t) % P
+            c0, c1 = bounds[b], bounds[b + 1]
+            o_p, l_p = gt.gt_attn_ring_step(Q[:, r0:r1].contiguous(), K[:, c0:c1].contiguous(),
+                                            V[:, c0:c1].contiguous(), shard, 0, c0, T, scale=0.125)
+            parts_o.append(o_p)
+            parts_l.append(l_p)
+        O, L = gt.gt_attn_merge(torch.stack(parts_o), torch.stack(parts_l), dtype=td)
+        torch.cuda.synchronize()
+        say(f"cp small {dt} rank {r}")
+        check_fwd(f"cp rank {r}", to_np(O), to_np(L), O_ref[:, r0:r1], L_ref[:, r0:r1], dt)
+
+
+def test_forward_is_deterministic():
+    H, N, d, nb = 4, 777, 64, 20
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=21, dt="bf16")
+    Q, K, V = (to_dev(x, torch.bfloat16) for x in (q, k, v))
+    S, T = to_dev(spd, torch.uint8), to_dev(table)
+    O1, L1 = gt.gt_attn_fwd(Q, K, V, S, T)
+    O2, L2 = gt.gt_attn_fwd(Q, K, V, S, T)
+    torch.cuda.synchronize()
+    assert torch.equal(O1, O2) and torch.equal(L1, L2)
+
+
+def test_gradient_invariants_bf16():
+    """sum_b dtable = 0, sum_j dK_j = 0, sum_j dV_j = sum_i dO_i (GPU, no oracle)."""
+    H, N, d, nb = 2, 2048, 64, 32
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=31, dt="bf16")
+    got = _run_full(q, k, v, do, table, spd, "bf16", 0.125)
+    scale_dt = np.abs(got["dtable"]).max()
+    assert np.abs(got["dtable"].sum(1)).max() <= 1e-2 * scale_dt + 1e-4
+    assert rel_l2(got["dk"].sum(1), np.zeros((H, d))) <= 1e-2 * np.linalg.norm(got["dk"])
+    assert rel_l2(got["dv"].sum(1), do.sum(1)) <= 1e-2
