@@ -89,6 +89,24 @@ gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v,
                         int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
                         float scale, void* stream);
 
+/* The backward split into its three stages, for callers that schedule them
+ * (e.g. the two independent stages on two streams) or time them:
+ *   phase 0  prepare: rowsum(dO * O) and LSE * log2(e) into the workspace;
+ *            dtable = 0
+ *   phase 1  dK, dV and dtable (needs phase 0)
+ *   phase 2  dQ (needs phase 0; independent of phase 1)
+ * Arguments and results are exactly those of gt_attn_bwd; running phases
+ * 0, 1, 2 on one stream is gt_attn_bwd. Outputs a phase does not produce
+ * are not touched. phase outside 0..2 gives GT_ERR_INVALID. */
+gt_status_t gt_attn_bwd_phase(int32_t phase,
+                              const void* q, const void* k, const void* v,
+                              const uint8_t* spd, const float* table, int32_t n_buckets,
+                              const void* o, const float* lse, const void* d_o,
+                              void* dq, void* dk, void* dv, float* dtable,
+                              void* workspace, size_t workspace_bytes,
+                              int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
+                              float scale, void* stream);
+
 /* One step of graph-aware context parallelism (Section III-A-1: ring-based
  * KV rotation, query-dimension bias sharding, Eq. (2)). A rank holding the
  * query shard q_shard and, at this step, one KV block computes the block's

@@ -19,7 +19,7 @@ from pathlib import Path
 
 import torch
 
-__all__ = ["gt_attn_fwd", "gt_attn_bwd", "gt_attn_ring_step", "gt_attn_merge",
+__all__ = ["gt_attn_fwd", "gt_attn_bwd", "gt_attn_bwd_phase", "gt_attn_ring_step", "gt_attn_merge",
            "gt_attn_bwd_workspace_size", "gt_status_string", "gt_attn_version",
            "GTError", "lib", "LIB_PATH"]
 
@@ -58,6 +58,8 @@ def lib() -> ctypes.CDLL:
         L.gt_attn_bwd.restype = _I32
         L.gt_attn_bwd.argtypes = [_P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _P, _P, _P, _P,
                                   ctypes.c_size_t, _I32, _I64, _I32, _I32, _F, _P]
+        L.gt_attn_bwd_phase.restype = _I32
+        L.gt_attn_bwd_phase.argtypes = [_I32] + L.gt_attn_bwd.argtypes
         L.gt_attn_ring_step.restype = _I32
         L.gt_attn_ring_step.argtypes = [_P, _I64, _P, _P, _I64, _P, _I64, _I64, _I64, _P, _I32,
                                         _P, _P, _I32, _I32, _I32, _F, _P]
@@ -142,6 +144,13 @@ def gt_attn_bwd(q, k, v, spd, table, o, lse, d_o, scale: float | None = None,
     """dQ, dK, dV, dTable (C ABI gt_attn_bwd). `grads` may hold preallocated
     (dq, dk, dv, dtable); `workspace` a uint8 device tensor of at least
     gt_attn_bwd_workspace_size bytes."""
+    return gt_attn_bwd_phase(-1, q, k, v, spd, table, o, lse, d_o, scale, workspace, grads, stream)
+
+
+def gt_attn_bwd_phase(phase: int, q, k, v, spd, table, o, lse, d_o, scale: float | None = None,
+                      workspace=None, grads=None, stream=None):
+    """One stage of the backward (C ABI gt_attn_bwd_phase): 0 prepare,
+    1 dK/dV/dtable, 2 dQ; phase -1 runs gt_attn_bwd (all three)."""
     H, N, d = q.shape
     _dev_contig(q, k, v, spd, table, o, lse, d_o)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
@@ -153,11 +162,14 @@ def gt_attn_bwd(q, k, v, spd, table, o, lse, d_o, scale: float | None = None,
     need = gt_attn_bwd_workspace_size(H, N, d, q.dtype)
     if workspace is None:
         workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
-    st = lib().gt_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(spd), _ptr(table), table.shape[1],
-                           _ptr(o), _ptr(lse), _ptr(d_o), _ptr(dq), _ptr(dk), _ptr(dv),
-                           _ptr(dtable), _ptr(workspace), workspace.numel() * workspace.element_size(),
-                           H, N, d, _dt(q), scale, _stream(stream))
-    _check(st, "gt_attn_bwd")
+    args = (_ptr(q), _ptr(k), _ptr(v), _ptr(spd), _ptr(table), table.shape[1],
+            _ptr(o), _ptr(lse), _ptr(d_o), _ptr(dq), _ptr(dk), _ptr(dv),
+            _ptr(dtable), _ptr(workspace), workspace.numel() * workspace.element_size(),
+            H, N, d, _dt(q), scale, _stream(stream))
+    if phase == -1:
+        _check(lib().gt_attn_bwd(*args), "gt_attn_bwd")
+    else:
+        _check(lib().gt_attn_bwd_phase(int(phase), *args), "gt_attn_bwd_phase")
     return dq, dk, dv, dtable
 
 

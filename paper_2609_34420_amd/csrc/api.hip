@@ -10,6 +10,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int64_t kMaxGrid = 0x7fffffffLL;
+constexpr int64_t kMaxLd = 1LL << 25;   // spd row stride: 32-bit buffer offsets
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -60,6 +61,7 @@ gt_status_t gt_attn_ring_step(const void* q_shard, int64_t Sq, const void* k_sha
   if (!q_shard || !table || !o_part || !lse_part) return GT_ERR_INVALID;
   if (Sk > 0 && (!k_shard || !v_shard || !spd)) return GT_ERR_INVALID;
   if (Sk > 0 && ld_spd < col_off + Sk) return GT_ERR_INVALID;
+  if (Sk > 0 && ld_spd > kMaxLd) return GT_ERR_UNSUPPORTED;
   if (!aligned16(q_shard) || !aligned16(o_part) || (Sk > 0 && (!aligned16(k_shard) || !aligned16(v_shard))))
     return GT_ERR_INVALID;
   if ((Sq + 127) / 128 * (int64_t)H > kMaxGrid) return GT_ERR_INVALID;
@@ -83,6 +85,7 @@ gt_status_t gt_attn_fwd(const void* q, const void* k, const void* v, const uint8
   if (!q || !k || !v || !spd || !table || !o || !lse) return GT_ERR_INVALID;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return GT_ERR_INVALID;
   if ((N + 127) / 128 * (int64_t)H > kMaxGrid) return GT_ERR_INVALID;
+  if (N > kMaxLd) return GT_ERR_UNSUPPORTED;
   gt::FwdArgs a{};
   a.q = q; a.k = k; a.v = v;
   a.spd = spd; a.ld_spd = N; a.row_off = 0; a.col_off = 0;
@@ -98,14 +101,16 @@ size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dt
   (void)dtype;
   if (H < 1 || N < 1) return 0;
   const size_t rows = (size_t)H * (size_t)N;
-  return 2 * align_up(rows * sizeof(float));
+  const size_t nblk = (size_t)((N + 255) / 256);
+  return 2 * align_up(rows * sizeof(float)) + align_up((size_t)H * nblk * 2 * sizeof(float));
 }
 
-gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v, const uint8_t* spd,
-                        const float* table, int32_t n_buckets, const void* o,
-                        const float* lse, const void* d_o, void* dq, void* dk, void* dv,
-                        float* dtable, void* workspace, size_t workspace_bytes, int32_t H,
-                        int64_t N, int32_t d, gt_dtype_t dtype, float scale, void* stream) {
+static gt_status_t bwd_impl(int32_t phase, const void* q, const void* k, const void* v,
+                            const uint8_t* spd, const float* table, int32_t n_buckets,
+                            const void* o, const float* lse, const void* d_o, void* dq,
+                            void* dk, void* dv, float* dtable, void* workspace,
+                            size_t workspace_bytes, int32_t H, int64_t N, int32_t d,
+                            gt_dtype_t dtype, float scale, void* stream) {
   if (!dtype_ok(dtype)) return GT_ERR_UNSUPPORTED;
   if (!dims_ok(d)) return GT_ERR_UNSUPPORTED;
   if (H < 1 || N < 1 || n_buckets < 1 || n_buckets > 256 || !scale_ok(scale)) return GT_ERR_INVALID;
@@ -115,6 +120,7 @@ gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v, const uint8
       !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
     return GT_ERR_INVALID;
   if ((N + 127) / 128 * (int64_t)H > kMaxGrid) return GT_ERR_INVALID;
+  if (N > kMaxLd) return GT_ERR_UNSUPPORTED;
   const size_t need = gt_attn_bwd_workspace_size(H, N, d, dtype);
   if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
     return GT_ERR_WORKSPACE;
@@ -127,9 +133,30 @@ gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v, const uint8
   a.dq = dq; a.dk = dk; a.dv = dv; a.dtable = dtable;
   a.lse2 = static_cast<float*>(workspace);
   a.dlt = reinterpret_cast<float*>(static_cast<char*>(workspace) + align_up(rows * sizeof(float)));
+  a.nmax = reinterpret_cast<float*>(static_cast<char*>(workspace) + 2 * align_up(rows * sizeof(float)));
   a.H = H; a.N = N; a.scale = scale;
   a.spd_vec = spd_vec(spd, N, 0, 0);
-  return launched(gt::launch_bwd(a, d, dtype == GT_BF16, static_cast<hipStream_t>(stream)));
+  return launched(gt::launch_bwd(a, d, dtype == GT_BF16, phase, static_cast<hipStream_t>(stream)));
+}
+
+gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v, const uint8_t* spd,
+                        const float* table, int32_t n_buckets, const void* o,
+                        const float* lse, const void* d_o, void* dq, void* dk, void* dv,
+                        float* dtable, void* workspace, size_t workspace_bytes, int32_t H,
+                        int64_t N, int32_t d, gt_dtype_t dtype, float scale, void* stream) {
+  return bwd_impl(-1, q, k, v, spd, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
+                  workspace, workspace_bytes, H, N, d, dtype, scale, stream);
+}
+
+gt_status_t gt_attn_bwd_phase(int32_t phase, const void* q, const void* k, const void* v,
+                              const uint8_t* spd, const float* table, int32_t n_buckets,
+                              const void* o, const float* lse, const void* d_o, void* dq,
+                              void* dk, void* dv, float* dtable, void* workspace,
+                              size_t workspace_bytes, int32_t H, int64_t N, int32_t d,
+                              gt_dtype_t dtype, float scale, void* stream) {
+  if (phase < 0 || phase > 2) return GT_ERR_INVALID;
+  return bwd_impl(phase, q, k, v, spd, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
+                  workspace, workspace_bytes, H, N, d, dtype, scale, stream);
 }
 
 gt_status_t gt_attn_merge(const float* o_parts, const float* lse_parts, int32_t n_parts,

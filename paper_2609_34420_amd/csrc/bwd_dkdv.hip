@@ -1,0 +1,406 @@
+// Backward, key-stationary stage: dK, dV and the bias-table gradient (bf16).
+//
+// Each wave owns 32 keys (lane & 31 = key) and streams every query through
+// S = Q K^T with the queries on the MFMA rows, so the lane's registers hold
+// P and dS for its key and 16 consecutive queries (lane half g: queries
+// 16 g + r). Those registers are directly the B operands of
+//   dV^T += dO^T P   and   dK^T += Q^T dS,
+// with dO^T and Q^T read from LDS. The softmax statistics enter through the
+// matrix-core accumulators: S starts from -LSE log2(e) / (scale log2(e)) and
+// dP from -Dlt, so per score element the vector work is one FMA with the
+// bias, one exp2, one multiply and the two bf16 conversions.
+//
+// Bias and table gradient: the table (times log2 e) is replicated 16 times
+// in LDS (copy = lane & 15) and the bucket histogram has the same layout, so
+// one address register serves the bias read and the gradient add. The
+// histogram is fixed point: LDS float atomics are slow on this hardware,
+// 64-bit integer adds are not. dS is accumulated as round(dS * 2^F), where
+// the power-of-two scale per head keeps every term below 2^30 in magnitude:
+// |dS_ij| <= |dO_i . V_j - Dlt_i| <= 2 |dO_i| max_j |V_j| (Cauchy-Schwarz,
+// with O_i a convex combination of the V_j), and the prepare stage records
+// block maxima of |dO_i| and |V_j|. The scale enters for free through the
+// V operand of dP (and the dP accumulator start), so dS arrives already
+// scaled; dK takes 2^-F in its final multiply. Sums of up to 2^32 terms fit
+// in 64 bits. The histogram is flushed once per workgroup, converted back
+// to fp32, with one global atomic per bucket.
+//
+// Query tiles (Q, dO in both layouts, statistics) are double buffered in
+// LDS: the next tile's global loads are in flight while the current one is
+// computed, one barrier per tile. spd bytes are fetched one 32-query
+// sub-block ahead of their use.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace gt {
+
+namespace {
+
+constexpr int kNW = 8;              // waves per workgroup
+constexpr int kBK = kNW * 32;       // keys per workgroup
+constexpr int kBQ = 64;             // queries per staged tile
+constexpr int kThreads = kNW * 64;
+constexpr int kCopies = 16;                 // table / histogram copies (lane & 15)
+constexpr int kTabEntries = 256 * kCopies;
+
+template <int D>
+struct DkdvSmem {
+  uint16_t q[2][kBQ * D];
+  uint16_t o[2][kBQ * D];
+  uint16_t qt[2][D * kBQ];
+  uint16_t ot[2][D * kBQ];
+  float init_s[2][kBQ];             // -LSE log2 e / (scale log2 e); -inf for empty rows
+  float init_p[2][kBQ];             // -Dlt
+};
+
+struct StageRegs {
+  uint4 v0, v1;
+  float stat;
+};
+
+// Global -> registers for the query tile at i0. Rows past N read the clamped
+// row N-1 (unconditional loads); stage_store() zeroes them.
+template <int D, bool QFULL>
+__device__ __forceinline__ void stage_load(const BwdArgs& a, const uint16_t* qh, const uint16_t* oh,
+                                           const float* lse2h, const float* dlth, int64_t i0,
+                                           StageRegs& r) {
+  constexpr int CPR = D / 8;
+  constexpr int ITEMS = 32 * CPR;   // row pairs x 16-byte chunks, per tensor
+  const int t = threadIdx.x;
+  if (t < 2 * ITEMS) {
+    const int u = t % ITEMS;
+    const int ip = u % 32, cc = u / 32;
+    const uint16_t* src = (t < ITEMS) ? qh : oh;
+    const int64_t row = i0 + 2 * ip;
+    const int64_t r0 = (QFULL || row < a.N) ? row : a.N - 1;
+    const int64_t r1 = (QFULL || row + 1 < a.N) ? row + 1 : a.N - 1;
+    r.v0 = *reinterpret_cast<const uint4*>(src + r0 * D + cc * 8);
+    r.v1 = *reinterpret_cast<const uint4*>(src + r1 * D + cc * 8);
+  }
+  if (t < 2 * kBQ) {
+    const int64_t i = i0 + (t & (kBQ - 1));
+    const int64_t ic = (QFULL || i < a.N) ? i : a.N - 1;
+    r.stat = (t < kBQ) ? lse2h[ic] : dlth[ic];
+  }
+}
+
+// Registers -> LDS buffer `buf`: Q and dO row-major and transposed, and the
+// accumulator starts of S (-lse2 / (scale log2 e), -inf for padded rows so
+// that P = 0) and of the scaled dP (-Dlt 2^F).
+template <int D, bool QFULL>
+__device__ __forceinline__ void stage_store(DkdvSmem<D>& sm, int buf, StageRegs r, int64_t i0,
+                                            int64_t n, float inv_sl2, float sF) {
+  constexpr int CPR = D / 8;
+  constexpr int ITEMS = 32 * CPR;
+  const int t = threadIdx.x;
+  const bool tail = !QFULL && i0 + kBQ > n;
+  if (t < 2 * ITEMS) {
+    const int u = t % ITEMS;
+    const int ip = u % 32, cc = u / 32;
+    uint16_t* rm = (t < ITEMS) ? sm.q[buf] : sm.o[buf];
+    uint16_t* tr = (t < ITEMS) ? sm.qt[buf] : sm.ot[buf];
+    const int row = 2 * ip;
+    if (tail) {
+      if (i0 + row >= n) r.v0 = make_uint4(0, 0, 0, 0);
+      if (i0 + row + 1 >= n) r.v1 = make_uint4(0, 0, 0, 0);
+    }
+    *reinterpret_cast<uint4*>(rm + row * D + swz_rows<D>(row, cc) * 8) = r.v0;
+    *reinterpret_cast<uint4*>(rm + (row + 1) * D + swz_rows<D>(row + 1, cc) * 8) = r.v1;
+    const uint16_t* p0 = reinterpret_cast<const uint16_t*>(&r.v0);
+    const uint16_t* p1 = reinterpret_cast<const uint16_t*>(&r.v1);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int crow = cc * 8 + e;
+      *reinterpret_cast<uint32_t*>(tr + crow * kBQ + swz_t64(crow, row >> 3) * 8 + (row & 7)) =
+          (uint32_t)p0[e] | ((uint32_t)p1[e] << 16);
+    }
+  }
+  if (t < 2 * kBQ) {
+    const int q = t & (kBQ - 1);
+    const bool in = QFULL || i0 + q < n;
+    if (t < kBQ)
+      sm.init_s[buf][q] = in ? -r.stat * inv_sl2 : -INFINITY;
+    else
+      sm.init_p[buf][q] = in ? -r.stat * sF : 0.0f;
+  }
+}
+
+// spd bytes of this lane's key for the 16 queries i_base + 16 g + r, by raw
+// buffer loads: a scalar base per sub-block, scalar row offsets r * ld and a
+// per-lane offset 16 g ld + key. QFULL (N a multiple of the query tile): every
+// row exists. Otherwise rows past n read the clamped row n-1 (their P is 0,
+// any bucket will do), branch-free.
+template <bool QFULL>
+__device__ __forceinline__ void load_bytes(const uint8_t* spd_cols, int64_t ld, int64_t i_base,
+                                           int64_t n, uint32_t key_off, uint32_t b[16]) {
+  const int g = (threadIdx.x >> 5) & 1;
+  if constexpr (QFULL) {
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(spd_cols + i_base * ld);
+    const uint32_t voff = (uint32_t)(16 * g) * (uint32_t)ld + key_off;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) b[r] = buf_u8(rs, voff, (uint32_t)(r * ld));
+  } else {
+    // base at the clamped first row, so every offset below is >= 0
+    const int64_t ib = i_base < n ? i_base : n - 1;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(spd_cols + ib * ld);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      int64_t row = i_base + 16 * g + r;
+      row = row < n ? row : n - 1;
+      b[r] = buf_u8(rs, (uint32_t)((row - ib) * ld) + key_off, 0u);
+    }
+  }
+}
+
+__device__ __forceinline__ int round_to_int(float x) {
+  int r;
+  asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(r) : "v"(x));   // floor(x + 0.5)
+  return r;
+}
+
+template <int D, bool KTAIL>
+__device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const uint2* tabw,
+                                              unsigned long long* hist, int buf, int qs,
+                                              const bf16x8* kf, const bf16x8* vf,
+                                              const uint32_t* b, float sl2, bool jok,
+                                              f32x16* dk, f32x16* dv) {
+  constexpr int NKC = D / 16;
+  constexpr int NCB = D / 32;
+  const int lane = threadIdx.x & 63;
+  const int col = lane & 31, g = lane >> 5;
+  const int ib = qs * 32 + 16 * g;   // this lane half's first query in the tile
+
+  f32x16 s, dp;
+  {
+    const float4* is4 = reinterpret_cast<const float4*>(&sm.init_s[buf][ib]);
+    const float4* ip4 = reinterpret_cast<const float4*>(&sm.init_p[buf][ib]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float4 x = is4[u], y = ip4[u];
+      s[4 * u] = x.x; s[4 * u + 1] = x.y; s[4 * u + 2] = x.z; s[4 * u + 3] = x.w;
+      dp[4 * u] = y.x; dp[4 * u + 1] = y.y; dp[4 * u + 2] = y.z; dp[4 * u + 3] = y.w;
+    }
+  }
+  const int qrow = qs * 32 + perm32(col);
+#pragma unroll
+  for (int kc = 0; kc < NKC; ++kc) {
+    const int off = qrow * D + swz_rows<D>(qrow, kc * 2 + g) * 8;
+    s = mfma32(lds_b128(sm.q[buf] + off), kf[kc], s);
+    dp = mfma32(lds_b128(sm.o[buf] + off), vf[kc], dp);
+  }
+  // Lane: key; registers r: queries. dp holds (dO.V - Dlt) 2^F, so ds below
+  // is dS 2^F.
+  float p[16], ds[16];
+  uint32_t idx[16];
+  float tb[16];
+  const uint32_t cpy = (uint32_t)(lane & (kCopies - 1));
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    idx[r] = (b[r] << 4) | cpy;                    // copy cpy of bucket b
+    tb[r] = __uint_as_float(tabw[idx[r]].x);
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const float x = fmaf(s[r], sl2, tb[r]);
+    float pv = exp2_fast(x);
+    if constexpr (KTAIL) pv = jok ? pv : 0.0f;
+    p[r] = pv;
+    ds[r] = pv * dp[r];
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r)
+    atomicAdd(&hist[idx[r]], (unsigned long long)(long long)round_to_int(ds[r]));
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const bf16x8 pb = cvt_bf16x8(p + 8 * q);
+    const bf16x8 db = cvt_bf16x8(ds + 8 * q);
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const int crow = cb * 32 + col;
+      const int off = crow * kBQ + swz_t64(crow, (ib >> 3) + q) * 8;
+      dv[cb] = mfma32(lds_b128(sm.ot[buf] + off), pb, dv[cb]);
+      dk[cb] = mfma32(lds_b128(sm.qt[buf] + off), db, dk[cb]);
+    }
+  }
+}
+
+template <int D, bool KTAIL, bool QFULL>
+__device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, const uint2* tabw,
+                                          unsigned long long* hist, int h, int64_t key0, int64_t j,
+                                          bool jok, int fexp) {
+  constexpr int NKC = D / 16;
+  constexpr int NCB = D / 32;
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 5;
+  const int64_t hoff = (int64_t)h * a.N * D;
+  const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + hoff;
+  const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + hoff;
+  const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + hoff;
+  const uint16_t* oh = reinterpret_cast<const uint16_t*>(a.d_o) + hoff;
+  const float* lse2h = a.lse2 + (int64_t)h * a.N;
+  const float* dlth = a.dlt + (int64_t)h * a.N;
+  const float sl2 = a.scale * kLog2e;
+  const float inv_sl2 = 1.0f / sl2;
+
+  const float sF = ldexpf(1.0f, fexp);
+
+  // K and 2^F V of this lane's key as B operands (rows past N: zero); the
+  // power-of-two scale is exact in bf16.
+  bf16x8 kf[NKC], vf[NKC];
+#pragma unroll
+  for (int kc = 0; kc < NKC; ++kc) {
+    kf[kc] = jok ? *reinterpret_cast<const bf16x8*>(kh + j * D + kc * 16 + g * 8) : zero_bf16x8();
+    const bf16x8 v8 = jok ? *reinterpret_cast<const bf16x8*>(vh + j * D + kc * 16 + g * 8) : zero_bf16x8();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) vf[kc][e] = (__bf16)((float)v8[e] * sF);
+  }
+  f32x16 dk[NCB], dv[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    dk[cb] = zero_f32x16();
+    dv[cb] = zero_f32x16();
+  }
+
+  const int64_t ld = a.ld_spd;
+  const int64_t jc = jok ? j : a.N - 1;
+  const uint32_t key_off = (uint32_t)(jc - key0);
+  const uint8_t* spd_cols = a.spd + key0;
+  const int64_t ntiles = (a.N + kBQ - 1) / kBQ;
+
+  StageRegs st;
+  stage_load<D, QFULL>(a, qh, oh, lse2h, dlth, 0, st);
+  uint32_t bA[16], bB[16];
+  load_bytes<QFULL>(spd_cols, ld, 0, a.N, key_off, bA);
+  stage_store<D, QFULL>(sm, 0, st, 0, a.N, inv_sl2, sF);
+  __syncthreads();
+
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int buf = (int)(t & 1);
+    const int64_t i0 = t * kBQ;
+    const bool more = t + 1 < ntiles;
+    load_bytes<QFULL>(spd_cols, ld, i0 + 32, a.N, key_off, bB);
+    if (more) stage_load<D, QFULL>(a, qh, oh, lse2h, dlth, i0 + kBQ, st);
+    dkdv_subblock<D, KTAIL>(sm, tabw, hist, buf, 0, kf, vf, bA, sl2, jok, dk, dv);
+    if (more) load_bytes<QFULL>(spd_cols, ld, i0 + kBQ, a.N, key_off, bA);
+    dkdv_subblock<D, KTAIL>(sm, tabw, hist, buf, 1, kf, vf, bB, sl2, jok, dk, dv);
+    if (more) stage_store<D, QFULL>(sm, buf ^ 1, st, i0 + kBQ, a.N, inv_sl2, sF);
+    __syncthreads();
+  }
+
+  const float dk_scale = a.scale * ldexpf(1.0f, -fexp);
+  if (jok) {
+    uint16_t* dkp = reinterpret_cast<uint16_t*>(a.dk) + hoff + j * D;
+    uint16_t* dvp = reinterpret_cast<uint16_t*>(a.dv) + hoff + j * D;
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = cb * 32 + 8 * u + 4 * g;
+        uint2 pk, pv;
+        pk.x = (uint32_t)f2bf(dk[cb][4 * u] * dk_scale) | ((uint32_t)f2bf(dk[cb][4 * u + 1] * dk_scale) << 16);
+        pk.y = (uint32_t)f2bf(dk[cb][4 * u + 2] * dk_scale) | ((uint32_t)f2bf(dk[cb][4 * u + 3] * dk_scale) << 16);
+        pv.x = (uint32_t)f2bf(dv[cb][4 * u]) | ((uint32_t)f2bf(dv[cb][4 * u + 1]) << 16);
+        pv.y = (uint32_t)f2bf(dv[cb][4 * u + 2]) | ((uint32_t)f2bf(dv[cb][4 * u + 3]) << 16);
+        *reinterpret_cast<uint2*>(dkp + c) = pk;
+        *reinterpret_cast<uint2*>(dvp + c) = pv;
+      }
+    }
+  }
+}
+
+template <int D, bool QFULL>
+__global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
+  __shared__ __attribute__((aligned(16))) DkdvSmem<D> sm;
+  // Table copies (fp32 bits, 8-byte stride) and histogram copies (int64) in
+  // separate arrays with the same index: the bias reads never alias the
+  // gradient adds and share one address register.
+  __shared__ uint2 tabw[kTabEntries];
+  __shared__ unsigned long long hist[kTabEntries];
+  __shared__ float red[2][kNW];
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, col = tid & 31;
+  const int64_t nkb = (a.N + kBK - 1) / kBK;
+  const int64_t lid = xcd_remap(blockIdx.x, nkb * a.H);
+  const int h = (int)(lid % a.H);
+  const int64_t kblk = lid / a.H;
+  const int64_t j = kblk * kBK + wave * 32 + col;
+  const bool jok = j < a.N;
+
+  for (int t = tid; t < kTabEntries; t += kThreads) {
+    const int bkt = t / kCopies;
+    const float tv = (bkt < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + bkt] * kLog2e : 0.0f;
+    tabw[t] = make_uint2(__float_as_uint(tv), 0u);
+    hist[t] = 0ull;
+  }
+
+  // Fixed-point exponent F of this head: 2 max|dO| max|V| 2^F <= 2^30
+  // (a 1.5 % margin covers the bf16 rounding of O and of the products).
+  {
+    const int64_t nblk = (a.N + 255) / 256;
+    const float* nm = a.nmax + (int64_t)h * nblk * 2;
+    float md = 0.0f, mv = 0.0f;
+    for (int64_t t = tid; t < nblk; t += kThreads) {
+      md = fmaxf(md, nm[2 * t]);
+      mv = fmaxf(mv, nm[2 * t + 1]);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      md = fmaxf(md, __shfl_xor(md, off));
+      mv = fmaxf(mv, __shfl_xor(mv, off));
+    }
+    if ((tid & 63) == 0) {
+      red[0][wave] = md;
+      red[1][wave] = mv;
+    }
+  }
+  __syncthreads();
+  float md = red[0][0], mv = red[1][0];
+#pragma unroll
+  for (int w = 1; w < kNW; ++w) {
+    md = fmaxf(md, red[0][w]);
+    mv = fmaxf(mv, red[1][w]);
+  }
+  const float bound = 2.03f * sqrtf(md) * sqrtf(mv);
+  int fexp = 40;
+  if (bound > 0.0f && bound < INFINITY) {
+    int e;
+    frexpf(bound, &e);                 // bound < 2^e
+    fexp = 30 - e;
+    fexp = fexp > 40 ? 40 : (fexp < -100 ? -100 : fexp);
+  }
+
+  if ((kblk + 1) * kBK <= a.N)
+    dkdv_main<D, false, QFULL>(a, sm, tabw, hist, h, kblk * kBK, j, jok, fexp);
+  else
+    dkdv_main<D, true, QFULL>(a, sm, tabw, hist, h, kblk * kBK, j, jok, fexp);
+
+  __syncthreads();
+  const double unscale = ldexp(1.0, -fexp);
+  for (int bkt = tid; bkt < a.n_buckets; bkt += kThreads) {
+    long long t = 0;
+#pragma unroll
+    for (int c = 0; c < kCopies; ++c) t += (long long)hist[bkt * kCopies + ((c + bkt) & (kCopies - 1))];
+    if (t != 0) atomicAdd(&a.dtable[(int64_t)h * a.n_buckets + bkt], (float)((double)t * unscale));
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s) {
+  const int64_t nkb = (a.N + kBK - 1) / kBK;
+  const dim3 grid((unsigned)(nkb * a.H));
+  const bool qfull = a.N % kBQ == 0;
+  if (d == 64) {
+    if (qfull)
+      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<64, true>), grid, dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<64, false>), grid, dim3(kThreads), 0, s, a);
+  } else {
+    if (qfull)
+      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<32, true>), grid, dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<32, false>), grid, dim3(kThreads), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace gt

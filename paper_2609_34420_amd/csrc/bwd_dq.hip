@@ -1,0 +1,228 @@
+// Backward, query-stationary stage: dQ (bf16).
+//
+// Same layout as the forward: each wave owns 32*QB queries, computes
+// S^T = K Q^T and dP^T = V dO^T with the queries on the lanes, forms
+// dS^T = P^T * (dP^T - Dlt) from the saved log-sum-exp, and accumulates
+// dQ^T += K^T dS^T with dS^T straight from registers. K (row-major and
+// transposed) and V tiles are double buffered in LDS and the next tile's
+// global loads and spd bytes are in flight while the current one computes.
+#include "common.hpp"
+#include "kernels.hpp"
+#include "tiles.hpp"
+
+namespace gt {
+
+namespace {
+
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * 64;
+constexpr int kBC = 64;
+
+template <int D, int QB, bool MASK>
+__device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sKt, const uint16_t* sV,
+                                        const float* sT, const bf16x8 (&qf)[QB][D / 16],
+                                        const bf16x8 (&df)[QB][D / 16], const float (&lse2)[QB],
+                                        const float (&dlt)[QB], const uint32_t (&w)[QB][kBC / 32][4],
+                                        int64_t j0, int64_t nk, float sl2,
+                                        f32x16 (&acc)[QB][D / 32]) {
+  constexpr int KB = kBC / 32;
+  constexpr int NKC = D / 16;
+  constexpr int NCB = D / 32;
+  const int lane = threadIdx.x & 63;
+  const int col = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      f32x16 s = zero_f32x16(), dp = zero_f32x16();
+      const int krow = kb * 32 + perm32(col);
+#pragma unroll
+      for (int kc = 0; kc < NKC; ++kc) {
+        const int off = krow * D + swz_rows<D>(krow, kc * 2 + g) * 8;
+        s = mfma32(lds_b128(sK + off), qf[qb][kc], s);
+        dp = mfma32(lds_b128(sV + off), df[qb][kc], dp);
+      }
+      float ds[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const uint32_t b = (w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu;
+        const float x = fmaf(s[r], sl2, sT[b]) - lse2[qb];
+        float pv = exp2_fast(x);
+        if constexpr (MASK) pv = (j0 + kb * 32 + 16 * g + r < nk) ? pv : 0.0f;
+        ds[r] = pv * (dp[r] - dlt[qb]);
+      }
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const bf16x8 db = cvt_bf16x8(ds + 8 * q);
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          const int crow = cb * 32 + col;
+          acc[qb][cb] = mfma32(lds_b128(sKt + crow * kBC + swz_t64(crow, kb * 4 + 2 * g + q) * 8), db,
+                               acc[qb][cb]);
+        }
+      }
+    }
+  }
+}
+
+// VEC: spd rows are 16-byte aligned. FULL: VEC and N a multiple of the key
+// tile, so every spd group is loaded whole and no tile needs masking.
+template <int D, int QB, bool VEC, bool FULL>
+__global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
+  constexpr int KB = kBC / 32;
+  constexpr int NKC = D / 16;
+  constexpr int NCB = D / 32;
+  constexpr int BR = kWaves * 32 * QB;
+  using Stager = KVStager<D, kThreads, true, true, true, false>;
+
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBC * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sKt[2][D * kBC];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][kBC * D];
+  __shared__ float sT[256];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 31, g = lane >> 5;
+
+  const int64_t nqb = (a.N + BR - 1) / BR;
+  const int64_t lid = xcd_remap(blockIdx.x, nqb * a.H);
+  const int h = (int)(lid % a.H);
+  const int64_t qblk = lid / a.H;
+  const int64_t qbase = qblk * BR + (int64_t)wave * 32 * QB;
+
+  for (int t = tid; t < 256; t += kThreads)
+    sT[t] = (t < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + t] * kLog2e : 0.0f;
+
+  const int64_t hoff = (int64_t)h * a.N * D;
+  const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + hoff;
+  const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + hoff;
+  const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + hoff;
+  const uint16_t* oh = reinterpret_cast<const uint16_t*>(a.d_o) + hoff;
+  const float sl2 = a.scale * kLog2e;
+
+  // Q^T, dO^T operands and statistics; rows past N load the clamped row N-1
+  // and get lse2 = +inf (P = 0); their dQ is not stored.
+  bf16x8 qf[QB][NKC], df[QB][NKC];
+  float lse2[QB], dlt[QB];
+  int64_t qrow[QB];
+  f32x16 acc[QB][NCB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int64_t i = qbase + qb * 32 + col;
+    qrow[qb] = i < a.N ? i : a.N - 1;
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      qf[qb][kc] = *reinterpret_cast<const bf16x8*>(qh + qrow[qb] * D + kc * 16 + g * 8);
+      df[qb][kc] = *reinterpret_cast<const bf16x8*>(oh + qrow[qb] * D + kc * 16 + g * 8);
+    }
+    const float l2 = a.lse2[(int64_t)h * a.N + qrow[qb]];
+    const float dl = a.dlt[(int64_t)h * a.N + qrow[qb]];
+    lse2[qb] = i < a.N ? l2 : INFINITY;
+    dlt[qb] = i < a.N ? dl : 0.0f;
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) acc[qb][cb] = zero_f32x16();
+  }
+
+  const int64_t ld = a.ld_spd;
+  const int64_t rb = qbase < a.N ? qbase : a.N - 1;
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.spd + rb * ld);
+  uint32_t voff[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) voff[qb] = (uint32_t)((qrow[qb] - rb) * ld) + 16u * g;
+  auto fetch_spd = [&](int64_t jt, uint32_t (&w)[QB][KB][4]) {
+    if (FULL || (VEC && jt + kBC <= a.N)) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) buf_u128(rs, voff[qb], (uint32_t)(jt + kb * 32), w[qb][kb]);
+    } else {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const uint8_t* row = a.spd + qrow[qb] * ld;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) load_spd16_bytes(row, jt + kb * 32 + 16 * g, a.N, w[qb][kb]);
+      }
+    }
+  };
+
+  const int64_t ntiles = (a.N + kBC - 1) / kBC;
+  Stager st;
+  uint32_t wc[QB][KB][4];
+  st.load(kh, vh, 0, a.N);
+  fetch_spd(0, wc);
+  if (kBC > a.N) st.mask_tail(0, a.N);
+  st.store(sK[0], sKt[0], sV[0], nullptr);
+  __syncthreads();
+
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int buf = (int)(t & 1);
+    const int64_t j0 = t * kBC;
+    const bool more = t + 1 < ntiles;
+    uint32_t wn[QB][KB][4];
+    if (more) {
+      st.load(kh, vh, j0 + kBC, a.N);
+      fetch_spd(j0 + kBC, wn);
+    }
+    if (FULL || j0 + kBC <= a.N)
+      dq_tile<D, QB, false>(sK[buf], sKt[buf], sV[buf], sT, qf, df, lse2, dlt, wc, j0, a.N, sl2, acc);
+    else
+      dq_tile<D, QB, true>(sK[buf], sKt[buf], sV[buf], sT, qf, df, lse2, dlt, wc, j0, a.N, sl2, acc);
+    if (more) {
+      if (!FULL && j0 + 2 * kBC > a.N) st.mask_tail(j0 + kBC, a.N);
+      st.store(sK[buf ^ 1], sKt[buf ^ 1], sV[buf ^ 1], nullptr);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) wc[qb][kb][e] = wn[qb][kb][e];
+    }
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int64_t i = qbase + qb * 32 + col;
+    if (i >= a.N) continue;
+    uint16_t* dqp = reinterpret_cast<uint16_t*>(a.dq) + hoff + i * D;
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = cb * 32 + 8 * u + 4 * g;
+        uint2 pk;
+        pk.x = (uint32_t)f2bf(acc[qb][cb][4 * u] * a.scale) | ((uint32_t)f2bf(acc[qb][cb][4 * u + 1] * a.scale) << 16);
+        pk.y = (uint32_t)f2bf(acc[qb][cb][4 * u + 2] * a.scale) | ((uint32_t)f2bf(acc[qb][cb][4 * u + 3] * a.scale) << 16);
+        *reinterpret_cast<uint2*>(dqp + c) = pk;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dq_bf16(const BwdArgs& a, int d, hipStream_t s) {
+  constexpr int QB = 1;
+  constexpr int BR = kWaves * 32 * QB;
+  const int64_t nqb = (a.N + BR - 1) / BR;
+  const dim3 grid((unsigned)(nqb * a.H));
+  const bool full = a.spd_vec && a.N % kBC == 0;
+  if (d == 64) {
+    if (full)
+      hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, QB, true, true>), grid, dim3(kThreads), 0, s, a);
+    else if (a.spd_vec)
+      hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, QB, true, false>), grid, dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, QB, false, false>), grid, dim3(kThreads), 0, s, a);
+  } else {
+    if (full)
+      hipLaunchKernelGGL((bwd_dq_bf16_kernel<32, QB, true, true>), grid, dim3(kThreads), 0, s, a);
+    else if (a.spd_vec)
+      hipLaunchKernelGGL((bwd_dq_bf16_kernel<32, QB, true, false>), grid, dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((bwd_dq_bf16_kernel<32, QB, false, false>), grid, dim3(kThreads), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace gt

@@ -91,30 +91,42 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t w, int64_t total) {
   return (w & 7) * (total >> 3) + (w >> 3);
 }
 
-// 16 spd bytes spd_row[j .. j+15] as four dwords; bytes at or past `limit`
-// read as 0. `vec`: the 16 bytes are 16-byte aligned and may be loaded whole.
-__device__ __forceinline__ void load_spd16(const uint8_t* spd_row, int64_t j, int64_t limit,
-                                           bool vec, uint32_t w[4]) {
-  if (spd_row == nullptr) {
-    w[0] = w[1] = w[2] = w[3] = 0u;
-    return;
+// Raw buffer resource over [base, base + 2 GiB): untyped loads, 32-bit data
+// format (the gfx9-family descriptor word). Offsets passed to the loads below
+// are always inside the caller's buffer; the range field is not relied on.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t buf_u8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(r, voff, soff, 0);
+}
+
+__device__ __forceinline__ void buf_u128(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                         uint32_t w[4]) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+  w[0] = v[0]; w[1] = v[1]; w[2] = v[2]; w[3] = v[3];
+}
+
+// 16 spd bytes row[j .. j+15] as four dwords, byte by byte, bytes at or past
+// `limit` read as 0. Used for unaligned slices and the last partial group;
+// kept rolled so it costs few registers.
+__device__ __forceinline__ void load_spd16_bytes(const uint8_t* row, int64_t j, int64_t limit,
+                                                 uint32_t w[4]) {
+  uint64_t lo = 0, hi = 0;
+  const int64_t n = limit - j < 16 ? limit - j : 16;
+#pragma unroll 1
+  for (int t = 0; t < (int)n; ++t) {
+    const uint64_t b = row[j + t];
+    if (t < 8)
+      lo |= b << (8 * t);
+    else
+      hi |= b << (8 * (t - 8));
   }
-  if (vec && j + 16 <= limit) {
-    const uint4 v = *reinterpret_cast<const uint4*>(spd_row + j);
-    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
-    return;
-  }
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    uint32_t x = 0;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int64_t jj = j + 4 * q + t;
-      const uint32_t b = (jj < limit) ? (uint32_t)spd_row[jj] : 0u;
-      x |= b << (8 * t);
-    }
-    w[q] = x;
-  }
+  w[0] = (uint32_t)lo; w[1] = (uint32_t)(lo >> 32);
+  w[2] = (uint32_t)hi; w[3] = (uint32_t)(hi >> 32);
 }
 
 }  // namespace gt

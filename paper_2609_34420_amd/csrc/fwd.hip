@@ -13,24 +13,102 @@
 // shared by the 4 waves; the per-head table (times log2 e) lives in LDS.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "tiles.hpp"
 
 namespace gt {
 
 namespace {
 
 constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
 constexpr int kBC = 64;          // keys per LDS tile
+constexpr float kRescaleSlack = 8.0f;   // log2 units the running max may lag
 
-template <int D, int QB, bool OUT_F32>
-__global__ __launch_bounds__(256) void fwd_bf16_kernel(FwdArgs a) {
-  constexpr int KB = kBC / 32;   // 32-key sub-blocks per tile
-  constexpr int NKC = D / 16;    // k-chunks of Q K^T
-  constexpr int NCB = D / 32;    // 32-row blocks of O^T
-  constexpr int CPR = D / 8;     // 16-byte chunks per K row
+// One key tile for every query block of the wave. Each 32-key sub-block is
+// finished (scores, softmax update, P V) before the next one starts, which
+// keeps the live score registers to one 32x32 block.
+template <int D, int QB, bool MASK>
+__device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV, const float* sT,
+                                         const bf16x8 (&qf)[QB][D / 16],
+                                         const uint32_t (&w)[QB][kBC / 32][4], int64_t j0,
+                                         int64_t Sk, float sl2, float (&m)[QB], float (&l)[QB],
+                                         f32x16 (&acc)[QB][D / 32]) {
+  constexpr int KB = kBC / 32;
+  constexpr int NKC = D / 16;
+  constexpr int NCB = D / 32;
+  const int lane = threadIdx.x & 63;
+  const int col = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      f32x16 s = zero_f32x16();
+      const int krow = kb * 32 + perm32(col);
+#pragma unroll
+      for (int kc = 0; kc < NKC; ++kc)
+        s = mfma32(lds_b128(sK + krow * D + swz_rows<D>(krow, kc * 2 + g) * 8), qf[qb][kc], s);
+      float x[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const uint32_t b = (w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu;
+        const float xv = fmaf(s[r], sl2, sT[b]);
+        if constexpr (MASK)
+          x[r] = (j0 + kb * 32 + 16 * g + r < Sk) ? xv : -INFINITY;
+        else
+          x[r] = xv;
+      }
+      float mx = x[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      // Lazy rescale: keep the reference max unless a score exceeds it by
+      // more than the slack (p <= 2^slack stays exact in fp32 and bf16).
+      if (__any(mx > m[qb] + kRescaleSlack)) {
+        const float mnew = fmaxf(m[qb], mx);
+        const float alpha = (mnew == -INFINITY) ? 1.0f : exp2_fast(m[qb] - mnew);
+        m[qb] = mnew;
+        l[qb] *= alpha;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[qb][cb][r] *= alpha;
+      }
+      const float msafe = (m[qb] == -INFINITY) ? 0.0f : m[qb];
+      float p[16];
+      float ls = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        p[r] = exp2_fast(x[r] - msafe);
+        ls += p[r];
+      }
+      l[qb] += ls;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const bf16x8 pb = cvt_bf16x8(p + 8 * q);
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          const int crow = cb * 32 + col;
+          acc[qb][cb] = mfma32(lds_b128(sV + crow * kBC + swz_t64(crow, kb * 4 + 2 * g + q) * 8), pb,
+                               acc[qb][cb]);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// VEC: spd rows are 16-byte aligned. FULL: VEC and Sk a multiple of the key
+// tile, so every spd group is loaded whole and no tile needs masking.
+template <int D, int QB, bool OUT_F32, bool VEC, bool FULL>
+__global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
+  constexpr int KB = kBC / 32;
+  constexpr int NKC = D / 16;
+  constexpr int NCB = D / 32;
   constexpr int BR = kWaves * 32 * QB;
+  using Stager = KVStager<D, kThreads, true, false, false, true>;
 
-  __shared__ __attribute__((aligned(16))) uint16_t sK[kBC * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[D * kBC];   // V^T
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBC * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][D * kBC];   // V^T
   __shared__ float sT[256];
 
   const int tid = threadIdx.x;
@@ -43,7 +121,7 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(FwdArgs a) {
   const int64_t qblk = lid / a.H;
   const int64_t qbase = qblk * BR + (int64_t)wave * 32 * QB;
 
-  for (int t = tid; t < 256; t += 256)
+  for (int t = tid; t < 256; t += kThreads)
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + t] * kLog2e : 0.0f;
 
   const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)h * a.Sq * D;
@@ -51,18 +129,43 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(FwdArgs a) {
   const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + (int64_t)h * a.Sk * D;
   const float sl2 = a.scale * kLog2e;
 
+  // Q^T operands; rows past Sq load the clamped row Sq-1 (their output is
+  // not stored).
   bf16x8 qf[QB][NKC];
-  const uint8_t* srow[QB];
+  int64_t qrow[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int64_t i = qbase + qb * 32 + col;
-    const bool ok = i < a.Sq;
+    qrow[qb] = i < a.Sq ? i : a.Sq - 1;
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc)
-      qf[qb][kc] = ok ? *reinterpret_cast<const bf16x8*>(qh + i * D + kc * 16 + g * 8)
-                      : zero_bf16x8();
-    srow[qb] = ok ? a.spd + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
+      qf[qb][kc] = *reinterpret_cast<const bf16x8*>(qh + qrow[qb] * D + kc * 16 + g * 8);
   }
+
+  // spd bytes of key group j..j+15 of the lane's query row: one 16-byte raw
+  // buffer load (scalar base per wave, lane offset row*ld + 16 g, scalar key
+  // offset), or byte loads for the partial last tile and unaligned slices.
+  const int64_t ld = a.ld_spd;
+  const int64_t rb = qbase < a.Sq ? qbase : a.Sq - 1;
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.spd + (a.row_off + rb) * ld + a.col_off);
+  uint32_t voff[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) voff[qb] = (uint32_t)((qrow[qb] - rb) * ld) + 16u * g;
+  auto fetch_spd = [&](int64_t jt, uint32_t (&w)[QB][KB][4]) {
+    if (FULL || (VEC && jt + kBC <= a.Sk)) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) buf_u128(rs, voff[qb], (uint32_t)(jt + kb * 32), w[qb][kb]);
+    } else {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const uint8_t* row = a.spd + (a.row_off + qrow[qb]) * ld + a.col_off;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) load_spd16_bytes(row, jt + kb * 32 + 16 * g, a.Sk, w[qb][kb]);
+      }
+    }
+  };
 
   float m[QB], l[QB];
   f32x16 acc[QB][NCB];
@@ -74,90 +177,41 @@ __global__ __launch_bounds__(256) void fwd_bf16_kernel(FwdArgs a) {
     for (int cb = 0; cb < NCB; ++cb) acc[qb][cb] = zero_f32x16();
   }
 
-  for (int64_t j0 = 0; j0 < a.Sk; j0 += kBC) {
-    __syncthreads();
-    // K tile, row-major with swizzled 16-byte chunks.
-    for (int c = tid; c < kBC * CPR; c += 256) {
-      const int row = c / CPR, ch = c % CPR;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (j0 + row < a.Sk) val = *reinterpret_cast<const uint4*>(kh + (j0 + row) * D + ch * 8);
-      *reinterpret_cast<uint4*>(sK + row * D + swz_rows<D>(row, ch) * 8) = val;
-    }
-    // V^T tile: two key rows per thread packed into dwords.
-    for (int c = tid; c < (kBC / 2) * CPR; c += 256) {
-      const int jp = c % (kBC / 2), cc = c / (kBC / 2);
-      const int j = 2 * jp;
-      uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
-      if (j0 + j < a.Sk) v0 = *reinterpret_cast<const uint4*>(vh + (j0 + j) * D + cc * 8);
-      if (j0 + j + 1 < a.Sk) v1 = *reinterpret_cast<const uint4*>(vh + (j0 + j + 1) * D + cc * 8);
-      const uint16_t* p0 = reinterpret_cast<const uint16_t*>(&v0);
-      const uint16_t* p1 = reinterpret_cast<const uint16_t*>(&v1);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int crow = cc * 8 + e;
-        const uint32_t w = (uint32_t)p0[e] | ((uint32_t)p1[e] << 16);
-        *reinterpret_cast<uint32_t*>(sV + crow * kBC + swz_t64(crow, j >> 3) * 8 + (j & 7)) = w;
-      }
-    }
-    __syncthreads();
+  const int64_t ntiles = (a.Sk + kBC - 1) / kBC;
+  Stager st;
+  uint32_t wc[QB][KB][4];
+  if (ntiles > 0) {
+    st.load(kh, vh, 0, a.Sk);
+    fetch_spd(0, wc);
+    if (!FULL && kBC > a.Sk) st.mask_tail(0, a.Sk);
+    st.store(sK[0], nullptr, nullptr, sV[0]);
+  }
+  __syncthreads();
 
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      float x[KB][16];
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        f32x16 s = zero_f32x16();
-        const int krow = kb * 32 + perm32(col);
-#pragma unroll
-        for (int kc = 0; kc < NKC; ++kc)
-          s = mfma32(lds_b128(sK + krow * D + swz_rows<D>(krow, kc * 2 + g) * 8), qf[qb][kc], s);
-        const int64_t jb = j0 + kb * 32 + 16 * g;
-        uint32_t w4[4];
-        load_spd16(srow[qb], jb, a.Sk, a.spd_vec != 0, w4);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const uint32_t b = (w4[r >> 2] >> (8 * (r & 3))) & 0xffu;
-          const float xv = s[r] * sl2 + sT[b];
-          x[kb][r] = (jb + r < a.Sk) ? xv : -INFINITY;
-        }
-      }
-      float mx = x[0][0];
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, x[kb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mnew = fmaxf(m[qb], mx);
-      const float msafe = (mnew == -INFINITY) ? 0.0f : mnew;
-      const float alpha = exp2_fast(m[qb] - msafe);
-      m[qb] = mnew;
-      l[qb] *= alpha;
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[qb][cb][r] *= alpha;
-      float ls = 0.0f;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        float p[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          p[r] = exp2_fast(x[kb][r] - msafe);
-          ls += p[r];
-        }
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const bf16x8 pb = cvt_bf16x8(p + 8 * q);
-#pragma unroll
-          for (int cb = 0; cb < NCB; ++cb) {
-            const int crow = cb * 32 + col;
-            const bf16x8 vf = lds_b128(sV + crow * kBC + swz_t64(crow, kb * 4 + 2 * g + q) * 8);
-            acc[qb][cb] = mfma32(vf, pb, acc[qb][cb]);
-          }
-        }
-      }
-      l[qb] += ls;
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int buf = (int)(t & 1);
+    const int64_t j0 = t * kBC;
+    const bool more = t + 1 < ntiles;
+    uint32_t wn[QB][KB][4];
+    if (more) {
+      st.load(kh, vh, j0 + kBC, a.Sk);
+      fetch_spd(j0 + kBC, wn);
     }
+    if (FULL || j0 + kBC <= a.Sk)
+      fwd_tile<D, QB, false>(sK[buf], sV[buf], sT, qf, wc, j0, a.Sk, sl2, m, l, acc);
+    else
+      fwd_tile<D, QB, true>(sK[buf], sV[buf], sT, qf, wc, j0, a.Sk, sl2, m, l, acc);
+    if (more) {
+      if (!FULL && j0 + 2 * kBC > a.Sk) st.mask_tail(j0 + kBC, a.Sk);
+      st.store(sK[buf ^ 1], nullptr, nullptr, sV[buf ^ 1]);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) wc[qb][kb][e] = wn[qb][kb][e];
+    }
+    __syncthreads();
   }
 
   // Epilogue: O = O_acc / l, LSE = (m + log2 l) ln 2.
@@ -259,8 +313,13 @@ template <int D, int QB, bool OUT_F32>
 hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t s) {
   constexpr int BR = kWaves * 32 * QB;
   const int64_t nqb = (a.Sq + BR - 1) / BR;
-  const int64_t grid = nqb * a.H;
-  hipLaunchKernelGGL((fwd_bf16_kernel<D, QB, OUT_F32>), dim3((unsigned)grid), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)(nqb * a.H));
+  if (a.spd_vec && a.Sk % kBC == 0)
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, QB, OUT_F32, true, true>), grid, dim3(kThreads), 0, s, a);
+  else if (a.spd_vec)
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, QB, OUT_F32, true, false>), grid, dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, QB, OUT_F32, false, false>), grid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -276,7 +335,7 @@ hipError_t launch_fwd_f32(const FwdArgs& a, hipStream_t s) {
 hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStream_t s) {
   if (bf16) {
     if (d == 64) return out_f32 ? launch_fwd_bf16<64, 1, true>(a, s) : launch_fwd_bf16<64, 1, false>(a, s);
-    return out_f32 ? launch_fwd_bf16<32, 1, true>(a, s) : launch_fwd_bf16<32, 1, false>(a, s);
+    return out_f32 ? launch_fwd_bf16<32, 2, true>(a, s) : launch_fwd_bf16<32, 2, false>(a, s);
   }
   return d == 64 ? launch_fwd_f32<64>(a, s) : launch_fwd_f32<32>(a, s);
 }

@@ -44,6 +44,7 @@ struct BwdArgs {
   float* dtable;
   float* lse2;            // workspace [H, N]: LSE * log2(e), +inf for empty rows
   float* dlt;             // workspace [H, N]: rowsum(dO * O)
+  float* nmax;            // workspace [H, ceil(N/256), 2]: block max of |dO_i|^2, |V_i|^2
   int32_t H;
   int64_t N;
   float scale;
@@ -62,7 +63,10 @@ struct MergeArgs {
 
 // Launchers return the hipError_t of the launch.
 hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStream_t s);
-hipError_t launch_bwd(const BwdArgs& a, int d, bool bf16, hipStream_t s);
+// phase: -1 = all stages in order, 0 = prepare, 1 = dK/dV/dtable, 2 = dQ.
+hipError_t launch_bwd(const BwdArgs& a, int d, bool bf16, int phase, hipStream_t s);
+hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s);
+hipError_t launch_dq_bf16(const BwdArgs& a, int d, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, bool out_bf16, hipStream_t s);
 
 }  // namespace gt

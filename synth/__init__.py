@@ -26,20 +26,33 @@ _STREAMS = {"graph": 1, "q": 2, "k": 3, "v": 4, "do": 5, "table": 6, "rows": 7,
 
 
 def rng(seed: int, stream: str, layer: int = 0) -> np.random.Generator:
-    """Independent named substream of the master seed."""
+    """Independent named substream of the master seed (numpy)."""
     ss = np.random.SeedSequence(entropy=int(seed), spawn_key=(_STREAMS[stream], int(layer)))
     return np.random.Generator(np.random.PCG64(ss))
 
 
+def stream_seed(seed: int, stream: str, layer: int = 0) -> int:
+    """63-bit seed of a named substream (for torch CPU generators)."""
+    ss = np.random.SeedSequence(entropy=int(seed), spawn_key=(_STREAMS[stream], int(layer)))
+    return int(ss.generate_state(1, np.uint64)[0] >> np.uint64(1))
+
+
+def normal(seed: int, stream: str, shape, layer: int = 0) -> np.ndarray:
+    """float32 N(0, 1) draws of a named substream. torch's CPU generator is
+    used for speed; its output does not depend on the thread count."""
+    import torch
+
+    g = torch.Generator().manual_seed(stream_seed(seed, stream, layer))
+    return torch.randn(tuple(shape), generator=g, dtype=torch.float32).numpy()
+
+
 def round_bf16(x: np.ndarray) -> np.ndarray:
     """float32 -> nearest bf16 value (ties to even), returned as float32.
-    Inputs are finite normals; this is input quantisation, not arithmetic
-    of the method."""
-    x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32)
-    bias = ((u >> 16) & np.uint32(1)) + np.uint32(0x7FFF)
-    r = ((u + bias) & np.uint32(0xFFFF0000)).view(np.float32)
-    return r
+    Input quantisation, not arithmetic of the method."""
+    import torch
+
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).to(torch.float32).numpy()
 
 
 @dataclass
@@ -113,7 +126,7 @@ class Workload:
 
     # ---- dense tensors ----------------------------------------------------
     def _normal(self, seed, stream, shape, std, layer=0):
-        x = rng(seed, stream, layer).standard_normal(size=shape, dtype=np.float32)
+        x = normal(seed, stream, shape, layer)
         if std != 1.0:
             x *= np.float32(std)
         return round_bf16(x) if self.dtype == "bf16" else x

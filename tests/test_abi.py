@@ -107,9 +107,9 @@ def test_bwd_validation(kw, code):
 
 def test_bwd_workspace_size():
     L = gt.lib()
-    # two fp32 [H, N] arrays, each padded to 256 bytes
-    assert L.gt_attn_bwd_workspace_size(8, 131072, 64, BF16) == 2 * 8 * 131072 * 4
-    assert L.gt_attn_bwd_workspace_size(1, 7, 32, F32) == 2 * 256
+    # two fp32 [H, N] arrays and fp32 [H, ceil(N/256), 2], each padded to 256 bytes
+    assert L.gt_attn_bwd_workspace_size(8, 131072, 64, BF16) == 2 * 8 * 131072 * 4 + 8 * 512 * 2 * 4
+    assert L.gt_attn_bwd_workspace_size(1, 7, 32, F32) == 3 * 256
     assert L.gt_attn_bwd_workspace_size(0, 7, 32, F32) == 0
 
 

@@ -90,12 +90,16 @@ def test_zipf_spd_distribution_and_counter_based():
     assert 0.2 < probs[0] < 0.3
 
 
-def test_round_bf16_matches_torch():
+def test_round_bf16_is_round_to_nearest_even():
+    """Against the bit-level definition: add 0x7FFF plus the lowest kept bit,
+    then truncate the low 16 bits (finite inputs)."""
     x = np.random.default_rng(6).standard_normal(100000).astype(np.float32) * 3
     x[:4] = [1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -2.5, 0.0]   # ties round to even
     mine = synth.round_bf16(x)
-    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    u = x.view(np.uint32).astype(np.uint64)
+    ref = ((u + ((u >> 16) & 1) + 0x7FFF) & 0xFFFF0000).astype(np.uint32).view(np.float32)
     np.testing.assert_array_equal(mine, ref)
+    assert mine[0] == 1.0 and mine[1] == 1.0 + 2 ** -6
 
 
 def test_workload_tensors_are_seeded_and_bf16_exact():
