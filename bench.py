@@ -19,6 +19,7 @@ and copied to the GPU before the timed region.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -45,9 +46,12 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--workload", default="sbm128k")
     p.add_argument("--seed", type=int, default=0)
-    p.add_argument("--cpu-rows", type=int, default=32,
+    p.add_argument("--cpu-rows", type=int, default=384,
                    help="query rows of the oracle CPU baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="run one plain 1 GiB device copy before the timed region (its "
+                        "FETCH_SIZE / WRITE_SIZE counters calibrate the kernels')")
     return p.parse_args()
 
 
@@ -109,6 +113,14 @@ def run_gpu(w, args, dev):
             if ev is not None:
                 ev[2 + ph].record(stream)
 
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("copy calibration: 1 GiB device-to-device copy done")
+
     for i in range(args.warmup):
         step()
         torch.cuda.synchronize()
@@ -133,6 +145,31 @@ def run_gpu(w, args, dev):
     for kname, v in per.items():
         log(f"  {kname:9s} mean {sum(v) / len(v):9.3f} ms  min {min(v):9.3f} ms")
     return total_ms, wall, per
+
+
+_KERNEL_FILES = {"fwd": "fwd_bf16_kernel", "bwd_dkdv": "bwd_dkdv_bf16_kernel",
+                 "bwd_dq": "bwd_dq_bf16_kernel"}
+
+
+def kernel_sources_sha256() -> str:
+    h = hashlib.sha256()
+    for p in sorted((ROOT / "paper_2609_34420_amd" / "csrc").glob("*.[hc]*")):
+        h.update(p.name.encode())
+        h.update(p.read_bytes())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch (calibrated FETCH_SIZE + WRITE_SIZE) recorded under
+    profiles/, or None when the kernels changed since the counters were taken."""
+    f = ROOT / "profiles" / f"traffic_{workload}.json"
+    if not f.exists():
+        return None
+    rec = json.loads(f.read_text())
+    if rec.get("kernel_source_sha256") != kernel_sources_sha256():
+        return None
+    k = rec["kernels"].get(_KERNEL_FILES[kernel])
+    return None if k is None else k["fetch_bytes"] + k["write_bytes"]
 
 
 def cpu_baseline(w, args):
@@ -201,8 +238,9 @@ def main():
     mean = {k: sum(v) / len(v) for k, v in per.items()}
     dom = max(("fwd", "bwd_dkdv", "bwd_dq"), key=lambda k: mean[k])
     achieved = kernels[dom][0] / (mean[dom] * 1e-3)
+    traffic = measured_traffic(w.name, dom)
     roofline = {"bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK_BF16 / 1e12,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16, "traffic": None,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16, "traffic": traffic,
                 "kernel": dom, "kernel_ms": mean[dom], "flop_per_launch": kernels[dom][0],
                 "flop_rule": kernels[dom][1]}
 

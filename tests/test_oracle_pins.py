@@ -362,3 +362,25 @@ def test_ring_step_offsets_select_the_right_slice():
             t = target[row_off + i]
             if col_off <= t < col_off + Sk:
                 np.testing.assert_allclose(o[0, i], v[0, t], atol=1e-25, rtol=1e-20)
+
+
+def test_row_sampled_backward_equals_masked_full_backward():
+    """The full-size GPU checks rely on two facts, checked here on the full
+    oracle: dQ of a query row depends only on that row, and with dO zero
+    outside rows R the full dK, dV, dtable equal the backward of rows R."""
+    q, k, v, do, table, spd = _rand_case(H=2, N=60, d=8, nb=7, seed=21, out_of_range=True)
+    R = np.array([0, 5, 17, 33, 59])
+    s = 0.4
+    dq, _, _, _ = oracle.backward(q, k, v, spd, table, s, do)
+    dq_r, dk_r, dv_r, dt_r = oracle.block_backward(q[:, R], k, v, spd[R], table, s, do[:, R])
+    np.testing.assert_allclose(dq_r, dq[:, R], atol=1e-12)
+    dom = np.zeros_like(do)
+    dom[:, R] = do[:, R]
+    _, dk_m, dv_m, dt_m = oracle.backward(q, k, v, spd, table, s, dom)
+    np.testing.assert_allclose(dk_r, dk_m, atol=1e-12)
+    np.testing.assert_allclose(dv_r, dv_m, atol=1e-12)
+    np.testing.assert_allclose(dt_r, dt_m, atol=1e-12)
+    O, L = oracle.forward(q, k, v, spd, table, s)
+    O_r, L_r = oracle.block_attention(q[:, R], k, v, spd[R], table, s)
+    np.testing.assert_allclose(O_r, O[:, R], atol=1e-12)
+    np.testing.assert_allclose(L_r, L[:, R], atol=1e-12)
