@@ -65,8 +65,10 @@ __device__ __forceinline__ void stage_load(const BwdArgs& a, const uint16_t* qh,
                                            StageRegs& r) {
   constexpr int CPR = D / 8;
   constexpr int ITEMS = 32 * CPR;   // row pairs x 16-byte chunks, per tensor
-  const int t = threadIdx.x;
-  if (t < 2 * ITEMS) {
+  // Every thread loads (threads past the work items repeat one), so no
+  // wave skips a load and the loads in flight are the same on every path.
+  const int t = (2 * ITEMS >= kThreads) ? (int)threadIdx.x : (int)threadIdx.x % (2 * ITEMS);
+  {
     const int u = t % ITEMS;
     const int ip = u % 32, cc = u / 32;
     const uint16_t* src = (t < ITEMS) ? qh : oh;
@@ -76,10 +78,11 @@ __device__ __forceinline__ void stage_load(const BwdArgs& a, const uint16_t* qh,
     r.v0 = *reinterpret_cast<const uint4*>(src + r0 * D + cc * 8);
     r.v1 = *reinterpret_cast<const uint4*>(src + r1 * D + cc * 8);
   }
-  if (t < 2 * kBQ) {
-    const int64_t i = i0 + (t & (kBQ - 1));
+  {
+    const int ts = (int)threadIdx.x & (2 * kBQ - 1);
+    const int64_t i = i0 + (ts & (kBQ - 1));
     const int64_t ic = (QFULL || i < a.N) ? i : a.N - 1;
-    r.stat = (t < kBQ) ? lse2h[ic] : dlth[ic];
+    r.stat = (ts < kBQ ? lse2h : dlth)[ic];
   }
 }
 
@@ -99,6 +102,8 @@ __device__ __forceinline__ void stage_store(DkdvSmem<D>& sm, int buf, StageRegs 
     uint16_t* rm = (t < ITEMS) ? sm.q[buf] : sm.o[buf];
     uint16_t* tr = (t < ITEMS) ? sm.qt[buf] : sm.ot[buf];
     const int row = 2 * ip;
+    opaque(r.v0);
+    opaque(r.v1);
     if (tail) {
       if (i0 + row >= n) r.v0 = make_uint4(0, 0, 0, 0);
       if (i0 + row + 1 >= n) r.v1 = make_uint4(0, 0, 0, 0);
@@ -131,13 +136,13 @@ __device__ __forceinline__ void stage_store(DkdvSmem<D>& sm, int buf, StageRegs 
 // any bucket will do), branch-free.
 template <bool QFULL>
 __device__ __forceinline__ void load_bytes(const uint8_t* spd_cols, int64_t ld, int64_t i_base,
-                                           int64_t n, uint32_t key_off, uint32_t b[16]) {
+                                           int64_t n, uint32_t key_off, uint8_t b[16]) {
   const int g = (threadIdx.x >> 5) & 1;
   if constexpr (QFULL) {
     const __amdgpu_buffer_rsrc_t rs = make_rsrc(spd_cols + i_base * ld);
     const uint32_t voff = (uint32_t)(16 * g) * (uint32_t)ld + key_off;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) b[r] = buf_u8(rs, voff, (uint32_t)(r * ld));
+    for (int r = 0; r < 16; ++r) b[r] = (uint8_t)buf_u8(rs, voff, (uint32_t)(r * ld));
   } else {
     // base at the clamped first row, so every offset below is >= 0
     const int64_t ib = i_base < n ? i_base : n - 1;
@@ -146,7 +151,7 @@ __device__ __forceinline__ void load_bytes(const uint8_t* spd_cols, int64_t ld, 
     for (int r = 0; r < 16; ++r) {
       int64_t row = i_base + 16 * g + r;
       row = row < n ? row : n - 1;
-      b[r] = buf_u8(rs, (uint32_t)((row - ib) * ld) + key_off, 0u);
+      b[r] = (uint8_t)buf_u8(rs, (uint32_t)((row - ib) * ld) + key_off, 0u);
     }
   }
 }
@@ -161,7 +166,7 @@ template <int D, bool KTAIL>
 __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const uint2* tabw,
                                               unsigned long long* hist, int buf, int qs,
                                               const bf16x8* kf, const bf16x8* vf,
-                                              const uint32_t* b, float sl2, bool jok,
+                                              const uint8_t* b, float sl2, bool jok,
                                               f32x16* dk, f32x16* dv) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
@@ -195,7 +200,9 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const uint2* tabw
   const uint32_t cpy = (uint32_t)(lane & (kCopies - 1));
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    idx[r] = (b[r] << 4) | cpy;                    // copy cpy of bucket b
+    uint32_t bk = b[r];
+    opaque(bk);                                    // keep the byte's wait here
+    idx[r] = (bk << 4) | cpy;                      // copy cpy of bucket b
     tb[r] = __uint_as_float(tabw[idx[r]].x);
   }
 #pragma unroll
@@ -268,19 +275,26 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, con
 
   StageRegs st;
   stage_load<D, QFULL>(a, qh, oh, lse2h, dlth, 0, st);
-  uint32_t bA[16], bB[16];
+  uint8_t bA[16], bB[16];
   load_bytes<QFULL>(spd_cols, ld, 0, a.N, key_off, bA);
   stage_store<D, QFULL>(sm, 0, st, 0, a.N, inv_sl2, sF);
+  wait_loads();
   __syncthreads();
 
   for (int64_t t = 0; t < ntiles; ++t) {
     const int buf = (int)(t & 1);
     const int64_t i0 = t * kBQ;
     const bool more = t + 1 < ntiles;
+    // The prefetches are unconditional (the last tile re-reads itself), so
+    // every path through the loop has the same loads in flight and the
+    // waits before each use stay exact.
+    const int64_t inext = more ? i0 + kBQ : i0;
     load_bytes<QFULL>(spd_cols, ld, i0 + 32, a.N, key_off, bB);
-    if (more) stage_load<D, QFULL>(a, qh, oh, lse2h, dlth, i0 + kBQ, st);
+    stage_load<D, QFULL>(a, qh, oh, lse2h, dlth, inext, st);
+    sched_fence();
     dkdv_subblock<D, KTAIL>(sm, tabw, hist, buf, 0, kf, vf, bA, sl2, jok, dk, dv);
-    if (more) load_bytes<QFULL>(spd_cols, ld, i0 + kBQ, a.N, key_off, bA);
+    load_bytes<QFULL>(spd_cols, ld, inext, a.N, key_off, bA);
+    sched_fence();
     dkdv_subblock<D, KTAIL>(sm, tabw, hist, buf, 1, kf, vf, bB, sl2, jok, dk, dv);
     if (more) stage_store<D, QFULL>(sm, buf ^ 1, st, i0 + kBQ, a.N, inv_sl2, sF);
     __syncthreads();
@@ -317,7 +331,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   __shared__ unsigned long long hist[kTabEntries];
   __shared__ float red[2][kNW];
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, col = tid & 31;
+  const int wave = wave_id(), col = tid & 31;
   const int64_t nkb = (a.N + kBK - 1) / kBK;
   const int64_t lid = xcd_remap(blockIdx.x, nkb * a.H);
   const int h = (int)(lid % a.H);

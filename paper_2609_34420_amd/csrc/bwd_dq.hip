@@ -18,13 +18,16 @@ constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kBC = 64;
 
+// One key tile for every query block of the wave. The accumulators of S^T
+// and dP^T start at -lse2 / (scale log2 e) and -Dlt, so per score element the
+// vector work is the bias FMA, exp2, one multiply and the bf16 conversion.
 template <int D, int QB, bool MASK>
 __device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sKt, const uint16_t* sV,
                                         const float* sT, const bf16x8 (&qf)[QB][D / 16],
-                                        const bf16x8 (&df)[QB][D / 16], const float (&lse2)[QB],
-                                        const float (&dlt)[QB], const uint32_t (&w)[QB][kBC / 32][4],
-                                        int64_t j0, int64_t nk, float sl2,
-                                        f32x16 (&acc)[QB][D / 32]) {
+                                        const bf16x8 (&df)[QB][D / 16], const f32x16 (&init_s)[QB],
+                                        const f32x16 (&init_p)[QB],
+                                        const uint32_t (&w)[QB][kBC / 32][4], int64_t j0,
+                                        int64_t nk, float sl2, f32x16 (&acc)[QB][D / 32]) {
   constexpr int KB = kBC / 32;
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
@@ -34,7 +37,10 @@ __device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sKt,
   for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      f32x16 s = zero_f32x16(), dp = zero_f32x16();
+      float tb[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) tb[r] = sT[(w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu];
+      f32x16 s = init_s[qb], dp = init_p[qb];
       const int krow = kb * 32 + perm32(col);
 #pragma unroll
       for (int kc = 0; kc < NKC; ++kc) {
@@ -45,11 +51,9 @@ __device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sKt,
       float ds[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const uint32_t b = (w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu;
-        const float x = fmaf(s[r], sl2, sT[b]) - lse2[qb];
-        float pv = exp2_fast(x);
+        float pv = exp2_fast(fmaf(s[r], sl2, tb[r]));
         if constexpr (MASK) pv = (j0 + kb * 32 + 16 * g + r < nk) ? pv : 0.0f;
-        ds[r] = pv * (dp[r] - dlt[qb]);
+        ds[r] = pv * dp[r];
       }
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
@@ -61,6 +65,7 @@ __device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sKt,
                                acc[qb][cb]);
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 }
@@ -81,7 +86,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
   __shared__ float sT[256];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = wave_id();
   const int col = lane & 31, g = lane >> 5;
 
   const int64_t nqb = (a.N + BR - 1) / BR;
@@ -103,8 +108,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
   // Q^T, dO^T operands and statistics; rows past N load the clamped row N-1
   // and get lse2 = +inf (P = 0); their dQ is not stored.
   bf16x8 qf[QB][NKC], df[QB][NKC];
-  float lse2[QB], dlt[QB];
+  f32x16 init_s[QB], init_p[QB];
   int64_t qrow[QB];
+  const float inv_sl2 = 1.0f / sl2;
   f32x16 acc[QB][NCB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -117,8 +123,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
     }
     const float l2 = a.lse2[(int64_t)h * a.N + qrow[qb]];
     const float dl = a.dlt[(int64_t)h * a.N + qrow[qb]];
-    lse2[qb] = i < a.N ? l2 : INFINITY;
-    dlt[qb] = i < a.N ? dl : 0.0f;
+    const float is = i < a.N ? -l2 * inv_sl2 : -INFINITY;   // padded rows: P = 0
+    const float ip = i < a.N ? -dl : 0.0f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      init_s[qb][r] = is;
+      init_p[qb][r] = ip;
+    }
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) acc[qb][cb] = zero_f32x16();
   }
@@ -152,6 +163,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
   fetch_spd(0, wc);
   if (kBC > a.N) st.mask_tail(0, a.N);
   st.store(sK[0], sKt[0], sV[0], nullptr);
+  wait_loads();
   __syncthreads();
 
   for (int64_t t = 0; t < ntiles; ++t) {
@@ -163,10 +175,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
       st.load(kh, vh, j0 + kBC, a.N);
       fetch_spd(j0 + kBC, wn);
     }
+    sched_fence();
     if (FULL || j0 + kBC <= a.N)
-      dq_tile<D, QB, false>(sK[buf], sKt[buf], sV[buf], sT, qf, df, lse2, dlt, wc, j0, a.N, sl2, acc);
+      dq_tile<D, QB, false>(sK[buf], sKt[buf], sV[buf], sT, qf, df, init_s, init_p, wc, j0, a.N, sl2, acc);
     else
-      dq_tile<D, QB, true>(sK[buf], sKt[buf], sV[buf], sT, qf, df, lse2, dlt, wc, j0, a.N, sl2, acc);
+      dq_tile<D, QB, true>(sK[buf], sKt[buf], sV[buf], sT, qf, df, init_s, init_p, wc, j0, a.N, sl2, acc);
     if (more) {
       if (!FULL && j0 + 2 * kBC > a.N) st.mask_tail(j0 + kBC, a.N);
       st.store(sK[buf ^ 1], sKt[buf ^ 1], sV[buf ^ 1], nullptr);

@@ -6,6 +6,7 @@
 namespace gt {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -19,6 +20,32 @@ constexpr float kLn2 = 0.69314718055994531f;
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+
+// Index of the calling wave in its workgroup, as a wave-uniform (scalar)
+// value: derived values such as buffer descriptors then stay in SGPRs.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+}
+
+// Keep the compiler from moving instructions across this point (used after
+// issuing prefetch loads, so no use of their results is hoisted next to
+// them and forces an early wait).
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// Hide a loaded value from the optimiser until this point: nothing derived
+// from it (e.g. the shifts that pack a transposed tile) can be computed
+// earlier, next to the load, where it would force an early wait.
+__device__ __forceinline__ void opaque(uint4& x) {
+  asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+}
+__device__ __forceinline__ void opaque(uint32_t& x) { asm volatile("" : "+v"(x)); }
+
+// Wait for every outstanding vector-memory load (s_waitcnt vmcnt(0) with the
+// other counters left free). Used once before a software-pipelined loop, so
+// that values loaded ahead of it are not treated as pending inside the loop,
+// where a conservative merge of the two loop entries would otherwise make the
+// first use of the current tile also wait for the next tile's prefetch.
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // 2^x on the transcendental unit (v_exp_f32): exp2(-inf) = 0.
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -34,20 +61,24 @@ __device__ __forceinline__ int perm32(int m) {
 }
 
 // XOR swizzle of 16-byte chunks in a row-major LDS tile whose rows hold D
-// bf16 (D / 8 chunks). Chosen so that the 8 lanes of one ds_read_b128 phase
-// reading MFMA rows perm32(0..7) (or perm32(8..15), ...) hit 8 distinct bank
-// groups.
+// bf16 (D / 8 chunks). For the rows an MFMA operand read touches (block rows
+// perm32(lane)), every 8-lane group hits 8 distinct 16-byte bank groups of a
+// 32-bank LDS and every 16-lane group 16 distinct ones of a 64-bank LDS.
 template <int D>
 __device__ __forceinline__ int swz_rows(int row, int chunk) {
   if constexpr (D == 64) {
-    return chunk ^ ((row & 3) | ((row >> 2) & 4));
+    return chunk ^ (((row >> 1) & 1) | ((row >> 3) & 2) | (((row ^ (row >> 2)) & 1) << 2));
   } else {
     return chunk ^ (((row >> 1) & 1) | ((row >> 3) & 2));
   }
 }
 
-// Swizzle for a transposed tile: row = feature c, 64 keys per row (8 chunks).
-__device__ __forceinline__ int swz_t64(int row, int chunk) { return chunk ^ (row & 7); }
+// Swizzle for a transposed tile: row = feature c, 64 keys per row (8
+// chunks); consecutive rows read together get distinct bank groups under the
+// same two models.
+__device__ __forceinline__ int swz_t64(int row, int chunk) {
+  return chunk ^ ((((row >> 1) & 3) | ((row & 1) << 2)) ^ (((row >> 3) & 1) << 2));
+}
 
 __device__ __forceinline__ bf16x8 lds_b128(const uint16_t* p) {
   return *reinterpret_cast<const bf16x8*>(p);
@@ -72,6 +103,17 @@ __device__ __forceinline__ bf16x8 cvt_bf16x8(const float* x) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) r[i] = (__bf16)x[i];
   return r;
+}
+
+// Sum of the 8 bf16 values of v plus acc, by packed dot products with 1.
+__device__ __forceinline__ float sum_bf16x8(const bf16x8& v, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 8; i += 2) {
+    const bf16x2 pr = {v[i], v[i + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(pr, one, acc, false);
+  }
+  return acc;
 }
 
 __device__ __forceinline__ uint16_t f2bf(float x) {

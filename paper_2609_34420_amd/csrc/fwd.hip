@@ -24,15 +24,24 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kBC = 64;          // keys per LDS tile
 constexpr float kRescaleSlack = 8.0f;   // log2 units the running max may lag
 
-// One key tile for every query block of the wave. Each 32-key sub-block is
-// finished (scores, softmax update, P V) before the next one starts, which
-// keeps the live score registers to one 32x32 block.
+// Running softmax state of one 32-query block. Scores are kept relative to
+// a reference max: the S^T accumulator starts at -msafe / (scale log2 e), so
+// x = s * scale log2 e + bias is already x_abs - msafe and p = 2^x. The
+// reference only moves (with a rescale of the accumulator) when a score
+// passes it by more than the slack, which needs the one exchange between
+// the lane halves; otherwise no cross-lane step is needed.
+struct SoftmaxState {
+  float m;        // reference max (log2 units), -inf before any finite score
+  float l;        // this lane half's partial row sum, relative to m
+  f32x16 init;    // -msafe / (scale log2 e), msafe = m or 0 while m = -inf
+};
+
 template <int D, int QB, bool MASK>
 __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV, const float* sT,
                                          const bf16x8 (&qf)[QB][D / 16],
                                          const uint32_t (&w)[QB][kBC / 32][4], int64_t j0,
-                                         int64_t Sk, float sl2, float (&m)[QB], float (&l)[QB],
-                                         f32x16 (&acc)[QB][D / 32]) {
+                                         int64_t Sk, float sl2, float inv_sl2,
+                                         SoftmaxState (&st)[QB], f32x16 (&acc)[QB][D / 32]) {
   constexpr int KB = kBC / 32;
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
@@ -42,7 +51,10 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
   for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      f32x16 s = zero_f32x16();
+      float tb[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) tb[r] = sT[(w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu];
+      f32x16 s = st[qb].init;
       const int krow = kb * 32 + perm32(col);
 #pragma unroll
       for (int kc = 0; kc < NKC; ++kc)
@@ -50,8 +62,7 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
       float x[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const uint32_t b = (w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu;
-        const float xv = fmaf(s[r], sl2, sT[b]);
+        const float xv = fmaf(s[r], sl2, tb[r]);
         if constexpr (MASK)
           x[r] = (j0 + kb * 32 + 16 * g + r < Sk) ? xv : -INFINITY;
         else
@@ -60,31 +71,35 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
       float mx = x[0];
 #pragma unroll
       for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      // Lazy rescale: keep the reference max unless a score exceeds it by
-      // more than the slack (p <= 2^slack stays exact in fp32 and bf16).
-      if (__any(mx > m[qb] + kRescaleSlack)) {
-        const float mnew = fmaxf(m[qb], mx);
-        const float alpha = (mnew == -INFINITY) ? 1.0f : exp2_fast(m[qb] - mnew);
-        m[qb] = mnew;
-        l[qb] *= alpha;
+      const float thr = (st[qb].m == -INFINITY) ? -INFINITY : kRescaleSlack;
+      if (__any(mx > thr)) {
+        // Move the reference: both halves agree on the new max.
+        const float mall = fmaxf(mx, __shfl_xor(mx, 32));
+        const float msafe_old = (st[qb].m == -INFINITY) ? 0.0f : st[qb].m;
+        const float mnew = fmaxf(st[qb].m, mall + msafe_old);
+        const float alpha = (mnew == -INFINITY) ? 1.0f : exp2_fast(st[qb].m - mnew);
+        st[qb].l *= alpha;
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[qb][cb][r] *= alpha;
-      }
-      const float msafe = (m[qb] == -INFINITY) ? 0.0f : m[qb];
-      float p[16];
-      float ls = 0.0f;
+        const float msafe_new = (mnew == -INFINITY) ? 0.0f : mnew;
+        const float shift = msafe_new - msafe_old;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p[r] = exp2_fast(x[r] - msafe);
-        ls += p[r];
+        for (int r = 0; r < 16; ++r) x[r] -= shift;
+        st[qb].m = mnew;
+        const float iv = -msafe_new * inv_sl2;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[qb].init[r] = iv;
       }
-      l[qb] += ls;
+      float ls = st[qb].l;
 #pragma unroll
       for (int q = 0; q < 2; ++q) {
-        const bf16x8 pb = cvt_bf16x8(p + 8 * q);
+        float p[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) p[r] = exp2_fast(x[8 * q + r]);
+        const bf16x8 pb = cvt_bf16x8(p);
+        ls = sum_bf16x8(pb, ls);       // the row sum of exactly the P that P V uses
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
           const int crow = cb * 32 + col;
@@ -92,7 +107,7 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
                                acc[qb][cb]);
         }
       }
-      __builtin_amdgcn_sched_barrier(0);
+      st[qb].l = ls;
     }
   }
 }
@@ -112,7 +127,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
   __shared__ float sT[256];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = wave_id();
   const int col = lane & 31, g = lane >> 5;
 
   const int64_t nqb = (a.Sq + BR - 1) / BR;
@@ -167,12 +182,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
     }
   };
 
-  float m[QB], l[QB];
+  const float inv_sl2 = 1.0f / sl2;
+  SoftmaxState sm[QB];
   f32x16 acc[QB][NCB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    m[qb] = -INFINITY;
-    l[qb] = 0.0f;
+    sm[qb].m = -INFINITY;
+    sm[qb].l = 0.0f;
+    sm[qb].init = zero_f32x16();
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) acc[qb][cb] = zero_f32x16();
   }
@@ -186,6 +203,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
     if (!FULL && kBC > a.Sk) st.mask_tail(0, a.Sk);
     st.store(sK[0], nullptr, nullptr, sV[0]);
   }
+  wait_loads();
   __syncthreads();
 
   for (int64_t t = 0; t < ntiles; ++t) {
@@ -197,10 +215,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
       st.load(kh, vh, j0 + kBC, a.Sk);
       fetch_spd(j0 + kBC, wn);
     }
+    sched_fence();
     if (FULL || j0 + kBC <= a.Sk)
-      fwd_tile<D, QB, false>(sK[buf], sV[buf], sT, qf, wc, j0, a.Sk, sl2, m, l, acc);
+      fwd_tile<D, QB, false>(sK[buf], sV[buf], sT, qf, wc, j0, a.Sk, sl2, inv_sl2, sm, acc);
     else
-      fwd_tile<D, QB, true>(sK[buf], sV[buf], sT, qf, wc, j0, a.Sk, sl2, m, l, acc);
+      fwd_tile<D, QB, true>(sK[buf], sV[buf], sT, qf, wc, j0, a.Sk, sl2, inv_sl2, sm, acc);
     if (more) {
       if (!FULL && j0 + 2 * kBC > a.Sk) st.mask_tail(j0 + kBC, a.Sk);
       st.store(sK[buf ^ 1], nullptr, nullptr, sV[buf ^ 1]);
@@ -217,7 +236,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
   // Epilogue: O = O_acc / l, LSE = (m + log2 l) ln 2.
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    const float lt = l[qb] + __shfl_xor(l[qb], 32);
+    const float lt = sm[qb].l + __shfl_xor(sm[qb].l, 32);
     const int64_t i = qbase + qb * 32 + col;
     if (i >= a.Sq) continue;
     const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
@@ -241,7 +260,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
       }
     }
     if (g == 0)
-      a.lse[(int64_t)h * a.Sq + i] = lt > 0.0f ? (m[qb] + __log2f(lt)) * kLn2 : -INFINITY;
+      a.lse[(int64_t)h * a.Sq + i] = lt > 0.0f ? (sm[qb].m + __log2f(lt)) * kLn2 : -INFINITY;
   }
 }
 

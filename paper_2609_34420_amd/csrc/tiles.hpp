@@ -71,7 +71,7 @@ struct KVStager {
   }
 
   // k_row, k_t, v_row, v_t: LDS tiles of this buffer (unused ones may be null)
-  __device__ __forceinline__ void store(uint16_t* k_row, uint16_t* k_t, uint16_t* v_row, uint16_t* v_t) const {
+  __device__ __forceinline__ void store(uint16_t* k_row, uint16_t* k_t, uint16_t* v_row, uint16_t* v_t) {
 #pragma unroll
     for (int s = 0; s < IPT; ++s) {
       const int it = (int)threadIdx.x + s * NT;
@@ -79,12 +79,15 @@ struct KVStager {
         const int u = it % ITEMS;
         const int jp = u % (BC / 2), cc = u / (BC / 2);
         const int row = 2 * jp;
+        uint4 a = r0[s], b = r1[s];
+        opaque(a);
+        opaque(b);
         if (it < ITEMS) {
-          if constexpr (K_ROW) put_rows(k_row, row, cc, r0[s], r1[s]);
-          if constexpr (K_T) put_t(k_t, row, cc, r0[s], r1[s]);
+          if constexpr (K_ROW) put_rows(k_row, row, cc, a, b);
+          if constexpr (K_T) put_t(k_t, row, cc, a, b);
         } else {
-          if constexpr (V_ROW) put_rows(v_row, row, cc, r0[s], r1[s]);
-          if constexpr (V_T) put_t(v_t, row, cc, r0[s], r1[s]);
+          if constexpr (V_ROW) put_rows(v_row, row, cc, a, b);
+          if constexpr (V_T) put_t(v_t, row, cc, a, b);
         }
       }
     }
