@@ -9,11 +9,14 @@
 // (lane & 31) and 16 consecutive keys per 32-key block: row max and row sum
 // are lane-local plus one exchange between the two lane halves, and the
 // lane's 16 spd bytes are one 16-byte load. P^T then feeds O^T += V^T P^T
-// straight from registers. K (row-major) and V^T tiles are staged in LDS and
-// shared by the 4 waves; the per-head table (times log2 e) lives in LDS.
+// straight from registers. K and V tiles are staged row-major in LDS and
+// shared by the 4 waves (V^T is read with transposing LDS reads); the
+// per-head table (times log2 e) lives in LDS.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
-#include "tiles.hpp"
+#include "stage.hpp"
 
 namespace gt {
 
@@ -36,8 +39,25 @@ struct SoftmaxState {
   f32x16 init;    // -msafe / (scale log2 e), msafe = m or 0 while m = -inf
 };
 
+// Per-lane LDS element offsets of the operand reads (tile-relative; the
+// 32-key block and 8-key step offsets are immediates).
+template <int D>
+struct FwdOffsets {
+  int k[D / 16];          // K rows perm32(lane), feature chunk 2 kc + g
+  int v[2][D / 32];       // transposing reads h = 0, 1 of V, feature block cb
+  __device__ __forceinline__ FwdOffsets() {
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) k[kc] = row_operand_off<D>(kc);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int cb = 0; cb < D / 32; ++cb) v[h][cb] = tr_operand_off<D>(h, cb);
+  }
+};
+
 template <int D, int QB, bool MASK>
 __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV, const float* sT,
+                                         const FwdOffsets<D>& off,
                                          const bf16x8 (&qf)[QB][D / 16],
                                          const uint32_t (&w)[QB][kBC / 32][4], int64_t j0,
                                          int64_t Sk, float sl2, float inv_sl2,
@@ -46,7 +66,7 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
   const int lane = threadIdx.x & 63;
-  const int col = lane & 31, g = lane >> 5;
+  const int g = lane >> 5;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
@@ -55,10 +75,8 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
 #pragma unroll
       for (int r = 0; r < 16; ++r) tb[r] = sT[(w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu];
       f32x16 s = st[qb].init;
-      const int krow = kb * 32 + perm32(col);
 #pragma unroll
-      for (int kc = 0; kc < NKC; ++kc)
-        s = mfma32(lds_b128(sK + krow * D + swz_rows<D>(krow, kc * 2 + g) * 8), qf[qb][kc], s);
+      for (int kc = 0; kc < NKC; ++kc) s = mfma32(lds_b128(sK + kb * 32 * D + off.k[kc]), qf[qb][kc], s);
       float x[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -102,9 +120,8 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
         ls = sum_bf16x8(pb, ls);       // the row sum of exactly the P that P V uses
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
-          const int crow = cb * 32 + col;
-          acc[qb][cb] = mfma32(lds_b128(sV + crow * kBC + swz_t64(crow, kb * 4 + 2 * g + q) * 8), pb,
-                               acc[qb][cb]);
+          const uint16_t* vt = sV + (kb * 32 + 8 * q) * D;
+          acc[qb][cb] = mfma32(lds_tr_operand(vt, off.v[0][cb], off.v[1][cb]), pb, acc[qb][cb]);
         }
       }
       st[qb].l = ls;
@@ -120,10 +137,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
   constexpr int BR = kWaves * 32 * QB;
-  using Stager = KVStager<D, kThreads, true, false, false, true>;
+  using Stage = RowStage<D, kThreads>;
+  static_assert(kBC == kTileRows, "key tile is one staged tile");
 
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBC * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][D * kBC];   // V^T
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][kBC * D];
   __shared__ float sT[256];
 
   const int tid = threadIdx.x;
@@ -195,42 +213,58 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
   }
 
   const int64_t ntiles = (a.Sk + kBC - 1) / kBC;
-  Stager st;
-  uint32_t wc[QB][KB][4];
+  const FwdOffsets<D> off;
+  Stage stK, stV;
+  uint32_t wA[QB][KB][4], wB[QB][KB][4];   // spd words of even / odd tiles
   if (ntiles > 0) {
-    st.load(kh, vh, 0, a.Sk);
-    fetch_spd(0, wc);
-    if (!FULL && kBC > a.Sk) st.mask_tail(0, a.Sk);
-    st.store(sK[0], nullptr, nullptr, sV[0]);
+    stK.load(tile_rsrc<D>(kh, 0, a.Sk));
+    stV.load(tile_rsrc<D>(vh, 0, a.Sk));
+    fetch_spd(0, wA);
+    stK.store(sK[0]);
+    stV.store(sV[0]);
   }
   wait_loads();
   __syncthreads();
 
-  for (int64_t t = 0; t < ntiles; ++t) {
-    const int buf = (int)(t & 1);
+  // One key tile: prefetch the next tile (the last tile re-reads itself, so
+  // the loads in flight are the same on every path), compute on buffer BUF,
+  // then stage the prefetch into the other buffer.
+  auto step = [&](int64_t t, auto bufc, auto maskc) {
+    constexpr int BUF = decltype(bufc)::value;
+    constexpr bool MASK = decltype(maskc)::value;
+    auto& wcur = BUF ? wB : wA;
+    auto& wnext = BUF ? wA : wB;
     const int64_t j0 = t * kBC;
     const bool more = t + 1 < ntiles;
-    uint32_t wn[QB][KB][4];
-    if (more) {
-      st.load(kh, vh, j0 + kBC, a.Sk);
-      fetch_spd(j0 + kBC, wn);
-    }
+    const int64_t jn = more ? j0 + kBC : j0;
+    stK.load(tile_rsrc<D>(kh, jn, a.Sk));
+    stV.load(tile_rsrc<D>(vh, jn, a.Sk));
+    fetch_spd(jn, wnext);
     sched_fence();
-    if (FULL || j0 + kBC <= a.Sk)
-      fwd_tile<D, QB, false>(sK[buf], sV[buf], sT, qf, wc, j0, a.Sk, sl2, inv_sl2, sm, acc);
-    else
-      fwd_tile<D, QB, true>(sK[buf], sV[buf], sT, qf, wc, j0, a.Sk, sl2, inv_sl2, sm, acc);
+    fwd_tile<D, QB, MASK>(sK[BUF], sV[BUF], sT, off, qf, wcur, j0, a.Sk, sl2, inv_sl2, sm, acc);
     if (more) {
-      if (!FULL && j0 + 2 * kBC > a.Sk) st.mask_tail(j0 + kBC, a.Sk);
-      st.store(sK[buf ^ 1], nullptr, nullptr, sV[buf ^ 1]);
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) wc[qb][kb][e] = wn[qb][kb][e];
+      stK.store(sK[BUF ^ 1]);
+      stV.store(sV[BUF ^ 1]);
     }
     __syncthreads();
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using Full = std::false_type;     // every key of the tile exists
+  using Part = std::true_type;      // last tile, keys past Sk masked
+  // Full tiles in pairs (static buffers), then at most one full tile and the
+  // partial last tile.
+  const int64_t nfull = FULL ? ntiles : a.Sk / kBC;
+  int64_t t = 0;
+  for (; t + 1 < nfull; t += 2) {
+    step(t, B0(), Full());
+    step(t + 1, B1(), Full());
+  }
+  if (t < nfull) {
+    step(t, B0(), Full());
+    if (!FULL && t + 1 < ntiles) step(t + 1, B1(), Part());
+  } else if (!FULL && t < ntiles) {
+    step(t, B0(), Part());
   }
 
   // Epilogue: O = O_acc / l, LSE = (m + log2 l) ln 2.

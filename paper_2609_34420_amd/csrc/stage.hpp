@@ -1,0 +1,127 @@
+// Row-major LDS tiles of 64 rows x D bf16, staged global -> registers ->
+// LDS, and the two ways the products read them:
+//   * as an operand whose contraction runs along the row (K in S = Q K^T):
+//     one 16-byte read per lane;
+//   * as an operand whose contraction runs DOWN the rows (V in O = P V, K in
+//     dQ = dS K, Q and dO in dK = dS^T Q, dV = P^T dO): two transposing
+//     8-byte reads (ds_read_b64_tr_b16) per lane, so no tile is ever stored
+//     transposed and no register shuffling is needed.
+//
+// Transposing read, per 16-lane group: lane L receives element (L & 3) of the
+// 8 bytes read by lane 4 e + (L >> 2), for e = 0..3. If lane s of the group
+// reads row R + (s >> 2), columns C + 4 (s & 3) .. + 3, lane L therefore
+// receives column C + L of rows R .. R + 3: a 4 x 16 block arrives
+// transposed.
+#pragma once
+#include "common.hpp"
+
+namespace gt {
+
+constexpr int kTileRows = 64;
+
+// XOR swizzle of the 16-byte chunks of a tile row. Chosen (by exhaustive
+// search over XORs of up to two row bits per chunk bit) so that the tile
+// store (8 lanes per row), the row-operand reads (rows perm32(lane)) and the
+// transposing reads (4 rows x 4 column groups per 16 lanes) are all free of
+// bank conflicts, for a 64-bank LDS in 16-lane groups and a 32-bank LDS in
+// 8-lane groups. Row bits 3 and 5 are not used, so rows 8 and 32 apart share
+// one per-lane address pattern (their offsets are immediates).
+template <int D>
+__device__ __forceinline__ int swz_tile(int row, int chunk) {
+  if constexpr (D == 64)
+    return chunk ^ (((row >> 1) & 1) | (((row ^ (row >> 2)) & 1) << 1) |
+                    ((((row >> 1) ^ (row >> 4)) & 1) << 2));
+  else
+    return chunk ^ (((row >> 4) & 1) | ((((row >> 1) ^ (row >> 2)) & 1) << 1));
+}
+
+// Raw buffer resource over exactly nbytes: loads past the end return 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc_n(const void* base, int64_t nbytes) {
+  const int n = (int)(nbytes < 0x7fffffff ? nbytes : 0x7fffffff);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+
+// Resource over rows [r0, min(r0 + 64, nrows)) of a row-major [nrows, D]
+// bf16 tensor: the tile's rows past nrows read as zero.
+template <int D>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* t, int64_t r0, int64_t nrows) {
+  const int64_t rows = nrows - r0 < kTileRows ? nrows - r0 : kTileRows;
+  return make_rsrc_n(t + r0 * D, rows * D * 2);
+}
+
+__device__ __forceinline__ uint4 buf_b128(__amdgpu_buffer_rsrc_t r, uint32_t voff) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// One tensor's tile in flight: NT threads, 16 bytes per item, item u =
+// row u / (D/8), chunk u % (D/8). A tile is contiguous in global memory, so
+// item u sits at byte 16 u of it.
+template <int D, int NT>
+struct RowStage {
+  static constexpr int CPR = D / 8;
+  static constexpr int ITEMS = kTileRows * CPR;
+  static constexpr int IPT = ITEMS / NT;
+  static_assert(ITEMS % NT == 0, "tile items must divide evenly");
+  uint4 r[IPT];
+
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs) {
+#pragma unroll
+    for (int s = 0; s < IPT; ++s) r[s] = buf_b128(rs, (uint32_t)(threadIdx.x + s * NT) * 16u);
+  }
+  // LDS element offset of this thread's item s.
+  __device__ __forceinline__ static int lds_off(int s) {
+    const int u = (int)threadIdx.x + s * NT;
+    const int row = u / CPR;
+    return row * D + swz_tile<D>(row, u % CPR) * 8;
+  }
+  __device__ __forceinline__ void store(uint16_t* tile) {
+#pragma unroll
+    for (int s = 0; s < IPT; ++s) {
+      uint4 v = r[s];
+      opaque(v);
+      *reinterpret_cast<uint4*>(tile + lds_off(s)) = v;
+    }
+  }
+};
+
+// Per-lane element offset of the row-operand read of rows perm32(lane & 31)
+// (+ 32 sb as an immediate), feature chunk 2 kc + (lane >> 5).
+template <int D>
+__device__ __forceinline__ int row_operand_off(int kc) {
+  const int lane = threadIdx.x & 63;
+  const int row = perm32(lane & 31);
+  return row * D + swz_tile<D>(row, 2 * kc + (lane >> 5)) * 8;
+}
+
+// Per-lane element offset of transposing read h (0, 1) for output rows
+// (features) 32 cb .. 32 cb + 31: the lane half g covers tile rows
+// 16 g + 4 h .. + 3 (+ 8 q + 32 sb as immediates).
+template <int D>
+__device__ __forceinline__ int tr_operand_off(int h, int cb) {
+  const int lane = threadIdx.x & 63;
+  const int s = lane & 15;
+  const int row = 16 * (lane >> 5) + 4 * h + (s >> 2);
+  const int col = 32 * cb + 16 * ((lane >> 4) & 1) + 4 * (s & 3);
+  return row * D + swz_tile<D>(row, col >> 3) * 8 + (col & 4);
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ s16x4 lds_tr16(const uint16_t* p) {
+  typedef __attribute__((address_space(3))) s16x4* lds_ptr;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_ptr)(uint16_t*)p);
+}
+
+// A-operand of a 32x32x16 product whose rows are tile COLUMNS 32 cb + (lane
+// & 31) and whose k index 8 g + j (g = lane >> 5) is tile row base + 16 g + j
+// (base = 8 q + 32 sb): the transposed view of the tile, two reads.
+__device__ __forceinline__ bf16x8 lds_tr_operand(const uint16_t* tile, int off0, int off1) {
+  const s16x4 a = lds_tr16(tile + off0);
+  const s16x4 b = lds_tr16(tile + off1);
+  const s16x8 c = __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, c);
+}
+
+}  // namespace gt
