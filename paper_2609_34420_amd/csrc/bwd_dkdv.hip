@@ -24,12 +24,15 @@
 // in 64 bits. The histogram is flushed once per workgroup, converted back
 // to fp32, with one global atomic per bucket.
 //
-// Query tiles (Q, dO in both layouts, statistics) are double buffered in
-// LDS: the next tile's global loads are in flight while the current one is
-// computed, one barrier per tile. spd bytes are fetched one 32-query
-// sub-block ahead of their use.
+// Query tiles (Q and dO row-major, statistics) are double buffered in LDS;
+// Q^T and dO^T are read with transposing LDS reads. The next tile's global
+// loads are in flight while the current one is computed, one barrier per
+// tile. spd bytes are fetched one 32-query sub-block ahead of their use.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
+#include "stage.hpp"
 
 namespace gt {
 
@@ -42,92 +45,74 @@ constexpr int kThreads = kNW * 64;
 constexpr int kCopies = 16;                 // table / histogram copies (lane & 15)
 constexpr int kTabEntries = 256 * kCopies;
 
+// All LDS of the kernel in one block, table and histogram first: their
+// offsets stay below 64 KiB, so the one per-element address register serves
+// both with immediate offsets.
 template <int D>
 struct DkdvSmem {
+  uint2 tabw[kTabEntries];                // table copies (fp32 bits, 8-byte stride)
+  unsigned long long hist[kTabEntries];   // gradient histogram copies, same index
   uint16_t q[2][kBQ * D];
   uint16_t o[2][kBQ * D];
-  uint16_t qt[2][D * kBQ];
-  uint16_t ot[2][D * kBQ];
   float init_s[2][kBQ];             // -LSE log2 e / (scale log2 e); -inf for empty rows
-  float init_p[2][kBQ];             // -Dlt
+  float init_p[2][kBQ];             // -Dlt 2^F
+  float red[2][kNW];
 };
 
-struct StageRegs {
-  uint4 v0, v1;
-  float stat;
-};
-
-// Global -> registers for the query tile at i0. Rows past N read the clamped
-// row N-1 (unconditional loads); stage_store() zeroes them.
-template <int D, bool QFULL>
-__device__ __forceinline__ void stage_load(const BwdArgs& a, const uint16_t* qh, const uint16_t* oh,
-                                           const float* lse2h, const float* dlth, int64_t i0,
-                                           StageRegs& r) {
-  constexpr int CPR = D / 8;
-  constexpr int ITEMS = 32 * CPR;   // row pairs x 16-byte chunks, per tensor
-  // Every thread loads (threads past the work items repeat one), so no
-  // wave skips a load and the loads in flight are the same on every path.
-  const int t = (2 * ITEMS >= kThreads) ? (int)threadIdx.x : (int)threadIdx.x % (2 * ITEMS);
-  {
-    const int u = t % ITEMS;
-    const int ip = u % 32, cc = u / 32;
-    const uint16_t* src = (t < ITEMS) ? qh : oh;
-    const int64_t row = i0 + 2 * ip;
-    const int64_t r0 = (QFULL || row < a.N) ? row : a.N - 1;
-    const int64_t r1 = (QFULL || row + 1 < a.N) ? row + 1 : a.N - 1;
-    r.v0 = *reinterpret_cast<const uint4*>(src + r0 * D + cc * 8);
-    r.v1 = *reinterpret_cast<const uint4*>(src + r1 * D + cc * 8);
+// Per-lane LDS element offsets of the operand reads (tile-relative; the
+// 32-query sub-block and 8-query step offsets are immediates).
+template <int D>
+struct DkdvOffsets {
+  int row[D / 16];        // Q / dO rows perm32(lane), feature chunk 2 kc + g
+  int tr[2][D / 32];      // transposing reads h = 0, 1, feature block cb
+  __device__ __forceinline__ DkdvOffsets() {
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) row[kc] = row_operand_off<D>(kc);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int cb = 0; cb < D / 32; ++cb) tr[h][cb] = tr_operand_off<D>(h, cb);
   }
-  {
+};
+
+// A query tile in flight: Q and dO rows (rows past N read as zero) and the
+// statistics of its 64 queries.
+template <int D>
+struct QTileStage {
+  RowStage<D, kThreads> q, o;
+  float stat;
+
+  __device__ __forceinline__ void load(const uint16_t* qh, const uint16_t* oh, const float* lse2h,
+                                       const float* dlth, int64_t i0, int64_t n) {
+    q.load(tile_rsrc<D>(qh, i0, n));
+    o.load(tile_rsrc<D>(oh, i0, n));
+    // every thread loads (two copies of the 128 values), clamped to row N-1
     const int ts = (int)threadIdx.x & (2 * kBQ - 1);
     const int64_t i = i0 + (ts & (kBQ - 1));
-    const int64_t ic = (QFULL || i < a.N) ? i : a.N - 1;
-    r.stat = (ts < kBQ ? lse2h : dlth)[ic];
+    const int64_t ic = i < n ? i : n - 1;
+    stat = (ts < kBQ ? lse2h : dlth)[ic];
   }
-}
-
-// Registers -> LDS buffer `buf`: Q and dO row-major and transposed, and the
-// accumulator starts of S (-lse2 / (scale log2 e), -inf for padded rows so
-// that P = 0) and of the scaled dP (-Dlt 2^F).
-template <int D, bool QFULL>
-__device__ __forceinline__ void stage_store(DkdvSmem<D>& sm, int buf, StageRegs r, int64_t i0,
-                                            int64_t n, float inv_sl2, float sF) {
-  constexpr int CPR = D / 8;
-  constexpr int ITEMS = 32 * CPR;
-  const int t = threadIdx.x;
-  const bool tail = !QFULL && i0 + kBQ > n;
-  if (t < 2 * ITEMS) {
-    const int u = t % ITEMS;
-    const int ip = u % 32, cc = u / 32;
-    uint16_t* rm = (t < ITEMS) ? sm.q[buf] : sm.o[buf];
-    uint16_t* tr = (t < ITEMS) ? sm.qt[buf] : sm.ot[buf];
-    const int row = 2 * ip;
-    opaque(r.v0);
-    opaque(r.v1);
-    if (tail) {
-      if (i0 + row >= n) r.v0 = make_uint4(0, 0, 0, 0);
-      if (i0 + row + 1 >= n) r.v1 = make_uint4(0, 0, 0, 0);
-    }
-    *reinterpret_cast<uint4*>(rm + row * D + swz_rows<D>(row, cc) * 8) = r.v0;
-    *reinterpret_cast<uint4*>(rm + (row + 1) * D + swz_rows<D>(row + 1, cc) * 8) = r.v1;
-    const uint16_t* p0 = reinterpret_cast<const uint16_t*>(&r.v0);
-    const uint16_t* p1 = reinterpret_cast<const uint16_t*>(&r.v1);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int crow = cc * 8 + e;
-      *reinterpret_cast<uint32_t*>(tr + crow * kBQ + swz_t64(crow, row >> 3) * 8 + (row & 7)) =
-          (uint32_t)p0[e] | ((uint32_t)p1[e] << 16);
+  // Registers -> LDS buffer BUF, with the accumulator starts of S
+  // (-lse2 / (scale log2 e), -inf for padded rows so that P = 0) and of the
+  // scaled dP (-Dlt 2^F).
+  template <int BUF>
+  __device__ __forceinline__ void store(DkdvSmem<D>& sm, int64_t i0, int64_t n, float inv_sl2,
+                                        float sF) {
+    q.store(sm.q[BUF]);
+    o.store(sm.o[BUF]);
+    const int t = threadIdx.x;
+    if (t < 2 * kBQ) {
+      float st = stat;
+      opaque_f(st);
+      const int qi = t & (kBQ - 1);
+      const bool in = i0 + qi < n;
+      if (t < kBQ)
+        sm.init_s[BUF][qi] = in ? -st * inv_sl2 : -INFINITY;
+      else
+        sm.init_p[BUF][qi] = in ? -st * sF : 0.0f;
     }
   }
-  if (t < 2 * kBQ) {
-    const int q = t & (kBQ - 1);
-    const bool in = QFULL || i0 + q < n;
-    if (t < kBQ)
-      sm.init_s[buf][q] = in ? -r.stat * inv_sl2 : -INFINITY;
-    else
-      sm.init_p[buf][q] = in ? -r.stat * sF : 0.0f;
-  }
-}
+};
 
 // spd bytes of this lane's key for the 16 queries i_base + 16 g + r, by raw
 // buffer loads: a scalar base per sub-block, scalar row offsets r * ld and a
@@ -162,22 +147,21 @@ __device__ __forceinline__ int round_to_int(float x) {
   return r;
 }
 
-template <int D, bool KTAIL>
-__device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const uint2* tabw,
-                                              unsigned long long* hist, int buf, int qs,
+template <int D, bool KTAIL, int BUF, int QS>
+__device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const DkdvOffsets<D>& off,
                                               const bf16x8* kf, const bf16x8* vf,
                                               const uint8_t* b, float sl2, bool jok,
                                               f32x16* dk, f32x16* dv) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
   const int lane = threadIdx.x & 63;
-  const int col = lane & 31, g = lane >> 5;
-  const int ib = qs * 32 + 16 * g;   // this lane half's first query in the tile
+  const int g = lane >> 5;
+  const int ib = QS * 32 + 16 * g;   // this lane half's first query in the tile
 
   f32x16 s, dp;
   {
-    const float4* is4 = reinterpret_cast<const float4*>(&sm.init_s[buf][ib]);
-    const float4* ip4 = reinterpret_cast<const float4*>(&sm.init_p[buf][ib]);
+    const float4* is4 = reinterpret_cast<const float4*>(&sm.init_s[BUF][ib]);
+    const float4* ip4 = reinterpret_cast<const float4*>(&sm.init_p[BUF][ib]);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const float4 x = is4[u], y = ip4[u];
@@ -185,12 +169,10 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const uint2* tabw
       dp[4 * u] = y.x; dp[4 * u + 1] = y.y; dp[4 * u + 2] = y.z; dp[4 * u + 3] = y.w;
     }
   }
-  const int qrow = qs * 32 + perm32(col);
 #pragma unroll
   for (int kc = 0; kc < NKC; ++kc) {
-    const int off = qrow * D + swz_rows<D>(qrow, kc * 2 + g) * 8;
-    s = mfma32(lds_b128(sm.q[buf] + off), kf[kc], s);
-    dp = mfma32(lds_b128(sm.o[buf] + off), vf[kc], dp);
+    s = mfma32(lds_b128(sm.q[BUF] + QS * 32 * D + off.row[kc]), kf[kc], s);
+    dp = mfma32(lds_b128(sm.o[BUF] + QS * 32 * D + off.row[kc]), vf[kc], dp);
   }
   // Lane: key; registers r: queries. dp holds (dO.V - Dlt) 2^F, so ds below
   // is dS 2^F.
@@ -203,7 +185,7 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const uint2* tabw
     uint32_t bk = b[r];
     opaque(bk);                                    // keep the byte's wait here
     idx[r] = (bk << 4) | cpy;                      // copy cpy of bucket b
-    tb[r] = __uint_as_float(tabw[idx[r]].x);
+    tb[r] = __uint_as_float(sm.tabw[idx[r]].x);
   }
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
@@ -215,25 +197,23 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const uint2* tabw
   }
 #pragma unroll
   for (int r = 0; r < 16; ++r)
-    atomicAdd(&hist[idx[r]], (unsigned long long)(long long)round_to_int(ds[r]));
+    atomicAdd(&sm.hist[idx[r]], (unsigned long long)(long long)round_to_int(ds[r]));
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const bf16x8 pb = cvt_bf16x8(p + 8 * q);
     const bf16x8 db = cvt_bf16x8(ds + 8 * q);
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
-      const int crow = cb * 32 + col;
-      const int off = crow * kBQ + swz_t64(crow, (ib >> 3) + q) * 8;
-      dv[cb] = mfma32(lds_b128(sm.ot[buf] + off), pb, dv[cb]);
-      dk[cb] = mfma32(lds_b128(sm.qt[buf] + off), db, dk[cb]);
+      const int base = (QS * 32 + 8 * q) * D;
+      dv[cb] = mfma32(lds_tr_operand(sm.o[BUF] + base, off.tr[0][cb], off.tr[1][cb]), pb, dv[cb]);
+      dk[cb] = mfma32(lds_tr_operand(sm.q[BUF] + base, off.tr[0][cb], off.tr[1][cb]), db, dk[cb]);
     }
   }
 }
 
 template <int D, bool KTAIL, bool QFULL>
-__device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, const uint2* tabw,
-                                          unsigned long long* hist, int h, int64_t key0, int64_t j,
-                                          bool jok, int fexp) {
+__device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, int h, int64_t key0,
+                                          int64_t j, bool jok, int fexp) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
   const int lane = threadIdx.x & 63;
@@ -272,33 +252,40 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, con
   const uint32_t key_off = (uint32_t)(jc - key0);
   const uint8_t* spd_cols = a.spd + key0;
   const int64_t ntiles = (a.N + kBQ - 1) / kBQ;
+  const DkdvOffsets<D> off;
 
-  StageRegs st;
-  stage_load<D, QFULL>(a, qh, oh, lse2h, dlth, 0, st);
+  QTileStage<D> st;
+  st.load(qh, oh, lse2h, dlth, 0, a.N);
   uint8_t bA[16], bB[16];
   load_bytes<QFULL>(spd_cols, ld, 0, a.N, key_off, bA);
-  stage_store<D, QFULL>(sm, 0, st, 0, a.N, inv_sl2, sF);
+  st.template store<0>(sm, 0, a.N, inv_sl2, sF);
   wait_loads();
   __syncthreads();
 
-  for (int64_t t = 0; t < ntiles; ++t) {
-    const int buf = (int)(t & 1);
+  // One query tile on buffer BUF: the prefetches are unconditional (the last
+  // tile re-reads itself), so every path has the same loads in flight and
+  // the waits before each use stay exact.
+  auto step = [&](int64_t t, auto bufc) {
+    constexpr int BUF = decltype(bufc)::value;
     const int64_t i0 = t * kBQ;
     const bool more = t + 1 < ntiles;
-    // The prefetches are unconditional (the last tile re-reads itself), so
-    // every path through the loop has the same loads in flight and the
-    // waits before each use stay exact.
     const int64_t inext = more ? i0 + kBQ : i0;
     load_bytes<QFULL>(spd_cols, ld, i0 + 32, a.N, key_off, bB);
-    stage_load<D, QFULL>(a, qh, oh, lse2h, dlth, inext, st);
+    st.load(qh, oh, lse2h, dlth, inext, a.N);
     sched_fence();
-    dkdv_subblock<D, KTAIL>(sm, tabw, hist, buf, 0, kf, vf, bA, sl2, jok, dk, dv);
+    dkdv_subblock<D, KTAIL, BUF, 0>(sm, off, kf, vf, bA, sl2, jok, dk, dv);
     load_bytes<QFULL>(spd_cols, ld, inext, a.N, key_off, bA);
     sched_fence();
-    dkdv_subblock<D, KTAIL>(sm, tabw, hist, buf, 1, kf, vf, bB, sl2, jok, dk, dv);
-    if (more) stage_store<D, QFULL>(sm, buf ^ 1, st, i0 + kBQ, a.N, inv_sl2, sF);
+    dkdv_subblock<D, KTAIL, BUF, 1>(sm, off, kf, vf, bB, sl2, jok, dk, dv);
+    if (more) st.template store<BUF ^ 1>(sm, inext, a.N, inv_sl2, sF);
     __syncthreads();
+  };
+  int64_t t = 0;
+  for (; t + 1 < ntiles; t += 2) {
+    step(t, std::integral_constant<int, 0>());
+    step(t + 1, std::integral_constant<int, 1>());
   }
+  if (t < ntiles) step(t, std::integral_constant<int, 0>());
 
   const float dk_scale = a.scale * ldexpf(1.0f, -fexp);
   if (jok) {
@@ -324,12 +311,9 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, con
 template <int D, bool QFULL>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) DkdvSmem<D> sm;
-  // Table copies (fp32 bits, 8-byte stride) and histogram copies (int64) in
-  // separate arrays with the same index: the bias reads never alias the
-  // gradient adds and share one address register.
-  __shared__ uint2 tabw[kTabEntries];
-  __shared__ unsigned long long hist[kTabEntries];
-  __shared__ float red[2][kNW];
+  uint2* tabw = sm.tabw;
+  unsigned long long* hist = sm.hist;
+  float (*red)[kNW] = sm.red;
   const int tid = threadIdx.x;
   const int wave = wave_id(), col = tid & 31;
   const int64_t nkb = (a.N + kBK - 1) / kBK;
@@ -383,9 +367,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   }
 
   if ((kblk + 1) * kBK <= a.N)
-    dkdv_main<D, false, QFULL>(a, sm, tabw, hist, h, kblk * kBK, j, jok, fexp);
+    dkdv_main<D, false, QFULL>(a, sm, h, kblk * kBK, j, jok, fexp);
   else
-    dkdv_main<D, true, QFULL>(a, sm, tabw, hist, h, kblk * kBK, j, jok, fexp);
+    dkdv_main<D, true, QFULL>(a, sm, h, kblk * kBK, j, jok, fexp);
 
   __syncthreads();
   const double unscale = ldexp(1.0, -fexp);

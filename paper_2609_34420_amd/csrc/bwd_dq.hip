@@ -3,12 +3,15 @@
 // Same layout as the forward: each wave owns 32*QB queries, computes
 // S^T = K Q^T and dP^T = V dO^T with the queries on the lanes, forms
 // dS^T = P^T * (dP^T - Dlt) from the saved log-sum-exp, and accumulates
-// dQ^T += K^T dS^T with dS^T straight from registers. K (row-major and
-// transposed) and V tiles are double buffered in LDS and the next tile's
-// global loads and spd bytes are in flight while the current one computes.
+// dQ^T += K^T dS^T with dS^T straight from registers. K and V tiles are
+// double buffered row-major in LDS (K^T is read with transposing LDS reads)
+// and the next tile's global loads and spd bytes are in flight while the
+// current one computes.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
-#include "tiles.hpp"
+#include "stage.hpp"
 
 namespace gt {
 
@@ -21,9 +24,28 @@ constexpr int kBC = 64;
 // One key tile for every query block of the wave. The accumulators of S^T
 // and dP^T start at -lse2 / (scale log2 e) and -Dlt, so per score element the
 // vector work is the bias FMA, exp2, one multiply and the bf16 conversion.
+// Per-lane LDS element offsets (tile-relative; 32-key block and 8-key step
+// offsets are immediates). K and V rows share one pattern.
+template <int D>
+struct DqOffsets {
+  int row[D / 16];        // rows perm32(lane), feature chunk 2 kc + g
+  int kt[2][D / 32];      // transposing reads h = 0, 1 of K, feature block cb
+  __device__ __forceinline__ DqOffsets() {
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) row[kc] = row_operand_off<D>(kc);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int cb = 0; cb < D / 32; ++cb) kt[h][cb] = tr_operand_off<D>(h, cb);
+  }
+};
+
+// One key tile for every query block of the wave. The accumulators of S^T
+// and dP^T start at -lse2 / (scale log2 e) and -Dlt, so per score element the
+// vector work is the bias FMA, exp2, one multiply and the bf16 conversion.
 template <int D, int QB, bool MASK>
-__device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sKt, const uint16_t* sV,
-                                        const float* sT, const bf16x8 (&qf)[QB][D / 16],
+__device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sV, const float* sT,
+                                        const DqOffsets<D>& off, const bf16x8 (&qf)[QB][D / 16],
                                         const bf16x8 (&df)[QB][D / 16], const f32x16 (&init_s)[QB],
                                         const f32x16 (&init_p)[QB],
                                         const uint32_t (&w)[QB][kBC / 32][4], int64_t j0,
@@ -32,7 +54,7 @@ __device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sKt,
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
   const int lane = threadIdx.x & 63;
-  const int col = lane & 31, g = lane >> 5;
+  const int g = lane >> 5;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
@@ -41,12 +63,10 @@ __device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sKt,
 #pragma unroll
       for (int r = 0; r < 16; ++r) tb[r] = sT[(w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu];
       f32x16 s = init_s[qb], dp = init_p[qb];
-      const int krow = kb * 32 + perm32(col);
 #pragma unroll
       for (int kc = 0; kc < NKC; ++kc) {
-        const int off = krow * D + swz_rows<D>(krow, kc * 2 + g) * 8;
-        s = mfma32(lds_b128(sK + off), qf[qb][kc], s);
-        dp = mfma32(lds_b128(sV + off), df[qb][kc], dp);
+        s = mfma32(lds_b128(sK + kb * 32 * D + off.row[kc]), qf[qb][kc], s);
+        dp = mfma32(lds_b128(sV + kb * 32 * D + off.row[kc]), df[qb][kc], dp);
       }
       float ds[16];
 #pragma unroll
@@ -60,12 +80,10 @@ __device__ __forceinline__ void dq_tile(const uint16_t* sK, const uint16_t* sKt,
         const bf16x8 db = cvt_bf16x8(ds + 8 * q);
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
-          const int crow = cb * 32 + col;
-          acc[qb][cb] = mfma32(lds_b128(sKt + crow * kBC + swz_t64(crow, kb * 4 + 2 * g + q) * 8), db,
-                               acc[qb][cb]);
+          const uint16_t* kt = sK + (kb * 32 + 8 * q) * D;
+          acc[qb][cb] = mfma32(lds_tr_operand(kt, off.kt[0][cb], off.kt[1][cb]), db, acc[qb][cb]);
         }
       }
-      __builtin_amdgcn_sched_barrier(0);
     }
   }
 }
@@ -78,10 +96,10 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
   constexpr int BR = kWaves * 32 * QB;
-  using Stager = KVStager<D, kThreads, true, true, true, false>;
+  using Stage = RowStage<D, kThreads>;
+  static_assert(kBC == kTileRows, "key tile is one staged tile");
 
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBC * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sKt[2][D * kBC];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][kBC * D];
   __shared__ float sT[256];
 
@@ -157,40 +175,54 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
   };
 
   const int64_t ntiles = (a.N + kBC - 1) / kBC;
-  Stager st;
-  uint32_t wc[QB][KB][4];
-  st.load(kh, vh, 0, a.N);
-  fetch_spd(0, wc);
-  if (kBC > a.N) st.mask_tail(0, a.N);
-  st.store(sK[0], sKt[0], sV[0], nullptr);
+  const DqOffsets<D> off;
+  Stage stK, stV;
+  uint32_t wA[QB][KB][4], wB[QB][KB][4];   // spd words of even / odd tiles
+  stK.load(tile_rsrc<D>(kh, 0, a.N));
+  stV.load(tile_rsrc<D>(vh, 0, a.N));
+  fetch_spd(0, wA);
+  stK.store(sK[0]);
+  stV.store(sV[0]);
   wait_loads();
   __syncthreads();
 
-  for (int64_t t = 0; t < ntiles; ++t) {
-    const int buf = (int)(t & 1);
+  // One key tile: prefetch the next (the last tile re-reads itself, so the
+  // loads in flight are the same on every path), compute on buffer BUF,
+  // stage the prefetch into the other buffer.
+  auto step = [&](int64_t t, auto bufc, auto maskc) {
+    constexpr int BUF = decltype(bufc)::value;
+    constexpr bool MASK = decltype(maskc)::value;
+    auto& wcur = BUF ? wB : wA;
+    auto& wnext = BUF ? wA : wB;
     const int64_t j0 = t * kBC;
     const bool more = t + 1 < ntiles;
-    uint32_t wn[QB][KB][4];
-    if (more) {
-      st.load(kh, vh, j0 + kBC, a.N);
-      fetch_spd(j0 + kBC, wn);
-    }
+    const int64_t jn = more ? j0 + kBC : j0;
+    stK.load(tile_rsrc<D>(kh, jn, a.N));
+    stV.load(tile_rsrc<D>(vh, jn, a.N));
+    fetch_spd(jn, wnext);
     sched_fence();
-    if (FULL || j0 + kBC <= a.N)
-      dq_tile<D, QB, false>(sK[buf], sKt[buf], sV[buf], sT, qf, df, init_s, init_p, wc, j0, a.N, sl2, acc);
-    else
-      dq_tile<D, QB, true>(sK[buf], sKt[buf], sV[buf], sT, qf, df, init_s, init_p, wc, j0, a.N, sl2, acc);
+    dq_tile<D, QB, MASK>(sK[BUF], sV[BUF], sT, off, qf, df, init_s, init_p, wcur, j0, a.N, sl2, acc);
     if (more) {
-      if (!FULL && j0 + 2 * kBC > a.N) st.mask_tail(j0 + kBC, a.N);
-      st.store(sK[buf ^ 1], sKt[buf ^ 1], sV[buf ^ 1], nullptr);
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) wc[qb][kb][e] = wn[qb][kb][e];
+      stK.store(sK[BUF ^ 1]);
+      stV.store(sV[BUF ^ 1]);
     }
     __syncthreads();
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  using Full = std::false_type;
+  using Part = std::true_type;
+  const int64_t nfull = FULL ? ntiles : a.N / kBC;
+  int64_t t = 0;
+  for (; t + 1 < nfull; t += 2) {
+    step(t, B0(), Full());
+    step(t + 1, B1(), Full());
+  }
+  if (t < nfull) {
+    step(t, B0(), Full());
+    if (!FULL && t + 1 < ntiles) step(t + 1, B1(), Part());
+  } else if (!FULL && t < ntiles) {
+    step(t, B0(), Part());
   }
 
 #pragma unroll

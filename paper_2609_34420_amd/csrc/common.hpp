@@ -39,6 +39,7 @@ __device__ __forceinline__ void opaque(uint4& x) {
   asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
 }
 __device__ __forceinline__ void opaque(uint32_t& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void opaque_f(float& x) { asm volatile("" : "+v"(x)); }
 
 // Wait for every outstanding vector-memory load (s_waitcnt vmcnt(0) with the
 // other counters left free). Used once before a software-pipelined loop, so

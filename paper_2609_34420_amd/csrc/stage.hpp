@@ -56,31 +56,38 @@ __device__ __forceinline__ uint4 buf_b128(__amdgpu_buffer_rsrc_t r, uint32_t vof
 
 // One tensor's tile in flight: NT threads, 16 bytes per item, item u =
 // row u / (D/8), chunk u % (D/8). A tile is contiguous in global memory, so
-// item u sits at byte 16 u of it.
+// item u sits at byte 16 u of it. With fewer items than threads, the extra
+// threads load a duplicate (so every wave issues the same loads) and store
+// nothing.
 template <int D, int NT>
 struct RowStage {
   static constexpr int CPR = D / 8;
   static constexpr int ITEMS = kTileRows * CPR;
-  static constexpr int IPT = ITEMS / NT;
-  static_assert(ITEMS % NT == 0, "tile items must divide evenly");
+  static constexpr int IPT = ITEMS >= NT ? ITEMS / NT : 1;
+  static_assert(ITEMS % NT == 0 || NT % ITEMS == 0, "tile items must divide evenly");
   uint4 r[IPT];
 
+  __device__ __forceinline__ static int item(int s) {
+    return ITEMS >= NT ? (int)threadIdx.x + s * NT : (int)threadIdx.x % ITEMS;
+  }
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs) {
 #pragma unroll
-    for (int s = 0; s < IPT; ++s) r[s] = buf_b128(rs, (uint32_t)(threadIdx.x + s * NT) * 16u);
+    for (int s = 0; s < IPT; ++s) r[s] = buf_b128(rs, (uint32_t)item(s) * 16u);
   }
   // LDS element offset of this thread's item s.
   __device__ __forceinline__ static int lds_off(int s) {
-    const int u = (int)threadIdx.x + s * NT;
+    const int u = item(s);
     const int row = u / CPR;
     return row * D + swz_tile<D>(row, u % CPR) * 8;
   }
   __device__ __forceinline__ void store(uint16_t* tile) {
+    if (ITEMS >= NT || (int)threadIdx.x < ITEMS) {
 #pragma unroll
-    for (int s = 0; s < IPT; ++s) {
-      uint4 v = r[s];
-      opaque(v);
-      *reinterpret_cast<uint4*>(tile + lds_off(s)) = v;
+      for (int s = 0; s < IPT; ++s) {
+        uint4 v = r[s];
+        opaque(v);
+        *reinterpret_cast<uint4*>(tile + lds_off(s)) = v;
+      }
     }
   }
 };
