@@ -55,6 +55,10 @@ struct FwdOffsets {
   }
 };
 
+// Both 32-key blocks' score products are issued before the first block's
+// softmax, so the matrix cores work on block 1 while the vector ALUs work on
+// block 0. A reference move in block 0 shifts the already computed block-1
+// scores by the same amount.
 template <int D, int QB, bool MASK>
 __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV, const float* sT,
                                          const FwdOffsets<D>& off,
@@ -69,18 +73,23 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
   const int g = lane >> 5;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
+    f32x16 s[KB];
+    float tb[KB][16];
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      float tb[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) tb[r] = sT[(w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu];
-      f32x16 s = st[qb].init;
+      for (int r = 0; r < 16; ++r) tb[kb][r] = sT[(w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu];
+      s[kb] = st[qb].init;
 #pragma unroll
-      for (int kc = 0; kc < NKC; ++kc) s = mfma32(lds_b128(sK + kb * 32 * D + off.k[kc]), qf[qb][kc], s);
+      for (int kc = 0; kc < NKC; ++kc)
+        s[kb] = mfma32(lds_b128(sK + kb * 32 * D + off.k[kc]), qf[qb][kc], s[kb]);
+    }
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
       float x[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float xv = fmaf(s[r], sl2, tb[r]);
+        const float xv = fmaf(s[kb][r], sl2, tb[kb][r]);
         if constexpr (MASK)
           x[r] = (j0 + kb * 32 + 16 * g + r < Sk) ? xv : -INFINITY;
         else
@@ -105,6 +114,12 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
         const float shift = msafe_new - msafe_old;
 #pragma unroll
         for (int r = 0; r < 16; ++r) x[r] -= shift;
+        // later blocks of this tile were started from the old reference
+        const float ds = shift * inv_sl2;
+#pragma unroll
+        for (int kb2 = kb + 1; kb2 < KB; ++kb2)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s[kb2][r] -= ds;
         st[qb].m = mnew;
         const float iv = -msafe_new * inv_sl2;
 #pragma unroll
@@ -137,11 +152,13 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
   constexpr int BR = kWaves * 32 * QB;
-  using Stage = RowStage<D, kThreads>;
+  using Dma = TileDma<D, kWaves>;     // K and V
   static_assert(kBC == kTileRows, "key tile is one staged tile");
 
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kBC * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][kBC * D];
+  // Three-stage ring of K / V tiles, one array per stage so that no read of
+  // one stage can be taken to alias the copy into another.
+  __shared__ __attribute__((aligned(16))) uint16_t sK0[kBC * D], sK1[kBC * D], sK2[kBC * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sV0[kBC * D], sV1[kBC * D], sV2[kBC * D];
   __shared__ float sT[256];
 
   const int tid = threadIdx.x;
@@ -214,57 +231,65 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
 
   const int64_t ntiles = (a.Sk + kBC - 1) / kBC;
   const FwdOffsets<D> off;
-  Stage stK, stV;
-  uint32_t wA[QB][KB][4], wB[QB][KB][4];   // spd words of even / odd tiles
-  if (ntiles > 0) {
-    stK.load(tile_rsrc<D>(kh, 0, a.Sk));
-    stV.load(tile_rsrc<D>(vh, 0, a.Sk));
-    fetch_spd(0, wA);
-    stK.store(sK[0]);
-    stV.store(sV[0]);
-  }
-  wait_loads();
-  __syncthreads();
+  const Dma dma(wave);
+  uint32_t w0[QB][KB][4], w1[QB][KB][4], w2[QB][KB][4];   // spd words, by tile % 3
 
-  // One key tile: prefetch the next tile (the last tile re-reads itself, so
-  // the loads in flight are the same on every path), compute on buffer BUF,
-  // then stage the prefetch into the other buffer.
-  auto step = [&](int64_t t, auto bufc, auto maskc) {
-    constexpr int BUF = decltype(bufc)::value;
+  // Copy tile t (clamped to the last tile) into stage s and fetch its spd
+  // words: Dma::NLOADS + SPD_LOADS vector-memory ops per wave.
+  constexpr int SPD_LOADS = QB * KB;
+#define GT_FWD_ISSUE(t_, S_)                                                                    \
+  {                                                                                            \
+    const int64_t j_ = ((t_) < ntiles ? (t_) : ntiles - 1) * kBC;                              \
+    dma.load(tile_rsrc<D>(kh, j_, a.Sk), tile_rsrc<D>(vh, j_, a.Sk),                          \
+             (S_) == 0 ? sK0 : ((S_) == 1 ? sK1 : sK2), (S_) == 0 ? sV0 : ((S_) == 1 ? sV1 : sV2)); \
+    fetch_spd(j_, (S_) == 0 ? w0 : ((S_) == 1 ? w1 : w2));                                    \
+  }
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  if (ntiles > 0) {
+    GT_FWD_ISSUE(0, 0)
+    GT_FWD_ISSUE(1, 1)
+  }
+  __syncthreads();     // table, and the copy of tile 0 (waits for every load)
+
+  // Tile t from stage S = t % 3: copy tile t + 2 into stage (S + 2) % 3
+  // (last read in step t - 1, before that step's barrier), compute, then
+  // wait until this wave's copy of tile t + 1 has landed (only the spd
+  // words of tile t + 1 and this step's loads may still be in flight) and
+  // meet the other waves at the barrier.
+  auto step = [&](int64_t t, auto stagec, auto maskc) {
+    constexpr int S = decltype(stagec)::value;
     constexpr bool MASK = decltype(maskc)::value;
-    auto& wcur = BUF ? wB : wA;
-    auto& wnext = BUF ? wA : wB;
-    const int64_t j0 = t * kBC;
-    const bool more = t + 1 < ntiles;
-    const int64_t jn = more ? j0 + kBC : j0;
-    stK.load(tile_rsrc<D>(kh, jn, a.Sk));
-    stV.load(tile_rsrc<D>(vh, jn, a.Sk));
-    fetch_spd(jn, wnext);
+    GT_FWD_ISSUE(t + 2, (S + 2) % 3)
     sched_fence();
-    fwd_tile<D, QB, MASK>(sK[BUF], sV[BUF], sT, off, qf, wcur, j0, a.Sk, sl2, inv_sl2, sm, acc);
-    if (more) {
-      stK.store(sK[BUF ^ 1]);
-      stV.store(sV[BUF ^ 1]);
-    }
-    __syncthreads();
+    auto& w = S == 0 ? w0 : (S == 1 ? w1 : w2);
+    const uint16_t* k_s = S == 0 ? sK0 : (S == 1 ? sK1 : sK2);
+    const uint16_t* v_s = S == 0 ? sV0 : (S == 1 ? sV1 : sV2);
+    fwd_tile<D, QB, MASK>(k_s, v_s, sT, off, qf, w, t * kBC, a.Sk, sl2, inv_sl2, sm, acc);
+    if constexpr (FULL)
+      wait_vmcnt<2 * SPD_LOADS + Dma::NLOADS>();
+    else
+      wait_vmcnt<0>();     // the unaligned spd path issues a variable number of loads
+    __builtin_amdgcn_s_barrier();
   };
-  using B0 = std::integral_constant<int, 0>;
-  using B1 = std::integral_constant<int, 1>;
   using Full = std::false_type;     // every key of the tile exists
-  using Part = std::true_type;      // last tile, keys past Sk masked
-  // Full tiles in pairs (static buffers), then at most one full tile and the
-  // partial last tile.
+  using Part = std::true_type;      // keys past Sk masked
   const int64_t nfull = FULL ? ntiles : a.Sk / kBC;
   int64_t t = 0;
-  for (; t + 1 < nfull; t += 2) {
-    step(t, B0(), Full());
-    step(t + 1, B1(), Full());
+  for (; t + 3 <= nfull; t += 3) {
+    step(t, S0(), Full());
+    step(t + 1, S1(), Full());
+    step(t + 2, S2(), Full());
   }
-  if (t < nfull) {
-    step(t, B0(), Full());
-    if (!FULL && t + 1 < ntiles) step(t + 1, B1(), Part());
-  } else if (!FULL && t < ntiles) {
-    step(t, B0(), Part());
+  // At most two full tiles and the partial one remain, in stages 0, 1, 2.
+  if constexpr (FULL) {
+    if (t < ntiles) step(t, S0(), Full());
+    if (t + 1 < ntiles) step(t + 1, S1(), Full());
+  } else {
+    if (t < ntiles) step(t, S0(), Part());
+    if (t + 1 < ntiles) step(t + 1, S1(), Part());
+    if (t + 2 < ntiles) step(t + 2, S2(), Part());
   }
 
   // Epilogue: O = O_acc / l, LSE = (m + log2 l) ln 2.

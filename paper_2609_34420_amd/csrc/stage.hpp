@@ -92,6 +92,63 @@ struct RowStage {
   }
 };
 
+// Direct global -> LDS copy (buffer_load_dwordx4 ... lds): each lane's 16
+// bytes land at the wave-uniform LDS base + 16 lane, and lanes past the
+// descriptor's range write zeros. A pair of tiles (64 rows x D bf16 each,
+// one descriptor per tensor) is split into 1 KiB blocks handed to the NW
+// waves in order; within a block, lane l fills LDS chunk l % (D/8) of tile
+// row (block row 0) + l / (D/8), so it reads the logical chunk that the
+// swizzle stores there.
+template <int D, int NW>
+struct TileDma {
+  static constexpr int ROWB = D * 2;
+  static constexpr int RPB = 1024 / ROWB;              // rows per block
+  static constexpr int NBLK = kTileRows * ROWB / 1024; // blocks per tensor
+  static constexpr int BPW = 2 * NBLK / NW;            // blocks per wave
+  static_assert(2 * NBLK % NW == 0, "blocks must divide evenly over the waves");
+  static constexpr int NLOADS = BPW;                   // vector-memory ops per wave per tile pair
+  uint32_t voff[BPW];
+  int second[BPW], lds_byte[BPW];                      // wave-uniform
+
+  __device__ __forceinline__ explicit TileDma(int wave) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      const int gb = wave * BPW + i;
+      const int lb = gb % NBLK;
+      second[i] = gb / NBLK;
+      lds_byte[i] = lb * 1024;
+      const int row = lb * RPB + lane / (D / 8);
+      const int chunk = swz_tile<D>(row, lane % (D / 8));   // involution: logical chunk here
+      voff[i] = (uint32_t)(row * ROWB + chunk * 16);
+    }
+  }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs0, __amdgpu_buffer_rsrc_t rs1,
+                                       uint16_t* dst0, uint16_t* dst1) const {
+    typedef __attribute__((address_space(3))) void* lds_void;
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      uint8_t* base = reinterpret_cast<uint8_t*>(second[i] ? dst1 : dst0) + lds_byte[i];
+      // Device pass only: in the host pass of this source the builtin stops
+      // the host-side launch stubs of the kernels that use it from being emitted.
+#if __HIP_DEVICE_COMPILE__
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(second[i] ? rs1 : rs0, (lds_void)(void*)base, 16, voff[i], 0, 0, 0);
+#else
+      (void)base;
+      (void)rs0;
+      (void)rs1;
+#endif
+    }
+  }
+};
+
+// s_waitcnt vmcnt(N), other counters free.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // Per-lane element offset of the row-operand read of rows perm32(lane & 31)
 // (+ 32 sb as an immediate), feature chunk 2 kc + (lane >> 5).
 template <int D>
