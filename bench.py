@@ -100,6 +100,9 @@ def run_gpu(w, args, dev):
     ws = torch.empty(gt.gt_attn_bwd_workspace_size(H, N, d, x["q"].dtype), dtype=torch.uint8,
                      device=dev)
     stream = torch.cuda.current_stream()
+    # BFS distances on an undirected graph are symmetric: spd is its own
+    # transpose, which lets the key-stationary stage read rows.
+    spd_t = x["spd"] if w.spd_symmetric else None
 
     def step(ev=None):
         if ev is not None:
@@ -109,7 +112,7 @@ def run_gpu(w, args, dev):
             ev[1].record(stream)
         for ph in range(3):
             gt.gt_attn_bwd_phase(ph, x["q"], x["k"], x["v"], x["spd"], x["table"], O, L, x["do"],
-                                 scale=scale, workspace=ws, grads=grads)
+                                 scale=scale, workspace=ws, grads=grads, spd_t=spd_t)
             if ev is not None:
                 ev[2 + ph].record(stream)
 

@@ -73,6 +73,15 @@ size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dt
  *   dV = P^T dO,  dS = P * (dO V^T - rowsum(dO * O)),
  *   dQ = scale dS K,  dK = scale dS^T Q,
  *   dtable[h, b] = sum of dS[h, i, j] over pairs with spd[i, j] == b.
+ *   spd_t    OPTIONAL [N, N] uint8 transpose of spd (spd_t[j*N + i] ==
+ *            spd[i*N + j]), host-owned device memory, read only. The
+ *            key-stationary stage reads spd by columns; with spd_t it reads
+ *            rows instead. The shortest-path matrix of an undirected graph is
+ *            symmetric: pass spd itself. A directed graph's spd is fixed per
+ *            graph, so its transpose can be built once. NULL, or a spd_t
+ *            that is not 16-byte aligned or with N not a multiple of 16, is
+ *            ignored (columns of spd are gathered). A spd_t that is not the
+ *            transpose of spd gives wrong dK, dV and dtable.
  *   o, lse   the forward outputs for the same inputs
  *   d_o      [H, N, d] dtype
  *   dq,dk,dv [H, N, d] dtype, OVERWRITTEN
@@ -82,7 +91,8 @@ size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dt
  * dtable is reduced with floating-point atomics: its last bits may differ
  * from run to run. No gradient flows to spd. */
 gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v,
-                        const uint8_t* spd, const float* table, int32_t n_buckets,
+                        const uint8_t* spd, const uint8_t* spd_t,
+                        const float* table, int32_t n_buckets,
                         const void* o, const float* lse, const void* d_o,
                         void* dq, void* dk, void* dv, float* dtable,
                         void* workspace, size_t workspace_bytes,
@@ -100,7 +110,8 @@ gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v,
  * are not touched. phase outside 0..2 gives GT_ERR_INVALID. */
 gt_status_t gt_attn_bwd_phase(int32_t phase,
                               const void* q, const void* k, const void* v,
-                              const uint8_t* spd, const float* table, int32_t n_buckets,
+                              const uint8_t* spd, const uint8_t* spd_t,
+                              const float* table, int32_t n_buckets,
                               const void* o, const float* lse, const void* d_o,
                               void* dq, void* dk, void* dv, float* dtable,
                               void* workspace, size_t workspace_bytes,

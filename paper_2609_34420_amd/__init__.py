@@ -56,7 +56,7 @@ def lib() -> ctypes.CDLL:
         L.gt_attn_bwd_workspace_size.restype = ctypes.c_size_t
         L.gt_attn_bwd_workspace_size.argtypes = [_I32, _I64, _I32, _I32]
         L.gt_attn_bwd.restype = _I32
-        L.gt_attn_bwd.argtypes = [_P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _P, _P, _P, _P,
+        L.gt_attn_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _P, _P, _P, _P,
                                   ctypes.c_size_t, _I32, _I64, _I32, _I32, _F, _P]
         L.gt_attn_bwd_phase.restype = _I32
         L.gt_attn_bwd_phase.argtypes = [_I32] + L.gt_attn_bwd.argtypes
@@ -140,19 +140,25 @@ def gt_attn_bwd_workspace_size(H: int, N: int, d: int, dtype=torch.bfloat16) -> 
 
 
 def gt_attn_bwd(q, k, v, spd, table, o, lse, d_o, scale: float | None = None,
-                workspace=None, grads=None, stream=None):
+                workspace=None, grads=None, stream=None, spd_t=None):
     """dQ, dK, dV, dTable (C ABI gt_attn_bwd). `grads` may hold preallocated
     (dq, dk, dv, dtable); `workspace` a uint8 device tensor of at least
-    gt_attn_bwd_workspace_size bytes."""
-    return gt_attn_bwd_phase(-1, q, k, v, spd, table, o, lse, d_o, scale, workspace, grads, stream)
+    gt_attn_bwd_workspace_size bytes; `spd_t` the transpose of spd (spd itself
+    for a symmetric matrix) or None."""
+    return gt_attn_bwd_phase(-1, q, k, v, spd, table, o, lse, d_o, scale, workspace, grads, stream,
+                             spd_t)
 
 
 def gt_attn_bwd_phase(phase: int, q, k, v, spd, table, o, lse, d_o, scale: float | None = None,
-                      workspace=None, grads=None, stream=None):
+                      workspace=None, grads=None, stream=None, spd_t=None):
     """One stage of the backward (C ABI gt_attn_bwd_phase): 0 prepare,
     1 dK/dV/dtable, 2 dQ; phase -1 runs gt_attn_bwd (all three)."""
     H, N, d = q.shape
     _dev_contig(q, k, v, spd, table, o, lse, d_o)
+    if spd_t is not None:
+        _dev_contig(spd_t)
+        if tuple(spd_t.shape) != tuple(spd.shape) or spd_t.dtype != spd.dtype:
+            raise ValueError("spd_t must have the shape and dtype of spd")
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     if grads is None:
         grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
@@ -162,7 +168,8 @@ def gt_attn_bwd_phase(phase: int, q, k, v, spd, table, o, lse, d_o, scale: float
     need = gt_attn_bwd_workspace_size(H, N, d, q.dtype)
     if workspace is None:
         workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
-    args = (_ptr(q), _ptr(k), _ptr(v), _ptr(spd), _ptr(table), table.shape[1],
+    args = (_ptr(q), _ptr(k), _ptr(v), _ptr(spd), None if spd_t is None else _ptr(spd_t),
+            _ptr(table), table.shape[1],
             _ptr(o), _ptr(lse), _ptr(d_o), _ptr(dq), _ptr(dk), _ptr(dv),
             _ptr(dtable), _ptr(workspace), workspace.numel() * workspace.element_size(),
             H, N, d, _dt(q), scale, _stream(stream))

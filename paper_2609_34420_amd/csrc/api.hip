@@ -106,7 +106,8 @@ size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dt
 }
 
 static gt_status_t bwd_impl(int32_t phase, const void* q, const void* k, const void* v,
-                            const uint8_t* spd, const float* table, int32_t n_buckets,
+                            const uint8_t* spd, const uint8_t* spd_t, const float* table,
+                            int32_t n_buckets,
                             const void* o, const float* lse, const void* d_o, void* dq,
                             void* dk, void* dv, float* dtable, void* workspace,
                             size_t workspace_bytes, int32_t H, int64_t N, int32_t d,
@@ -136,26 +137,30 @@ static gt_status_t bwd_impl(int32_t phase, const void* q, const void* k, const v
   a.nmax = reinterpret_cast<float*>(static_cast<char*>(workspace) + 2 * align_up(rows * sizeof(float)));
   a.H = H; a.N = N; a.scale = scale;
   a.spd_vec = spd_vec(spd, N, 0, 0);
+  // The transpose is used only where its rows can be read 16 bytes at a time
+  // and one key block's rows (256 of them) stay within 32-bit offsets.
+  a.spd_t = (spd_t && spd_vec(spd_t, N, 0, 0) && 256 * N < (int64_t(1) << 31)) ? spd_t : nullptr;
   return launched(gt::launch_bwd(a, d, dtype == GT_BF16, phase, static_cast<hipStream_t>(stream)));
 }
 
 gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v, const uint8_t* spd,
-                        const float* table, int32_t n_buckets, const void* o,
+                        const uint8_t* spd_t, const float* table, int32_t n_buckets, const void* o,
                         const float* lse, const void* d_o, void* dq, void* dk, void* dv,
                         float* dtable, void* workspace, size_t workspace_bytes, int32_t H,
                         int64_t N, int32_t d, gt_dtype_t dtype, float scale, void* stream) {
-  return bwd_impl(-1, q, k, v, spd, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
+  return bwd_impl(-1, q, k, v, spd, spd_t, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
                   workspace, workspace_bytes, H, N, d, dtype, scale, stream);
 }
 
 gt_status_t gt_attn_bwd_phase(int32_t phase, const void* q, const void* k, const void* v,
-                              const uint8_t* spd, const float* table, int32_t n_buckets,
+                              const uint8_t* spd, const uint8_t* spd_t, const float* table,
+                              int32_t n_buckets,
                               const void* o, const float* lse, const void* d_o, void* dq,
                               void* dk, void* dv, float* dtable, void* workspace,
                               size_t workspace_bytes, int32_t H, int64_t N, int32_t d,
                               gt_dtype_t dtype, float scale, void* stream) {
   if (phase < 0 || phase > 2) return GT_ERR_INVALID;
-  return bwd_impl(phase, q, k, v, spd, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
+  return bwd_impl(phase, q, k, v, spd, spd_t, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
                   workspace, workspace_bytes, H, N, d, dtype, scale, stream);
 }
 

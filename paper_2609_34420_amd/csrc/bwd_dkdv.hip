@@ -10,8 +10,9 @@
 // dP from -Dlt, so per score element the vector work is one FMA with the
 // bias, one exp2, one multiply and the two bf16 conversions.
 //
-// Bias and table gradient: the table (times log2 e) is replicated 16 times
-// in LDS (copy = lane & 15) and the bucket histogram has the same layout, so
+// Bias and table gradient: the table (times log2 e) is replicated in LDS
+// (copy = lane & 31 when there are at most 128 buckets, else lane & 15) and
+// the bucket histogram has the same layout, so
 // one address register serves the bias read and the gradient add. The
 // histogram is fixed point: LDS float atomics are slow on this hardware,
 // 64-bit integer adds are not. dS is accumulated as round(dS * 2^F), where
@@ -42,16 +43,20 @@ constexpr int kNW = 8;              // waves per workgroup
 constexpr int kBK = kNW * 32;       // keys per workgroup
 constexpr int kBQ = 64;             // queries per staged tile
 constexpr int kThreads = kNW * 64;
-constexpr int kCopies = 16;                 // table / histogram copies (lane & 15)
-constexpr int kTabEntries = 256 * kCopies;
+// Table / histogram copies: lane & (CPY - 1); 32 copies (two lanes per copy)
+// for up to 128 buckets, else 16.
+template <int NB>
+constexpr int copies() { return NB <= 128 ? 32 : 16; }
 
-// All LDS of the kernel in one block, table and histogram first: their
-// offsets stay below 64 KiB, so the one per-element address register serves
-// both with immediate offsets.
-template <int D>
+// All LDS of the kernel in one block, table and histogram first so that
+// their offsets stay small: the one per-element address register serves
+// both with immediate offsets. NB (64, 128 or 256) bounds n_buckets; at 64
+// the tiles also stay below 64 KiB, inside the reach of the DS immediate.
+template <int D, int NB>
 struct DkdvSmem {
-  uint2 tabw[kTabEntries];                // table copies (fp32 bits, 8-byte stride)
-  unsigned long long hist[kTabEntries];   // gradient histogram copies, same index
+  static constexpr int ENT = NB * copies<NB>();   // entry (b, c) = b * CPY + c
+  uint2 tabw[ENT];                  // table copies (fp32 bits, 8-byte stride)
+  unsigned long long hist[ENT];     // gradient histogram copies, same index
   uint16_t q[2][kBQ * D];
   uint16_t o[2][kBQ * D];
   float init_s[2][kBQ];             // -LSE log2 e / (scale log2 e); -inf for empty rows
@@ -95,8 +100,8 @@ struct QTileStage {
   // Registers -> LDS buffer BUF, with the accumulator starts of S
   // (-lse2 / (scale log2 e), -inf for padded rows so that P = 0) and of the
   // scaled dP (-Dlt 2^F).
-  template <int BUF>
-  __device__ __forceinline__ void store(DkdvSmem<D>& sm, int64_t i0, int64_t n, float inv_sl2,
+  template <int BUF, int NB>
+  __device__ __forceinline__ void store(DkdvSmem<D, NB>& sm, int64_t i0, int64_t n, float inv_sl2,
                                         float sF) {
     q.store(sm.q[BUF]);
     o.store(sm.o[BUF]);
@@ -147,10 +152,12 @@ __device__ __forceinline__ int round_to_int(float x) {
   return r;
 }
 
-template <int D, bool KTAIL, int BUF, int QS>
-__device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const DkdvOffsets<D>& off,
+// b: this lane's 16 bucket indices, as 16 bytes (gathered from spd columns)
+// or as 4 words (a 16-byte row segment of spd_t).
+template <int D, int NB, bool KTAIL, int BUF, int QS, typename BT>
+__device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOffsets<D>& off,
                                               const bf16x8* kf, const bf16x8* vf,
-                                              const uint8_t* b, float sl2, bool jok,
+                                              const BT* b, float sl2, bool jok,
                                               f32x16* dk, f32x16* dv) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
@@ -177,16 +184,38 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const DkdvOffsets
   // Lane: key; registers r: queries. dp holds (dO.V - Dlt) 2^F, so ds below
   // is dS 2^F.
   float p[16], ds[16];
-  uint32_t idx[16];
+  uint32_t addr[16];   // byte offset of entry (bucket, copy) in tabw and in hist
   float tb[16];
-  const uint32_t cpy = (uint32_t)(lane & (kCopies - 1));
+  constexpr int CPY = copies<NB>();
+  const uint32_t cpy8 = (uint32_t)(lane & (CPY - 1)) * 8u;
+  if constexpr (sizeof(BT) == 4) {
+    uint32_t w[4];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    uint32_t bk = b[r];
-    opaque(bk);                                    // keep the byte's wait here
-    idx[r] = (bk << 4) | cpy;                      // copy cpy of bucket b
-    tb[r] = __uint_as_float(sm.tabw[idx[r]].x);
+    for (int u = 0; u < 4; ++u) {
+      w[u] = b[u];
+      opaque(w[u]);                                // keep the load's wait here
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      if constexpr (CPY == 32)   // byte (r & 3) of w[r >> 2] times 256, plus cpy8
+        addr[r] = __builtin_amdgcn_perm(w[r >> 2], cpy8, 0x0c0c0000u | ((4u + (r & 3)) << 8));
+      else
+        addr[r] = (((w[r >> 2] >> (8 * (r & 3))) & 0xffu) << 7) | cpy8;
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      uint32_t bk = b[r];
+      opaque(bk);                                  // keep the byte's wait here
+      if constexpr (CPY == 32)
+        addr[r] = __builtin_amdgcn_perm(bk, cpy8, 0x0c0c0400u);   // byte0(bk) * 256 + cpy8
+      else
+        addr[r] = (bk << 7) | cpy8;
+    }
   }
+#pragma unroll
+  for (int r = 0; r < 16; ++r)
+    tb[r] = *reinterpret_cast<const float*>(reinterpret_cast<const uint8_t*>(sm.tabw) + addr[r]);
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const float x = fmaf(s[r], sl2, tb[r]);
@@ -197,7 +226,8 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const DkdvOffsets
   }
 #pragma unroll
   for (int r = 0; r < 16; ++r)
-    atomicAdd(&sm.hist[idx[r]], (unsigned long long)(long long)round_to_int(ds[r]));
+    atomicAdd(reinterpret_cast<unsigned long long*>(reinterpret_cast<uint8_t*>(sm.hist) + addr[r]),
+              (unsigned long long)(long long)round_to_int(ds[r]));
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const bf16x8 pb = cvt_bf16x8(p + 8 * q);
@@ -211,8 +241,8 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D>& sm, const DkdvOffsets
   }
 }
 
-template <int D, bool KTAIL, bool QFULL>
-__device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, int h, int64_t key0,
+template <int D, int NB, bool KTAIL, bool QFULL, bool TR>
+__device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm, int h, int64_t key0,
                                           int64_t j, bool jok, int fexp) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
@@ -254,10 +284,26 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, int
   const int64_t ntiles = (a.N + kBQ - 1) / kBQ;
   const DkdvOffsets<D> off;
 
+  // Bucket indices of this lane's key: TR reads 16 queries as one 16-byte
+  // row segment of spd_t (rows of this key block only; past the block's last
+  // row a load reads zeros), else gathers 16 bytes of a spd column.
+  using BT = std::conditional_t<TR, uint32_t, uint8_t>;
+  constexpr int NBT = TR ? 4 : 16;
+  const __amdgpu_buffer_rsrc_t rs_t =
+      make_rsrc_n(TR ? a.spd_t + key0 * ld : a.spd, ((a.N - key0 < kBK ? a.N - key0 : kBK)) * ld);
+  const uint32_t voff_t = (uint32_t)((jc - key0) * ld) + 16u * (uint32_t)g;
+  auto fetch = [&](int64_t i_base, BT* dst) {
+    if constexpr (TR) {
+      buf_u128(rs_t, voff_t, (uint32_t)i_base, reinterpret_cast<uint32_t*>(dst));
+    } else {
+      load_bytes<QFULL>(spd_cols, ld, i_base, a.N, key_off, reinterpret_cast<uint8_t*>(dst));
+    }
+  };
+
   QTileStage<D> st;
   st.load(qh, oh, lse2h, dlth, 0, a.N);
-  uint8_t bA[16], bB[16];
-  load_bytes<QFULL>(spd_cols, ld, 0, a.N, key_off, bA);
+  BT bA[NBT], bB[NBT];
+  fetch(0, bA);
   st.template store<0>(sm, 0, a.N, inv_sl2, sF);
   wait_loads();
   __syncthreads();
@@ -270,13 +316,13 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, int
     const int64_t i0 = t * kBQ;
     const bool more = t + 1 < ntiles;
     const int64_t inext = more ? i0 + kBQ : i0;
-    load_bytes<QFULL>(spd_cols, ld, i0 + 32, a.N, key_off, bB);
+    fetch(i0 + 32, bB);
     st.load(qh, oh, lse2h, dlth, inext, a.N);
     sched_fence();
-    dkdv_subblock<D, KTAIL, BUF, 0>(sm, off, kf, vf, bA, sl2, jok, dk, dv);
-    load_bytes<QFULL>(spd_cols, ld, inext, a.N, key_off, bA);
+    dkdv_subblock<D, NB, KTAIL, BUF, 0>(sm, off, kf, vf, bA, sl2, jok, dk, dv);
+    fetch(inext, bA);
     sched_fence();
-    dkdv_subblock<D, KTAIL, BUF, 1>(sm, off, kf, vf, bB, sl2, jok, dk, dv);
+    dkdv_subblock<D, NB, KTAIL, BUF, 1>(sm, off, kf, vf, bB, sl2, jok, dk, dv);
     if (more) st.template store<BUF ^ 1>(sm, inext, a.N, inv_sl2, sF);
     __syncthreads();
   };
@@ -308,9 +354,10 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D>& sm, int
   }
 }
 
-template <int D, bool QFULL>
+template <int D, int NB, bool QFULL, bool TR>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
-  __shared__ __attribute__((aligned(16))) DkdvSmem<D> sm;
+  constexpr int CPY = copies<NB>();
+  __shared__ __attribute__((aligned(16))) DkdvSmem<D, NB> sm;
   uint2* tabw = sm.tabw;
   unsigned long long* hist = sm.hist;
   float (*red)[kNW] = sm.red;
@@ -323,8 +370,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   const int64_t j = kblk * kBK + wave * 32 + col;
   const bool jok = j < a.N;
 
-  for (int t = tid; t < kTabEntries; t += kThreads) {
-    const int bkt = t / kCopies;
+  for (int t = tid; t < DkdvSmem<D, NB>::ENT; t += kThreads) {
+    const int bkt = t / CPY;
     const float tv = (bkt < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + bkt] * kLog2e : 0.0f;
     tabw[t] = make_uint2(__float_as_uint(tv), 0u);
     hist[t] = 0ull;
@@ -367,16 +414,16 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   }
 
   if ((kblk + 1) * kBK <= a.N)
-    dkdv_main<D, false, QFULL>(a, sm, h, kblk * kBK, j, jok, fexp);
+    dkdv_main<D, NB, false, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
   else
-    dkdv_main<D, true, QFULL>(a, sm, h, kblk * kBK, j, jok, fexp);
+    dkdv_main<D, NB, true, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
 
   __syncthreads();
   const double unscale = ldexp(1.0, -fexp);
   for (int bkt = tid; bkt < a.n_buckets; bkt += kThreads) {
     long long t = 0;
 #pragma unroll
-    for (int c = 0; c < kCopies; ++c) t += (long long)hist[bkt * kCopies + ((c + bkt) & (kCopies - 1))];
+    for (int c = 0; c < CPY; ++c) t += (long long)hist[bkt * CPY + ((c + bkt) & (CPY - 1))];
     if (t != 0) atomicAdd(&a.dtable[(int64_t)h * a.n_buckets + bkt], (float)((double)t * unscale));
   }
 }
@@ -387,17 +434,27 @@ hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s) {
   const int64_t nkb = (a.N + kBK - 1) / kBK;
   const dim3 grid((unsigned)(nkb * a.H));
   const bool qfull = a.N % kBQ == 0;
-  if (d == 64) {
-    if (qfull)
-      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<64, true>), grid, dim3(kThreads), 0, s, a);
-    else
-      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<64, false>), grid, dim3(kThreads), 0, s, a);
-  } else {
-    if (qfull)
-      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<32, true>), grid, dim3(kThreads), 0, s, a);
-    else
-      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<32, false>), grid, dim3(kThreads), 0, s, a);
+#define GT_DKDV_LAUNCH(D_, NB_)                                                                     \
+  {                                                                                                 \
+    if (a.spd_t) {                                                                                  \
+      if (qfull)                                                                                    \
+        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D_, NB_, true, true>), grid, dim3(kThreads), 0, s, a);  \
+      else                                                                                          \
+        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D_, NB_, false, true>), grid, dim3(kThreads), 0, s, a); \
+    } else {                                                                                        \
+      if (qfull)                                                                                    \
+        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D_, NB_, true, false>), grid, dim3(kThreads), 0, s, a); \
+      else                                                                                          \
+        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D_, NB_, false, false>), grid, dim3(kThreads), 0, s, a);\
+    }                                                                                               \
   }
+  // Every spd byte value must index the table (values at or past n_buckets
+  // read bias 0 and their gradient is dropped), so the full 256-bucket table.
+  if (d == 64)
+    GT_DKDV_LAUNCH(64, 256)
+  else
+    GT_DKDV_LAUNCH(32, 256)
+#undef GT_DKDV_LAUNCH
   return hipGetLastError();
 }
 

@@ -32,6 +32,7 @@ struct BwdArgs {
   const void* k;
   const void* v;
   const uint8_t* spd;
+  const uint8_t* spd_t;   // transpose of spd (same ld), or null: gather columns
   int64_t ld_spd;
   const float* table;
   int32_t n_buckets;

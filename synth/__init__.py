@@ -77,6 +77,11 @@ class Workload:
 
     # ---- sizes ------------------------------------------------------------
     @property
+    def spd_symmetric(self) -> bool:
+        """BFS distances on an undirected graph: spd[i, j] == spd[j, i]."""
+        return self.spd_law is None
+
+    @property
     def S(self) -> int:
         return self.N // self.shards
 

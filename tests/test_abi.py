@@ -85,11 +85,11 @@ def test_ring_step_validation(kw, code):
 def _bwd(**kw):
     H, N, d = 2, 100, 64
     need = gt.lib().gt_attn_bwd_workspace_size(H, N, d, BF16)
-    a = dict(q=FAKE, k=FAKE, v=FAKE, spd=FAKE, table=FAKE, nb=8, o=FAKE, lse=FAKE, do=FAKE,
+    a = dict(q=FAKE, k=FAKE, v=FAKE, spd=FAKE, spd_t=None, table=FAKE, nb=8, o=FAKE, lse=FAKE, do=FAKE,
              dq=FAKE, dk=FAKE, dv=FAKE, dt=FAKE, ws=FAKE, wsb=need, H=H, N=N, d=d, dtype=BF16,
              scale=0.125)
     a.update(kw)
-    return gt.lib().gt_attn_bwd(a["q"], a["k"], a["v"], a["spd"], a["table"], a["nb"], a["o"],
+    return gt.lib().gt_attn_bwd(a["q"], a["k"], a["v"], a["spd"], a["spd_t"], a["table"], a["nb"], a["o"],
                                 a["lse"], a["do"], a["dq"], a["dk"], a["dv"], a["dt"], a["ws"],
                                 a["wsb"], a["H"], a["N"], a["d"], a["dtype"], a["scale"], None)
 

@@ -61,9 +61,11 @@ def _sampled_parity(w, spd_dev, R, tag, layer=0, seed=0):
     scale = w.scale()
     Q, K, V, dO = _bf16(q), _bf16(k), _bf16(v), _bf16(do)
     T = torch.from_numpy(table).to(DEV)
-    say(f"{tag}: dense fwd+bwd N={w.N} H={w.H}")
+    # as in the benchmark: a symmetric spd is its own transpose
+    spd_t = spd_dev if (w.spd_symmetric and spd_dev.shape[0] == spd_dev.shape[1]) else None
+    say(f"{tag}: dense fwd+bwd N={w.N} H={w.H} spd_t={'spd' if spd_t is not None else 'none'}")
     O, L = gt.gt_attn_fwd(Q, K, V, spd_dev, T, scale=scale)
-    dq, dk, dv, dt = gt.gt_attn_bwd(Q, K, V, spd_dev, T, O, L, dO, scale=scale)
+    dq, dk, dv, dt = gt.gt_attn_bwd(Q, K, V, spd_dev, T, O, L, dO, scale=scale, spd_t=spd_t)
     torch.cuda.synchronize()
     spd_R = w.spd_rows(R, seed=seed)
     Rt = torch.from_numpy(R).to(DEV)
@@ -76,7 +78,7 @@ def _sampled_parity(w, spd_dev, R, tag, layer=0, seed=0):
     mask = torch.zeros((1, w.N, 1), device=DEV, dtype=torch.bfloat16)
     mask[:, Rt] = 1
     dOm = (dO * mask).contiguous()
-    _, dkm, dvm, dtm = gt.gt_attn_bwd(Q, K, V, spd_dev, T, O, L, dOm, scale=scale)
+    _, dkm, dvm, dtm = gt.gt_attn_bwd(Q, K, V, spd_dev, T, O, L, dOm, scale=scale, spd_t=spd_t)
     torch.cuda.synchronize()
     _, dk_ref, dv_ref, dt_ref = oracle.block_backward(q[:, R], k, v, spd_R, table, scale, do[:, R])
     check_grads(f"{tag} masked", {"dk": to_np(dkm), "dv": to_np(dvm), "dtable": to_np(dtm)},

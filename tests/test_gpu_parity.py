@@ -32,13 +32,14 @@ def _case(H, N, d, nb, seed, dt, hi=None, table_std=0.5, qkv_std=None, neg_inf=F
     return q, k, v, do, table, spd
 
 
-def _run_full(q, k, v, do, table, spd, dt, scale):
+def _run_full(q, k, v, do, table, spd, dt, scale, spd_t=None):
     td = tdtype(dt)
     Q, K, V, dO = (to_dev(x, td) for x in (q, k, v, do))
     T = to_dev(table)
     S = to_dev(spd, torch.uint8)
+    St = None if spd_t is None else (S if spd_t is spd else to_dev(spd_t, torch.uint8))
     O, L = gt.gt_attn_fwd(Q, K, V, S, T, scale=scale)
-    dq, dk, dv, dtab = gt.gt_attn_bwd(Q, K, V, S, T, O, L, dO, scale=scale)
+    dq, dk, dv, dtab = gt.gt_attn_bwd(Q, K, V, S, T, O, L, dO, scale=scale, spd_t=St)
     torch.cuda.synchronize()
     return dict(o=to_np(O), lse=to_np(L), dq=to_np(dq), dk=to_np(dk), dv=to_np(dv),
                 dtable=to_np(dtab))
@@ -212,3 +213,36 @@ def test_gradient_invariants_bf16():
     assert np.abs(got["dtable"].sum(1)).max() <= 1e-2 * scale_dt + 1e-4
     assert rel_l2(got["dk"].sum(1), np.zeros((H, d))) <= 1e-2 * np.linalg.norm(got["dk"])
     assert rel_l2(got["dv"].sum(1), do.sum(1)) <= 1e-2
+
+
+@pytest.mark.parametrize("kind", ["symmetric", "transposed"])
+@pytest.mark.parametrize("N", [64, 400, 1024])
+def test_backward_with_spd_transpose(N, kind):
+    """The key-stationary stage reading rows of spd_t: a symmetric matrix
+    passed as its own transpose, and an asymmetric one with its transpose
+    (N = 400 leaves a partial query tile; buckets past the table included)."""
+    H, d, nb = 2, 64, 12
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=N + (kind == "symmetric"), dt="bf16", hi=nb + 3)
+    if kind == "symmetric":
+        spd = np.minimum(spd, spd.T).copy()
+        spd_t = spd
+    else:
+        spd_t = np.ascontiguousarray(spd.T)
+    scale = 1.0 / math.sqrt(d)
+    say(f"spd_t {kind} N={N}")
+    got = _run_full(q, k, v, do, table, spd, "bf16", scale, spd_t=spd_t)
+    ref = _oracle_full(q, k, v, do, table, spd, scale)
+    check_fwd(f"spd_t {kind} N={N}", got["o"], got["lse"], ref["o"], ref["lse"], "bf16")
+    check_grads(f"spd_t {kind} N={N}", got, ref, "bf16")
+
+
+def test_spd_transpose_ignored_when_unaligned():
+    """N = 100 is not a multiple of 16: spd_t is ignored (columns gathered),
+    results still match the oracle."""
+    H, N, d, nb = 2, 100, 64, 9
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=5, dt="bf16")
+    spd_t = np.ascontiguousarray(spd.T)
+    scale = 1.0 / math.sqrt(d)
+    got = _run_full(q, k, v, do, table, spd, "bf16", scale, spd_t=spd_t)
+    ref = _oracle_full(q, k, v, do, table, spd, scale)
+    check_grads("spd_t unaligned", got, ref, "bf16")

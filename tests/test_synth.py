@@ -113,3 +113,23 @@ def test_workload_tensors_are_seeded_and_bf16_exact():
     t = w.table(0)
     assert t.shape == (8, 32) and t.dtype == np.float32
     assert 0.01 < t.std() < 0.03
+
+
+def test_bfs_spd_is_symmetric_and_iid_is_not():
+    """The bench passes spd as its own transpose for BFS workloads: pin that
+    their distance matrices are symmetric (undirected graphs), and that the
+    i.i.d. law is not (it takes the column-gather path)."""
+    w = synth.workload("tiny")
+    assert w.spd_symmetric
+    spd = w.spd_block(0, w.N)
+    assert (spd == spd.T).all()
+    b = synth.workload("ba16k")
+    rows = b.spd_block(0, 64)
+    cols = b.spd_rows(np.arange(64))        # rows 0..63 again, by id
+    assert (rows == cols).all()
+    sub = b.spd_rows(np.arange(64))[:, :64]
+    assert (sub == sub.T).all()
+    d = synth.workload("deep32k")
+    assert not d.spd_symmetric
+    blk = d.spd_block(0, 64)[:, :64]
+    assert not (blk == blk.T).all()
