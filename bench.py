@@ -46,7 +46,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--workload", default="sbm128k")
     p.add_argument("--seed", type=int, default=0)
-    p.add_argument("--cpu-rows", type=int, default=384,
+    p.add_argument("--cpu-rows", type=int, default=512,
                    help="query rows of the oracle CPU baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",

@@ -61,26 +61,6 @@ __device__ __forceinline__ int perm32(int m) {
   return (((m >> 2) & 1) << 4) | ((m >> 3) << 2) | (m & 3);
 }
 
-// XOR swizzle of 16-byte chunks in a row-major LDS tile whose rows hold D
-// bf16 (D / 8 chunks). For the rows an MFMA operand read touches (block rows
-// perm32(lane)), every 8-lane group hits 8 distinct 16-byte bank groups of a
-// 32-bank LDS and every 16-lane group 16 distinct ones of a 64-bank LDS.
-template <int D>
-__device__ __forceinline__ int swz_rows(int row, int chunk) {
-  if constexpr (D == 64) {
-    return chunk ^ (((row >> 1) & 1) | ((row >> 3) & 2) | (((row ^ (row >> 2)) & 1) << 2));
-  } else {
-    return chunk ^ (((row >> 1) & 1) | ((row >> 3) & 2));
-  }
-}
-
-// Swizzle for a transposed tile: row = feature c, 64 keys per row (8
-// chunks); consecutive rows read together get distinct bank groups under the
-// same two models.
-__device__ __forceinline__ int swz_t64(int row, int chunk) {
-  return chunk ^ ((((row >> 1) & 3) | ((row & 1) << 2)) ^ (((row >> 3) & 1) << 2));
-}
-
 __device__ __forceinline__ bf16x8 lds_b128(const uint16_t* p) {
   return *reinterpret_cast<const bf16x8*>(p);
 }
