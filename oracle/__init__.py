@@ -16,5 +16,7 @@ from .attention import (  # noqa: F401
     ring_step,
     merge,
     ring_forward,
+    ring_backward_step,
+    ring_backward,
     lse_bias_only,
 )

@@ -29,7 +29,8 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = ["bias_block", "block_attention", "block_backward", "forward", "backward",
-           "ring_step", "merge", "ring_forward", "lse_bias_only"]
+           "ring_step", "merge", "ring_forward", "ring_backward_step", "ring_backward",
+           "lse_bias_only"]
 
 
 def _f64(x):
@@ -233,3 +234,72 @@ def lse_bias_only(spd_rows, table):
             mx = terms.max()
             out[h, r] = mx + np.log(np.exp(terms - mx).sum())
     return out
+
+
+def ring_backward_step(q_shard, o_shard, lse_shard, d_out_shard, k_blk, v_blk, spd, row_off,
+                       col_off, table, scale):
+    """Backward of one graph-aware context-parallel step: the rank's query
+    shard against the KV block it holds (Section III-A-1 parts 1-3 run in
+    reverse). The softmax of a query row spans every KV block, so P comes
+    from the merged forward's LSE and Dlt from its merged O (never from the
+    block's own partial):
+      P = exp(S - LSE), S = scale Q K_blk^T + table[spd slice] (Eq. (2)),
+      Dlt_i = sum_c dO_ic O_ic, dS = P * (dO V_blk^T - Dlt),
+      dQ_part = scale dS K_blk, dK_part = scale dS^T Q, dV_part = P^T dO,
+      dTable_part[h, b] = sum of dS_ij over the block's pairs with spd = b.
+    The parts of all KV blocks add up to the full gradients; dK_part and
+    dV_part belong to the KV block and travel with it around the ring.
+    spd: any 2-D array whose element (r, c) is the bucket of global query
+    row r and global key column c."""
+    q, o, do = _f64(q_shard), _f64(o_shard), _f64(d_out_shard)
+    k, v = _f64(k_blk), _f64(v_blk)
+    lse = _f64(lse_shard)
+    H, Sq, d = q.shape
+    Sk = k.shape[1]
+    nb = table.shape[1]
+    blk = np.asarray(spd)[row_off:row_off + Sq, col_off:col_off + Sk]
+    idx = blk.astype(np.int64)
+    inside = idx < nb
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    dt = np.zeros((H, nb), dtype=np.float64)
+    for h in range(H):
+        S = _scores(q[h], k[h], blk, table[h], scale)
+        P = _probs(S, lse[h])
+        dP = do[h] @ v[h].T
+        dlt = (do[h] * o[h]).sum(axis=1)
+        dS = P * (dP - dlt[:, None])
+        dq[h] = scale * (dS @ k[h])
+        dk[h] = scale * (dS.T @ q[h])
+        dv[h] = P.T @ do[h]
+        dt[h] = np.bincount(idx[inside], weights=dS[inside], minlength=nb)[:nb]
+    return dq, dk, dv, dt
+
+
+def ring_backward(q, k, v, spd, table, scale, d_out, bounds):
+    """Simulate the backward of every rank of the ring on the CPU: each rank
+    keeps its query rows and spd rows, runs ring_forward's merged (O, LSE)
+    for them, and visits the KV blocks in ring order, accumulating dQ
+    locally and each block's dK/dV parts and dTable across ranks.
+    Returns dQ, dK, dV [H, N, d] and dTable [H, nb]."""
+    P = len(bounds) - 1
+    q, k, v, d_out = np.asarray(q), np.asarray(k), np.asarray(v), np.asarray(d_out)
+    O, L = ring_forward(q, k, v, spd, table, scale, bounds)
+    dq = np.zeros(q.shape)
+    dk = np.zeros(k.shape)
+    dv = np.zeros(v.shape)
+    dt = np.zeros(table.shape)
+    for r in range(P):
+        r0, r1 = bounds[r], bounds[r + 1]
+        spd_rows = np.asarray(spd)[r0:r1]
+        for t in range(P):
+            blk = (r - t) % P
+            c0, c1 = bounds[blk], bounds[blk + 1]
+            a, b, c, e = ring_backward_step(q[:, r0:r1], O[:, r0:r1], L[:, r0:r1], d_out[:, r0:r1],
+                                            k[:, c0:c1], v[:, c0:c1], spd_rows, 0, c0, table, scale)
+            dq[:, r0:r1] += a
+            dk[:, c0:c1] += b
+            dv[:, c0:c1] += c
+            dt += e
+    return dq, dk, dv, dt

@@ -384,3 +384,61 @@ def test_row_sampled_backward_equals_masked_full_backward():
     O_r, L_r = oracle.block_attention(q[:, R], k, v, spd[R], table, s)
     np.testing.assert_allclose(O_r, O[:, R], atol=1e-12)
     np.testing.assert_allclose(L_r, L[:, R], atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Backward ring step pins
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("bounds", [[0, 50], [0, 13, 50], [0, 7, 31, 50],
+                                    [0, 3, 9, 10, 22, 30, 33, 41, 50]])
+def test_ring_backward_equals_unsharded(bounds):
+    """Every rank visiting every KV block with the merged LSE and Dlt, dQ
+    accumulated locally and dK/dV/dTable accumulated per block, reproduces
+    the unsharded backward (itself pinned by autograd and finite
+    differences), for P = 1, 2, 3, 8 with uneven shards and out-of-range
+    buckets."""
+    q, k, v, do, table, spd = _rand_case(H=2, N=50, d=8, nb=6, seed=21, out_of_range=True)
+    s = 0.35
+    ref = oracle.backward(q, k, v, spd, table, s, do)
+    got = oracle.ring_backward(q, k, v, spd, table, s, do, bounds)
+    for a, b in zip(got, ref):
+        np.testing.assert_allclose(a, b, atol=1e-11)
+
+
+def test_ring_backward_step_single_block_is_block_backward():
+    """One step covering every key (row_off = col_off = 0) with the block's
+    own LSE is exactly block_backward for those query rows."""
+    q, k, v, do, table, spd = _rand_case(H=2, N=30, d=6, nb=5, seed=22)
+    s = 0.5
+    R = np.arange(4, 19)
+    O, L = oracle.forward(q, k, v, spd, table, s)
+    got = oracle.ring_backward_step(q[:, R], O[:, R], L[:, R], do[:, R], k, v, spd[R], 0, 0,
+                                    table, s)
+    ref = oracle.block_backward(q[:, R], k, v, spd[R], table, s, do[:, R])
+    for a, b in zip(got, ref):
+        np.testing.assert_allclose(a, b, atol=1e-12)
+
+
+def test_ring_backward_step_masked_rows_and_offsets():
+    """A query row whose merged LSE is -inf gets no gradient; the spd slice
+    is taken at (row_off, col_off) of a larger matrix (an i/j or offset
+    mistake changes the bucket sums)."""
+    q, k, v, do, table, spd = _rand_case(H=1, N=24, d=4, nb=7, seed=23)
+    s = 0.7
+    O, L = oracle.forward(q, k, v, spd, table, s)
+    rows, cols = np.arange(5, 14), np.arange(10, 22)
+    Lm = L[:, rows].copy()
+    Lm[0, 2] = -np.inf
+    dq, dk, dv, dt = oracle.ring_backward_step(q[:, rows], O[:, rows], Lm, do[:, rows], k[:, cols],
+                                               v[:, cols], spd, 5, 10, table, s)
+    assert np.all(dq[0, 2] == 0)
+    # direct evaluation of the bucket sums of dS on the selected slice
+    Sg = s * q[0, rows] @ k[0, cols].T + np.where(spd[np.ix_(rows, cols)] < 7,
+                                                  table[0][np.minimum(spd[np.ix_(rows, cols)], 6)], 0.0)
+    P = np.exp(Sg - np.where(np.isfinite(Lm[0]), Lm[0], 0.0)[:, None])
+    P[2] = 0.0
+    dS = P * (do[0, rows] @ v[0, cols].T - (do[0, rows] * O[0, rows]).sum(1)[:, None])
+    b = spd[np.ix_(rows, cols)]
+    ref = np.array([dS[b == j].sum() for j in range(7)])
+    np.testing.assert_allclose(dt[0], ref, atol=1e-12)
