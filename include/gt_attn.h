@@ -158,6 +158,47 @@ gt_status_t gt_attn_merge(const float* o_parts, const float* lse_parts, int32_t 
                           int32_t H, int64_t S, int32_t d, gt_dtype_t dtype,
                           void* stream);
 
+/* Bytes of device workspace gt_attn_bwd_ring_step needs for these sizes. */
+size_t gt_attn_bwd_ring_workspace_size(int32_t H, int64_t Sq, int64_t Sk, int32_t d,
+                                       gt_dtype_t dtype);
+
+/* Backward of one ring step (Section III-A-1, Eq. (2); the chain rule through
+ * the block's share of Eq. (1)). The probabilities of the pairs (query shard
+ * row i, KV block key j) are recomputed with the merged statistics of the
+ * whole row, P[i, j] = exp(S[i, j] - LSE[i]) with S as in gt_attn_ring_step,
+ * so summing this step over every KV block of the ring is exactly the
+ * unsharded backward. The step ADDS its contributions:
+ *   dq_acc     += scale dS k_blk            dS = P * (d_o V^T - rowsum(d_o * o))
+ *   dk_acc     += scale dS^T q_shard        dv_acc += P^T d_o
+ *   dtable_acc[h, b] += sum of dS[h, i, j] over pairs whose spd byte is b
+ *   q_shard, d_o_shard  [H, Sq, d] dtype
+ *   o_shard    [H, Sq, d] dtype: the MERGED output of the shard's rows (the
+ *              result of gt_attn_merge over all blocks), not a partial
+ *   lse_shard  [H, Sq] fp32: the merged log-sum-exp of the same rows
+ *   k_blk, v_blk [H, Sk, d] dtype
+ *   spd, ld_spd, row_off, col_off  as in gt_attn_ring_step
+ *   dq_acc     [H, Sq, d] fp32, dk_acc, dv_acc [H, Sk, d] fp32,
+ *   dtable_acc [H, n_buckets] fp32: read and updated in place (zero them
+ *              before the first step of a ring)
+ *   workspace  at least gt_attn_bwd_ring_workspace_size(H, Sq, Sk, d, dtype)
+ *              bytes of device memory, 256-byte aligned, contents ignored.
+ * Sq >= 1, Sk >= 0, row_off >= 0, col_off >= 0, ld_spd >= col_off + Sk; the
+ * spd buffer must hold rows row_off .. row_off + Sq - 1. Sk = 0 touches
+ * nothing (k_blk, v_blk, spd, dk_acc, dv_acc may then be NULL). Steps on one
+ * stream are ordered; steps that update the same accumulators must not run
+ * concurrently. dtable_acc is updated with floating-point atomics. */
+gt_status_t gt_attn_bwd_ring_step(const void* q_shard, const void* o_shard,
+                                  const float* lse_shard, const void* d_o_shard, int64_t Sq,
+                                  const void* k_blk, const void* v_blk, int64_t Sk,
+                                  const uint8_t* spd, int64_t ld_spd,
+                                  int64_t row_off, int64_t col_off,
+                                  const float* table, int32_t n_buckets,
+                                  float* dq_acc, float* dk_acc, float* dv_acc,
+                                  float* dtable_acc,
+                                  void* workspace, size_t workspace_bytes,
+                                  int32_t H, int32_t d, gt_dtype_t dtype,
+                                  float scale, void* stream);
+
 /* Static, human-readable name of a status code. */
 const char* gt_status_string(gt_status_t s);
 

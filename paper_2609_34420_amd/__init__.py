@@ -10,6 +10,8 @@ If the library is missing or cannot be loaded, every call raises.
     dq, dk, dv, dtable = gt_attn_bwd(q, k, v, spd, table, o, lse, d_o)
     o_p, lse_p = gt_attn_ring_step(q_sh, k_sh, v_sh, spd_shard, row_off, col_off, table)
     o, lse = gt_attn_merge(o_parts, lse_parts, dtype=torch.bfloat16)
+    dq, dk, dv, dt = gt_attn_bwd_ring_step(q_sh, o_sh, lse_sh, do_sh, k_blk, v_blk, spd_shard,
+                                           row_off, col_off, table, acc=(dq, dk, dv, dt))
 """
 from __future__ import annotations
 
@@ -20,7 +22,8 @@ from pathlib import Path
 import torch
 
 __all__ = ["gt_attn_fwd", "gt_attn_bwd", "gt_attn_bwd_phase", "gt_attn_ring_step", "gt_attn_merge",
-           "gt_attn_bwd_workspace_size", "gt_status_string", "gt_attn_version",
+           "gt_attn_bwd_ring_step", "gt_attn_bwd_workspace_size", "gt_attn_bwd_ring_workspace_size",
+           "gt_status_string", "gt_attn_version",
            "GTError", "lib", "LIB_PATH"]
 
 LIB_PATH = Path(__file__).resolve().parent / "libgtattn.so"
@@ -63,6 +66,12 @@ def lib() -> ctypes.CDLL:
         L.gt_attn_ring_step.restype = _I32
         L.gt_attn_ring_step.argtypes = [_P, _I64, _P, _P, _I64, _P, _I64, _I64, _I64, _P, _I32,
                                         _P, _P, _I32, _I32, _I32, _F, _P]
+        L.gt_attn_bwd_ring_workspace_size.restype = ctypes.c_size_t
+        L.gt_attn_bwd_ring_workspace_size.argtypes = [_I32, _I64, _I64, _I32, _I32]
+        L.gt_attn_bwd_ring_step.restype = _I32
+        L.gt_attn_bwd_ring_step.argtypes = [_P, _P, _P, _P, _I64, _P, _P, _I64, _P, _I64, _I64, _I64,
+                                            _P, _I32, _P, _P, _P, _P, _P, ctypes.c_size_t,
+                                            _I32, _I32, _I32, _F, _P]
         L.gt_attn_merge.restype = _I32
         L.gt_attn_merge.argtypes = [_P, _P, _I32, _P, _P, _I32, _I64, _I32, _I32, _P]
         L.gt_status_string.restype = ctypes.c_char_p
@@ -202,6 +211,48 @@ def gt_attn_ring_step(q_shard, k_shard, v_shard, spd, row_off: int, col_off: int
                                  scale, _stream(stream))
     _check(st, "gt_attn_ring_step")
     return out, lse
+
+
+def gt_attn_bwd_ring_workspace_size(H: int, Sq: int, Sk: int, d: int, dtype=torch.bfloat16) -> int:
+    return int(lib().gt_attn_bwd_ring_workspace_size(
+        H, Sq, Sk, d, GT_BF16 if dtype == torch.bfloat16 else GT_F32))
+
+
+def gt_attn_bwd_ring_step(q_shard, o_shard, lse_shard, d_o_shard, k_blk, v_blk, spd,
+                          row_off: int, col_off: int, table, scale: float | None = None,
+                          acc=None, workspace=None, stream=None):
+    """Add one ring step's gradients (C ABI gt_attn_bwd_ring_step) into the
+    fp32 accumulators acc = (dq [H,Sq,d], dk [H,Sk,d], dv [H,Sk,d],
+    dtable [H,n_buckets]); acc=None starts them at zero. o_shard / lse_shard
+    are the merged forward results of the shard's rows."""
+    H, Sq, d = q_shard.shape
+    Sk = k_blk.shape[1] if k_blk is not None else 0
+    _dev_contig(q_shard, o_shard, lse_shard, d_o_shard, k_blk, v_blk, table)
+    _need(spd is None or (spd.dtype == torch.uint8 and spd.dim() == 2 and spd.stride(1) == 1),
+          "spd must be a uint8 2-D tensor with unit column stride")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dev = q_shard.device
+    if acc is None:
+        acc = (torch.zeros((H, Sq, d), device=dev, dtype=torch.float32),
+               torch.zeros((H, Sk, d), device=dev, dtype=torch.float32),
+               torch.zeros((H, Sk, d), device=dev, dtype=torch.float32),
+               torch.zeros_like(table))
+    dq, dk, dv, dtable = acc
+    _dev_contig(dq, dk, dv, dtable)
+    for t in acc:
+        _need(t.dtype == torch.float32, "accumulators must be fp32")
+    need = gt_attn_bwd_ring_workspace_size(H, Sq, Sk, d, q_shard.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=dev, dtype=torch.uint8)
+    ld = spd.stride(0) if spd is not None else 0
+    st = lib().gt_attn_bwd_ring_step(
+        _ptr(q_shard), _ptr(o_shard), _ptr(lse_shard), _ptr(d_o_shard), Sq,
+        _ptr(k_blk), _ptr(v_blk), Sk, _ptr(spd), ld, int(row_off), int(col_off),
+        _ptr(table), table.shape[1], _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dtable),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), H, d, _dt(q_shard),
+        scale, _stream(stream))
+    _check(st, "gt_attn_bwd_ring_step")
+    return dq, dk, dv, dtable
 
 
 def gt_attn_merge(o_parts, lse_parts, dtype=torch.bfloat16, out=None, lse=None, stream=None):

@@ -102,7 +102,7 @@ size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dt
   if (H < 1 || N < 1) return 0;
   const size_t rows = (size_t)H * (size_t)N;
   const size_t nblk = (size_t)((N + 255) / 256);
-  return 2 * align_up(rows * sizeof(float)) + align_up((size_t)H * nblk * 2 * sizeof(float));
+  return 2 * align_up(rows * sizeof(float)) + align_up((size_t)H * nblk * 4 * sizeof(float));
 }
 
 static gt_status_t bwd_impl(int32_t phase, const void* q, const void* k, const void* v,
@@ -135,7 +135,8 @@ static gt_status_t bwd_impl(int32_t phase, const void* q, const void* k, const v
   a.lse2 = static_cast<float*>(workspace);
   a.dlt = reinterpret_cast<float*>(static_cast<char*>(workspace) + align_up(rows * sizeof(float)));
   a.nmax = reinterpret_cast<float*>(static_cast<char*>(workspace) + 2 * align_up(rows * sizeof(float)));
-  a.H = H; a.N = N; a.scale = scale;
+  a.H = H; a.Sq = N; a.Sk = N; a.scale = scale;
+  a.row_off = 0; a.col_off = 0; a.accumulate = 0;
   a.spd_vec = spd_vec(spd, N, 0, 0);
   // The transpose is used only where its rows can be read 16 bytes at a time
   // and one key block's rows (256 of them) stay within 32-bit offsets.
@@ -162,6 +163,58 @@ gt_status_t gt_attn_bwd_phase(int32_t phase, const void* q, const void* k, const
   if (phase < 0 || phase > 2) return GT_ERR_INVALID;
   return bwd_impl(phase, q, k, v, spd, spd_t, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
                   workspace, workspace_bytes, H, N, d, dtype, scale, stream);
+}
+
+size_t gt_attn_bwd_ring_workspace_size(int32_t H, int64_t Sq, int64_t Sk, int32_t d,
+                                       gt_dtype_t dtype) {
+  (void)d;
+  (void)dtype;
+  if (H < 1 || Sq < 1 || Sk < 0) return 0;
+  const size_t rows = (size_t)H * (size_t)Sq;
+  const size_t nblk = (size_t)(((Sq > Sk ? Sq : Sk) + 255) / 256);
+  return 2 * align_up(rows * sizeof(float)) + align_up((size_t)H * nblk * 4 * sizeof(float));
+}
+
+gt_status_t gt_attn_bwd_ring_step(const void* q_shard, const void* o_shard, const float* lse_shard,
+                                  const void* d_o_shard, int64_t Sq, const void* k_blk,
+                                  const void* v_blk, int64_t Sk, const uint8_t* spd,
+                                  int64_t ld_spd, int64_t row_off, int64_t col_off,
+                                  const float* table, int32_t n_buckets, float* dq_acc,
+                                  float* dk_acc, float* dv_acc, float* dtable_acc,
+                                  void* workspace, size_t workspace_bytes, int32_t H, int32_t d,
+                                  gt_dtype_t dtype, float scale, void* stream) {
+  if (!dtype_ok(dtype)) return GT_ERR_UNSUPPORTED;
+  if (!dims_ok(d)) return GT_ERR_UNSUPPORTED;
+  if (H < 1 || Sq < 1 || Sk < 0 || row_off < 0 || col_off < 0) return GT_ERR_INVALID;
+  if (n_buckets < 1 || n_buckets > 256 || !scale_ok(scale)) return GT_ERR_INVALID;
+  if (!q_shard || !o_shard || !lse_shard || !d_o_shard || !table || !dq_acc || !dtable_acc)
+    return GT_ERR_INVALID;
+  if (Sk > 0 && (!k_blk || !v_blk || !spd || !dk_acc || !dv_acc)) return GT_ERR_INVALID;
+  if (Sk > 0 && ld_spd < col_off + Sk) return GT_ERR_INVALID;
+  if (Sk > 0 && ld_spd > kMaxLd) return GT_ERR_UNSUPPORTED;
+  if (!aligned16(q_shard) || !aligned16(o_shard) || !aligned16(d_o_shard) || !aligned16(dq_acc))
+    return GT_ERR_INVALID;
+  if (Sk > 0 && (!aligned16(k_blk) || !aligned16(v_blk) || !aligned16(dk_acc) || !aligned16(dv_acc)))
+    return GT_ERR_INVALID;
+  if (((Sq > Sk ? Sq : Sk) + 127) / 128 * (int64_t)H > kMaxGrid) return GT_ERR_INVALID;
+  const size_t need = gt_attn_bwd_ring_workspace_size(H, Sq, Sk, d, dtype);
+  if (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return GT_ERR_WORKSPACE;
+  if (Sk == 0) return GT_OK;   // an empty key block adds nothing
+  const size_t rows = (size_t)H * (size_t)Sq;
+  gt::BwdArgs a{};
+  a.q = q_shard; a.k = k_blk; a.v = v_blk;
+  a.spd = spd; a.spd_t = nullptr; a.ld_spd = ld_spd; a.row_off = row_off; a.col_off = col_off;
+  a.table = table; a.n_buckets = n_buckets;
+  a.o = o_shard; a.lse = lse_shard; a.d_o = d_o_shard;
+  a.dq = dq_acc; a.dk = dk_acc; a.dv = dv_acc; a.dtable = dtable_acc;
+  a.lse2 = static_cast<float*>(workspace);
+  a.dlt = reinterpret_cast<float*>(static_cast<char*>(workspace) + align_up(rows * sizeof(float)));
+  a.nmax = reinterpret_cast<float*>(static_cast<char*>(workspace) + 2 * align_up(rows * sizeof(float)));
+  a.H = H; a.Sq = Sq; a.Sk = Sk; a.scale = scale;
+  a.accumulate = 1;
+  a.spd_vec = spd_vec(spd, ld_spd, row_off, col_off);
+  return launched(gt::launch_bwd(a, d, dtype == GT_BF16, -1, static_cast<hipStream_t>(stream)));
 }
 
 gt_status_t gt_attn_merge(const float* o_parts, const float* lse_parts, int32_t n_parts,

@@ -23,73 +23,93 @@ constexpr int kWaves = 4;
 // ---------------------------------------------------------------------------
 // Preprocess: lse2, Dlt; dtable = 0.
 // ---------------------------------------------------------------------------
-// Preprocess, grid (ceil(N/256), H): per row lse2 = LSE log2 e (+inf for an
-// empty row), Dlt = rowsum(dO * O); per block of 256 rows the largest squared
-// norms of dO and V rows (the dK/dV stage bounds |dS| with them). Block
-// (0, 0) also zeroes dtable.
+// Preprocess, grid (ceil(max(Sq, Sk)/256), H): per query row lse2 = LSE log2 e
+// (+inf for an empty row), Dlt = rowsum(dO * O); per block of 256 rows the
+// largest squared norms of dO rows (query side) and V rows (key side) and the
+// largest |Dlt|: the dK/dV stage bounds |dS| with them. Block (0, 0) also
+// zeroes dtable unless the call accumulates.
 template <int D, bool BF16>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs a) {
-  __shared__ float red[2][4];
+  __shared__ float red[3][4];
   const int h = blockIdx.y;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (blockIdx.x == 0 && blockIdx.y == 0) {
+  if (blockIdx.x == 0 && blockIdx.y == 0 && !a.accumulate) {
     for (int t = threadIdx.x; t < a.H * a.n_buckets; t += 256) a.dtable[t] = 0.0f;
   }
-  float nd = 0.0f, nv = 0.0f;
-  if (i < a.N) {
-    const int64_t row = (int64_t)h * a.N + i;
+  float nd = 0.0f, nv = 0.0f, nl = 0.0f;
+  if (i < a.Sq) {
+    const int64_t row = (int64_t)h * a.Sq + i;
     float acc = 0.0f;
     if constexpr (BF16) {
       const uint16_t* o = reinterpret_cast<const uint16_t*>(a.o) + row * D;
       const uint16_t* d = reinterpret_cast<const uint16_t*>(a.d_o) + row * D;
-      const uint16_t* v = reinterpret_cast<const uint16_t*>(a.v) + row * D;
 #pragma unroll
       for (int c = 0; c < D; c += 8) {
         const uint4 ov = *reinterpret_cast<const uint4*>(o + c);
         const uint4 dv = *reinterpret_cast<const uint4*>(d + c);
-        const uint4 vv = *reinterpret_cast<const uint4*>(v + c);
         const uint16_t* op = reinterpret_cast<const uint16_t*>(&ov);
         const uint16_t* dp = reinterpret_cast<const uint16_t*>(&dv);
-        const uint16_t* vp = reinterpret_cast<const uint16_t*>(&vv);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float x = bf2f(dp[e]), y = bf2f(vp[e]);
+          const float x = bf2f(dp[e]);
           acc = fmaf(bf2f(op[e]), x, acc);
           nd = fmaf(x, x, nd);
-          nv = fmaf(y, y, nv);
         }
       }
     } else {
       const float* o = reinterpret_cast<const float*>(a.o) + row * D;
       const float* d = reinterpret_cast<const float*>(a.d_o) + row * D;
-      const float* v = reinterpret_cast<const float*>(a.v) + row * D;
 #pragma unroll
       for (int c = 0; c < D; ++c) {
         acc = fmaf(o[c], d[c], acc);
         nd = fmaf(d[c], d[c], nd);
-        nv = fmaf(v[c], v[c], nv);
       }
     }
     a.dlt[row] = acc;
+    nl = fabsf(acc);
     const float L = a.lse[row];
     a.lse2[row] = (L == -INFINITY) ? INFINITY : L * kLog2e;
+  }
+  if (i < a.Sk) {
+    const int64_t row = (int64_t)h * a.Sk + i;
+    if constexpr (BF16) {
+      const uint16_t* v = reinterpret_cast<const uint16_t*>(a.v) + row * D;
+#pragma unroll
+      for (int c = 0; c < D; c += 8) {
+        const uint4 vv = *reinterpret_cast<const uint4*>(v + c);
+        const uint16_t* vp = reinterpret_cast<const uint16_t*>(&vv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float y = bf2f(vp[e]);
+          nv = fmaf(y, y, nv);
+        }
+      }
+    } else {
+      const float* v = reinterpret_cast<const float*>(a.v) + row * D;
+#pragma unroll
+      for (int c = 0; c < D; ++c) nv = fmaf(v[c], v[c], nv);
+    }
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     nd = fmaxf(nd, __shfl_xor(nd, off));
     nv = fmaxf(nv, __shfl_xor(nv, off));
+    nl = fmaxf(nl, __shfl_xor(nl, off));
   }
   const int wave = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
     red[0][wave] = nd;
     red[1][wave] = nv;
+    red[2][wave] = nl;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     const int64_t nblk = gridDim.x;
-    float* out = a.nmax + ((int64_t)h * nblk + blockIdx.x) * 2;
+    float* out = a.nmax + ((int64_t)h * nblk + blockIdx.x) * 4;
     out[0] = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
     out[1] = fmaxf(fmaxf(red[1][0], red[1][1]), fmaxf(red[1][2], red[1][3]));
+    out[2] = fmaxf(fmaxf(red[2][0], red[2][1]), fmaxf(red[2][2], red[2][3]));
+    out[3] = 0.0f;
   }
 }
 
@@ -104,19 +124,19 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
   __shared__ float sT[256];
   __shared__ float sH[256];
   const int tid = threadIdx.x;
-  const int64_t nqb = (a.N + 127) / 128;
+  const int64_t nqb = (a.Sq + 127) / 128;
   const int h = (int)(blockIdx.x / nqb);
   const int64_t i = (blockIdx.x % nqb) * 128 + tid;
   for (int t = tid; t < 256; t += 128) {
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + t] : 0.0f;
     sH[t] = 0.0f;
   }
-  const int64_t hoff = (int64_t)h * a.N * D;
-  const float* qh = reinterpret_cast<const float*>(a.q) + hoff;
-  const float* kh = reinterpret_cast<const float*>(a.k) + hoff;
-  const float* vh = reinterpret_cast<const float*>(a.v) + hoff;
-  const float* oh = reinterpret_cast<const float*>(a.d_o) + hoff;
-  const bool ok = i < a.N;
+  const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
+  const float* qh = reinterpret_cast<const float*>(a.q) + hq;
+  const float* kh = reinterpret_cast<const float*>(a.k) + hk;
+  const float* vh = reinterpret_cast<const float*>(a.v) + hk;
+  const float* oh = reinterpret_cast<const float*>(a.d_o) + hq;
+  const bool ok = i < a.Sq;
   float qv[D], dov[D], acc[D];
 #pragma unroll
   for (int c = 0; c < D; ++c) {
@@ -124,20 +144,20 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
     dov[c] = ok ? oh[i * D + c] : 0.0f;
     acc[c] = 0.0f;
   }
-  const float L = ok ? a.lse[(int64_t)h * a.N + i] : -INFINITY;
-  const float dlt = ok ? a.dlt[(int64_t)h * a.N + i] : 0.0f;
-  const uint8_t* srow = ok ? a.spd + i * a.ld_spd : nullptr;
-  for (int64_t j0 = 0; j0 < a.N; j0 += TK) {
+  const float L = ok ? a.lse[(int64_t)h * a.Sq + i] : -INFINITY;
+  const float dlt = ok ? a.dlt[(int64_t)h * a.Sq + i] : 0.0f;
+  const uint8_t* srow = ok ? a.spd + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
+  for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
     __syncthreads();
     for (int t = tid; t < TK * D; t += 128) {
       const int r = t / D, c = t % D;
-      const bool in = j0 + r < a.N;
+      const bool in = j0 + r < a.Sk;
       sK[r][c] = in ? kh[(j0 + r) * D + c] : 0.0f;
       sV[r][c] = in ? vh[(j0 + r) * D + c] : 0.0f;
     }
     __syncthreads();
     if (!ok || L == -INFINITY) continue;
-    const int nk = (int)((a.N - j0) < TK ? (a.N - j0) : TK);
+    const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
     for (int r = 0; r < nk; ++r) {
       float s = 0.0f, dp = 0.0f;
 #pragma unroll
@@ -154,9 +174,9 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
     }
   }
   if (ok) {
-    float* dqp = reinterpret_cast<float*>(a.dq) + hoff + i * D;
+    float* dqp = reinterpret_cast<float*>(a.dq) + hq + i * D;
 #pragma unroll
-    for (int c = 0; c < D; ++c) dqp[c] = acc[c] * a.scale;
+    for (int c = 0; c < D; ++c) dqp[c] = (a.accumulate ? dqp[c] : 0.0f) + acc[c] * a.scale;
   }
   __syncthreads();
   for (int t = tid; t < a.n_buckets; t += 128)
@@ -171,17 +191,18 @@ __global__ __launch_bounds__(128) void bwd_dkdv_f32_kernel(BwdArgs a) {
   __shared__ float sL[TQ], sD[TQ];
   __shared__ float sT[256];
   const int tid = threadIdx.x;
-  const int64_t nkb = (a.N + 127) / 128;
+  const int64_t nkb = (a.Sk + 127) / 128;
   const int h = (int)(blockIdx.x / nkb);
   const int64_t j = (blockIdx.x % nkb) * 128 + tid;
   for (int t = tid; t < 256; t += 128)
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + t] : 0.0f;
-  const int64_t hoff = (int64_t)h * a.N * D;
-  const float* qh = reinterpret_cast<const float*>(a.q) + hoff;
-  const float* kh = reinterpret_cast<const float*>(a.k) + hoff;
-  const float* vh = reinterpret_cast<const float*>(a.v) + hoff;
-  const float* oh = reinterpret_cast<const float*>(a.d_o) + hoff;
-  const bool ok = j < a.N;
+  const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
+  const float* qh = reinterpret_cast<const float*>(a.q) + hq;
+  const float* kh = reinterpret_cast<const float*>(a.k) + hk;
+  const float* vh = reinterpret_cast<const float*>(a.v) + hk;
+  const float* oh = reinterpret_cast<const float*>(a.d_o) + hq;
+  const uint8_t* sbase = a.spd + a.row_off * a.ld_spd + a.col_off;
+  const bool ok = j < a.Sk;
   float kv[D], vv[D], dk[D], dv[D];
 #pragma unroll
   for (int c = 0; c < D; ++c) {
@@ -190,22 +211,22 @@ __global__ __launch_bounds__(128) void bwd_dkdv_f32_kernel(BwdArgs a) {
     dk[c] = 0.0f;
     dv[c] = 0.0f;
   }
-  for (int64_t i0 = 0; i0 < a.N; i0 += TQ) {
+  for (int64_t i0 = 0; i0 < a.Sq; i0 += TQ) {
     __syncthreads();
     for (int t = tid; t < TQ * D; t += 128) {
       const int r = t / D, c = t % D;
-      const bool in = i0 + r < a.N;
+      const bool in = i0 + r < a.Sq;
       sQ[r][c] = in ? qh[(i0 + r) * D + c] : 0.0f;
       sO[r][c] = in ? oh[(i0 + r) * D + c] : 0.0f;
     }
     for (int t = tid; t < TQ; t += 128) {
-      const bool in = i0 + t < a.N;
-      sL[t] = in ? a.lse[(int64_t)h * a.N + i0 + t] : -INFINITY;
-      sD[t] = in ? a.dlt[(int64_t)h * a.N + i0 + t] : 0.0f;
+      const bool in = i0 + t < a.Sq;
+      sL[t] = in ? a.lse[(int64_t)h * a.Sq + i0 + t] : -INFINITY;
+      sD[t] = in ? a.dlt[(int64_t)h * a.Sq + i0 + t] : 0.0f;
     }
     __syncthreads();
     if (!ok) continue;
-    const int nq = (int)((a.N - i0) < TQ ? (a.N - i0) : TQ);
+    const int nq = (int)((a.Sq - i0) < TQ ? (a.Sq - i0) : TQ);
     for (int r = 0; r < nq; ++r) {
       if (sL[r] == -INFINITY) continue;
       float s = 0.0f, dp = 0.0f;
@@ -214,7 +235,7 @@ __global__ __launch_bounds__(128) void bwd_dkdv_f32_kernel(BwdArgs a) {
         s = fmaf(sQ[r][c], kv[c], s);
         dp = fmaf(sO[r][c], vv[c], dp);
       }
-      const float p = expf(s + sT[a.spd[(i0 + r) * a.ld_spd + j]] - sL[r]);
+      const float p = expf(s + sT[sbase[(i0 + r) * a.ld_spd + j]] - sL[r]);
       const float ds = p * (dp - sD[r]);
 #pragma unroll
       for (int c = 0; c < D; ++c) {
@@ -224,12 +245,12 @@ __global__ __launch_bounds__(128) void bwd_dkdv_f32_kernel(BwdArgs a) {
     }
   }
   if (!ok) return;
-  float* dkp = reinterpret_cast<float*>(a.dk) + hoff + j * D;
-  float* dvp = reinterpret_cast<float*>(a.dv) + hoff + j * D;
+  float* dkp = reinterpret_cast<float*>(a.dk) + hk + j * D;
+  float* dvp = reinterpret_cast<float*>(a.dv) + hk + j * D;
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    dkp[c] = dk[c] * a.scale;
-    dvp[c] = dv[c];
+    dkp[c] = (a.accumulate ? dkp[c] : 0.0f) + dk[c] * a.scale;
+    dvp[c] = (a.accumulate ? dvp[c] : 0.0f) + dv[c];
   }
 }
 
@@ -237,7 +258,8 @@ template <int D>
 hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
   hipError_t e = hipSuccess;
   if (phase < 0 || phase == 0) {
-    const dim3 grid((unsigned)((a.N + 255) / 256), (unsigned)a.H);
+    const int64_t rows = a.Sq > a.Sk ? a.Sq : a.Sk;
+    const dim3 grid((unsigned)((rows + 255) / 256), (unsigned)a.H);
     if (bf16)
       hipLaunchKernelGGL((bwd_prep_kernel<D, true>), grid, dim3(256), 0, s, a);
     else
@@ -254,13 +276,13 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
     return e;
   }
   // fp32: dK/dV in phase 1, dQ and dtable in phase 2
-  const int64_t nb = (a.N + 127) / 128;
+  const int64_t nkb = (a.Sk + 127) / 128, nqb = (a.Sq + 127) / 128;
   if (phase < 0 || phase == 1) {
-    hipLaunchKernelGGL((bwd_dkdv_f32_kernel<D>), dim3((unsigned)(nb * a.H)), dim3(128), 0, s, a);
+    hipLaunchKernelGGL((bwd_dkdv_f32_kernel<D>), dim3((unsigned)(nkb * a.H)), dim3(128), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (phase < 0 || phase == 2) {
-    hipLaunchKernelGGL((bwd_dq_f32_kernel<D>), dim3((unsigned)(nb * a.H)), dim3(128), 0, s, a);
+    hipLaunchKernelGGL((bwd_dq_f32_kernel<D>), dim3((unsigned)(nqb * a.H)), dim3(128), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return e;

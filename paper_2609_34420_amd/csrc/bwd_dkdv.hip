@@ -17,9 +17,10 @@
 // histogram is fixed point: LDS float atomics are slow on this hardware,
 // 64-bit integer adds are not. dS is accumulated as round(dS * 2^F), where
 // the power-of-two scale per head keeps every term below 2^30 in magnitude:
-// |dS_ij| <= |dO_i . V_j - Dlt_i| <= 2 |dO_i| max_j |V_j| (Cauchy-Schwarz,
-// with O_i a convex combination of the V_j), and the prepare stage records
-// block maxima of |dO_i| and |V_j|. The scale enters for free through the
+// |dS_ij| <= |dO_i . V_j - Dlt_i| <= max_i |dO_i| max_j |V_j| + max_i |Dlt_i|
+// (P_ij <= 1, Cauchy-Schwarz), and the prepare stage records block maxima of
+// |dO_i|, |V_j| and |Dlt_i|. Dlt enters on its own because in a ring step O
+// mixes the values of every key block, not only of the keys at hand. The scale enters for free through the
 // V operand of dP (and the dP accumulator start), so dS arrives already
 // scaled; dK takes 2^-F in its final multiply. Sums of up to 2^32 terms fit
 // in 64 bits. The histogram is flushed once per workgroup, converted back
@@ -61,7 +62,7 @@ struct DkdvSmem {
   uint16_t o[2][kBQ * D];
   float init_s[2][kBQ];             // -LSE log2 e / (scale log2 e); -inf for empty rows
   float init_p[2][kBQ];             // -Dlt 2^F
-  float red[2][kNW];
+  float red[3][kNW];
 };
 
 // Per-lane LDS element offsets of the operand reads (tile-relative; the
@@ -248,13 +249,14 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   constexpr int NCB = D / 32;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 5;
-  const int64_t hoff = (int64_t)h * a.N * D;
-  const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + hoff;
-  const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + hoff;
-  const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + hoff;
-  const uint16_t* oh = reinterpret_cast<const uint16_t*>(a.d_o) + hoff;
-  const float* lse2h = a.lse2 + (int64_t)h * a.N;
-  const float* dlth = a.dlt + (int64_t)h * a.N;
+  const int64_t hq = (int64_t)h * a.Sq * D;   // query-side rows
+  const int64_t hk = (int64_t)h * a.Sk * D;   // key-side rows
+  const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + hq;
+  const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + hk;
+  const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + hk;
+  const uint16_t* oh = reinterpret_cast<const uint16_t*>(a.d_o) + hq;
+  const float* lse2h = a.lse2 + (int64_t)h * a.Sq;
+  const float* dlth = a.dlt + (int64_t)h * a.Sq;
   const float sl2 = a.scale * kLog2e;
   const float inv_sl2 = 1.0f / sl2;
 
@@ -278,10 +280,10 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   }
 
   const int64_t ld = a.ld_spd;
-  const int64_t jc = jok ? j : a.N - 1;
+  const int64_t jc = jok ? j : a.Sk - 1;
   const uint32_t key_off = (uint32_t)(jc - key0);
-  const uint8_t* spd_cols = a.spd + key0;
-  const int64_t ntiles = (a.N + kBQ - 1) / kBQ;
+  const uint8_t* spd_cols = a.spd + a.row_off * ld + a.col_off + key0;
+  const int64_t ntiles = (a.Sq + kBQ - 1) / kBQ;
   const DkdvOffsets<D> off;
 
   // Bucket indices of this lane's key: TR reads 16 queries as one 16-byte
@@ -290,21 +292,21 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   using BT = std::conditional_t<TR, uint32_t, uint8_t>;
   constexpr int NBT = TR ? 4 : 16;
   const __amdgpu_buffer_rsrc_t rs_t =
-      make_rsrc_n(TR ? a.spd_t + key0 * ld : a.spd, ((a.N - key0 < kBK ? a.N - key0 : kBK)) * ld);
+      make_rsrc_n(TR ? a.spd_t + key0 * ld : a.spd, ((a.Sk - key0 < kBK ? a.Sk - key0 : kBK)) * ld);
   const uint32_t voff_t = (uint32_t)((jc - key0) * ld) + 16u * (uint32_t)g;
   auto fetch = [&](int64_t i_base, BT* dst) {
     if constexpr (TR) {
       buf_u128(rs_t, voff_t, (uint32_t)i_base, reinterpret_cast<uint32_t*>(dst));
     } else {
-      load_bytes<QFULL>(spd_cols, ld, i_base, a.N, key_off, reinterpret_cast<uint8_t*>(dst));
+      load_bytes<QFULL>(spd_cols, ld, i_base, a.Sq, key_off, reinterpret_cast<uint8_t*>(dst));
     }
   };
 
   QTileStage<D> st;
-  st.load(qh, oh, lse2h, dlth, 0, a.N);
+  st.load(qh, oh, lse2h, dlth, 0, a.Sq);
   BT bA[NBT], bB[NBT];
   fetch(0, bA);
-  st.template store<0>(sm, 0, a.N, inv_sl2, sF);
+  st.template store<0>(sm, 0, a.Sq, inv_sl2, sF);
   wait_loads();
   __syncthreads();
 
@@ -317,13 +319,13 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
     const bool more = t + 1 < ntiles;
     const int64_t inext = more ? i0 + kBQ : i0;
     fetch(i0 + 32, bB);
-    st.load(qh, oh, lse2h, dlth, inext, a.N);
+    st.load(qh, oh, lse2h, dlth, inext, a.Sq);
     sched_fence();
     dkdv_subblock<D, NB, KTAIL, BUF, 0>(sm, off, kf, vf, bA, sl2, jok, dk, dv);
     fetch(inext, bA);
     sched_fence();
     dkdv_subblock<D, NB, KTAIL, BUF, 1>(sm, off, kf, vf, bB, sl2, jok, dk, dv);
-    if (more) st.template store<BUF ^ 1>(sm, inext, a.N, inv_sl2, sF);
+    if (more) st.template store<BUF ^ 1>(sm, inext, a.Sq, inv_sl2, sF);
     __syncthreads();
   };
   int64_t t = 0;
@@ -334,9 +336,28 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   if (t < ntiles) step(t, std::integral_constant<int, 0>());
 
   const float dk_scale = a.scale * ldexpf(1.0f, -fexp);
-  if (jok) {
-    uint16_t* dkp = reinterpret_cast<uint16_t*>(a.dk) + hoff + j * D;
-    uint16_t* dvp = reinterpret_cast<uint16_t*>(a.dv) + hoff + j * D;
+  if (jok && a.accumulate) {
+    // fp32 partials of the key block, accumulated across ring steps
+    float* dkp = reinterpret_cast<float*>(a.dk) + hk + j * D;
+    float* dvp = reinterpret_cast<float*>(a.dv) + hk + j * D;
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = cb * 32 + 8 * u + 4 * g;
+        float4 xk = *reinterpret_cast<const float4*>(dkp + c);
+        float4 xv = *reinterpret_cast<const float4*>(dvp + c);
+        xk.x += dk[cb][4 * u] * dk_scale; xk.y += dk[cb][4 * u + 1] * dk_scale;
+        xk.z += dk[cb][4 * u + 2] * dk_scale; xk.w += dk[cb][4 * u + 3] * dk_scale;
+        xv.x += dv[cb][4 * u]; xv.y += dv[cb][4 * u + 1];
+        xv.z += dv[cb][4 * u + 2]; xv.w += dv[cb][4 * u + 3];
+        *reinterpret_cast<float4*>(dkp + c) = xk;
+        *reinterpret_cast<float4*>(dvp + c) = xv;
+      }
+    }
+  } else if (jok) {
+    uint16_t* dkp = reinterpret_cast<uint16_t*>(a.dk) + hk + j * D;
+    uint16_t* dvp = reinterpret_cast<uint16_t*>(a.dv) + hk + j * D;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
@@ -363,12 +384,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   float (*red)[kNW] = sm.red;
   const int tid = threadIdx.x;
   const int wave = wave_id(), col = tid & 31;
-  const int64_t nkb = (a.N + kBK - 1) / kBK;
+  const int64_t nkb = (a.Sk + kBK - 1) / kBK;
   const int64_t lid = xcd_remap(blockIdx.x, nkb * a.H);
   const int h = (int)(lid % a.H);
   const int64_t kblk = lid / a.H;
   const int64_t j = kblk * kBK + wave * 32 + col;
-  const bool jok = j < a.N;
+  const bool jok = j < a.Sk;
 
   for (int t = tid; t < DkdvSmem<D, NB>::ENT; t += kThreads) {
     const int bkt = t / CPY;
@@ -377,34 +398,38 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
     hist[t] = 0ull;
   }
 
-  // Fixed-point exponent F of this head: 2 max|dO| max|V| 2^F <= 2^30
-  // (a 1.5 % margin covers the bf16 rounding of O and of the products).
+  // Fixed-point exponent F of this head: (max|dO| max|V| + max|Dlt|) 2^F
+  // <= 2^30 (a 1.5 % margin covers the rounding of P and of the products).
   {
-    const int64_t nblk = (a.N + 255) / 256;
-    const float* nm = a.nmax + (int64_t)h * nblk * 2;
-    float md = 0.0f, mv = 0.0f;
+    const int64_t nblk = ((a.Sq > a.Sk ? a.Sq : a.Sk) + 255) / 256;
+    const float* nm = a.nmax + (int64_t)h * nblk * 4;
+    float md = 0.0f, mv = 0.0f, ml = 0.0f;
     for (int64_t t = tid; t < nblk; t += kThreads) {
-      md = fmaxf(md, nm[2 * t]);
-      mv = fmaxf(mv, nm[2 * t + 1]);
+      md = fmaxf(md, nm[4 * t]);
+      mv = fmaxf(mv, nm[4 * t + 1]);
+      ml = fmaxf(ml, nm[4 * t + 2]);
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
       md = fmaxf(md, __shfl_xor(md, off));
       mv = fmaxf(mv, __shfl_xor(mv, off));
+      ml = fmaxf(ml, __shfl_xor(ml, off));
     }
     if ((tid & 63) == 0) {
       red[0][wave] = md;
       red[1][wave] = mv;
+      red[2][wave] = ml;
     }
   }
   __syncthreads();
-  float md = red[0][0], mv = red[1][0];
+  float md = red[0][0], mv = red[1][0], ml = red[2][0];
 #pragma unroll
   for (int w = 1; w < kNW; ++w) {
     md = fmaxf(md, red[0][w]);
     mv = fmaxf(mv, red[1][w]);
+    ml = fmaxf(ml, red[2][w]);
   }
-  const float bound = 2.03f * sqrtf(md) * sqrtf(mv);
+  const float bound = 1.015f * (sqrtf(md) * sqrtf(mv) + ml);
   int fexp = 40;
   if (bound > 0.0f && bound < INFINITY) {
     int e;
@@ -413,7 +438,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
     fexp = fexp > 40 ? 40 : (fexp < -100 ? -100 : fexp);
   }
 
-  if ((kblk + 1) * kBK <= a.N)
+  if ((kblk + 1) * kBK <= a.Sk)
     dkdv_main<D, NB, false, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
   else
     dkdv_main<D, NB, true, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
@@ -431,9 +456,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
 }  // namespace
 
 hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s) {
-  const int64_t nkb = (a.N + kBK - 1) / kBK;
+  const int64_t nkb = (a.Sk + kBK - 1) / kBK;
   const dim3 grid((unsigned)(nkb * a.H));
-  const bool qfull = a.N % kBQ == 0;
+  const bool qfull = a.Sq % kBQ == 0;
 #define GT_DKDV_LAUNCH(D_, NB_)                                                                     \
   {                                                                                                 \
     if (a.spd_t) {                                                                                  \

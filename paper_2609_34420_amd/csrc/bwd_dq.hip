@@ -107,7 +107,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
   const int lane = tid & 63, wave = wave_id();
   const int col = lane & 31, g = lane >> 5;
 
-  const int64_t nqb = (a.N + BR - 1) / BR;
+  const int64_t nqb = (a.Sq + BR - 1) / BR;
   const int64_t lid = xcd_remap(blockIdx.x, nqb * a.H);
   const int h = (int)(lid % a.H);
   const int64_t qblk = lid / a.H;
@@ -116,11 +116,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
   for (int t = tid; t < 256; t += kThreads)
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + t] * kLog2e : 0.0f;
 
-  const int64_t hoff = (int64_t)h * a.N * D;
-  const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + hoff;
-  const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + hoff;
-  const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + hoff;
-  const uint16_t* oh = reinterpret_cast<const uint16_t*>(a.d_o) + hoff;
+  const int64_t hq = (int64_t)h * a.Sq * D;   // query-side rows
+  const int64_t hk = (int64_t)h * a.Sk * D;   // key-side rows
+  const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + hq;
+  const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + hk;
+  const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + hk;
+  const uint16_t* oh = reinterpret_cast<const uint16_t*>(a.d_o) + hq;
   const float sl2 = a.scale * kLog2e;
 
   // Q^T, dO^T operands and statistics; rows past N load the clamped row N-1
@@ -133,16 +134,16 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int64_t i = qbase + qb * 32 + col;
-    qrow[qb] = i < a.N ? i : a.N - 1;
+    qrow[qb] = i < a.Sq ? i : a.Sq - 1;
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
       qf[qb][kc] = *reinterpret_cast<const bf16x8*>(qh + qrow[qb] * D + kc * 16 + g * 8);
       df[qb][kc] = *reinterpret_cast<const bf16x8*>(oh + qrow[qb] * D + kc * 16 + g * 8);
     }
-    const float l2 = a.lse2[(int64_t)h * a.N + qrow[qb]];
-    const float dl = a.dlt[(int64_t)h * a.N + qrow[qb]];
-    const float is = i < a.N ? -l2 * inv_sl2 : -INFINITY;   // padded rows: P = 0
-    const float ip = i < a.N ? -dl : 0.0f;
+    const float l2 = a.lse2[(int64_t)h * a.Sq + qrow[qb]];
+    const float dl = a.dlt[(int64_t)h * a.Sq + qrow[qb]];
+    const float is = i < a.Sq ? -l2 * inv_sl2 : -INFINITY;   // padded rows: P = 0
+    const float ip = i < a.Sq ? -dl : 0.0f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       init_s[qb][r] = is;
@@ -153,13 +154,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
   }
 
   const int64_t ld = a.ld_spd;
-  const int64_t rb = qbase < a.N ? qbase : a.N - 1;
-  const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.spd + rb * ld);
+  const int64_t rb = qbase < a.Sq ? qbase : a.Sq - 1;
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.spd + (a.row_off + rb) * ld + a.col_off);
   uint32_t voff[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) voff[qb] = (uint32_t)((qrow[qb] - rb) * ld) + 16u * g;
   auto fetch_spd = [&](int64_t jt, uint32_t (&w)[QB][KB][4]) {
-    if (FULL || (VEC && jt + kBC <= a.N)) {
+    if (FULL || (VEC && jt + kBC <= a.Sk)) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
@@ -167,19 +168,19 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
     } else {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
-        const uint8_t* row = a.spd + qrow[qb] * ld;
+        const uint8_t* row = a.spd + (a.row_off + qrow[qb]) * ld + a.col_off;
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) load_spd16_bytes(row, jt + kb * 32 + 16 * g, a.N, w[qb][kb]);
+        for (int kb = 0; kb < KB; ++kb) load_spd16_bytes(row, jt + kb * 32 + 16 * g, a.Sk, w[qb][kb]);
       }
     }
   };
 
-  const int64_t ntiles = (a.N + kBC - 1) / kBC;
+  const int64_t ntiles = (a.Sk + kBC - 1) / kBC;
   const DqOffsets<D> off;
   Stage stK, stV;
   uint32_t wA[QB][KB][4], wB[QB][KB][4];   // spd words of even / odd tiles
-  stK.load(tile_rsrc<D>(kh, 0, a.N));
-  stV.load(tile_rsrc<D>(vh, 0, a.N));
+  stK.load(tile_rsrc<D>(kh, 0, a.Sk));
+  stV.load(tile_rsrc<D>(vh, 0, a.Sk));
   fetch_spd(0, wA);
   stK.store(sK[0]);
   stV.store(sV[0]);
@@ -197,11 +198,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
     const int64_t j0 = t * kBC;
     const bool more = t + 1 < ntiles;
     const int64_t jn = more ? j0 + kBC : j0;
-    stK.load(tile_rsrc<D>(kh, jn, a.N));
-    stV.load(tile_rsrc<D>(vh, jn, a.N));
+    stK.load(tile_rsrc<D>(kh, jn, a.Sk));
+    stV.load(tile_rsrc<D>(vh, jn, a.Sk));
     fetch_spd(jn, wnext);
     sched_fence();
-    dq_tile<D, QB, MASK>(sK[BUF], sV[BUF], sT, off, qf, df, init_s, init_p, wcur, j0, a.N, sl2, acc);
+    dq_tile<D, QB, MASK>(sK[BUF], sV[BUF], sT, off, qf, df, init_s, init_p, wcur, j0, a.Sk, sl2, acc);
     if (more) {
       stK.store(sK[BUF ^ 1]);
       stV.store(sV[BUF ^ 1]);
@@ -212,7 +213,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
   using B1 = std::integral_constant<int, 1>;
   using Full = std::false_type;
   using Part = std::true_type;
-  const int64_t nfull = FULL ? ntiles : a.N / kBC;
+  const int64_t nfull = FULL ? ntiles : a.Sk / kBC;
   int64_t t = 0;
   for (; t + 1 < nfull; t += 2) {
     step(t, B0(), Full());
@@ -228,8 +229,23 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int64_t i = qbase + qb * 32 + col;
-    if (i >= a.N) continue;
-    uint16_t* dqp = reinterpret_cast<uint16_t*>(a.dq) + hoff + i * D;
+    if (i >= a.Sq) continue;
+    if (a.accumulate) {   // fp32 partial of the query shard, accumulated across ring steps
+      float* dqa = reinterpret_cast<float*>(a.dq) + hq + i * D;
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int c = cb * 32 + 8 * u + 4 * g;
+          float4 x = *reinterpret_cast<const float4*>(dqa + c);
+          x.x += acc[qb][cb][4 * u] * a.scale; x.y += acc[qb][cb][4 * u + 1] * a.scale;
+          x.z += acc[qb][cb][4 * u + 2] * a.scale; x.w += acc[qb][cb][4 * u + 3] * a.scale;
+          *reinterpret_cast<float4*>(dqa + c) = x;
+        }
+      }
+      continue;
+    }
+    uint16_t* dqp = reinterpret_cast<uint16_t*>(a.dq) + hq + i * D;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
@@ -249,9 +265,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_bf16_kernel(BwdArgs a) {
 hipError_t launch_dq_bf16(const BwdArgs& a, int d, hipStream_t s) {
   constexpr int QB = 1;
   constexpr int BR = kWaves * 32 * QB;
-  const int64_t nqb = (a.N + BR - 1) / BR;
+  const int64_t nqb = (a.Sq + BR - 1) / BR;
   const dim3 grid((unsigned)(nqb * a.H));
-  const bool full = a.spd_vec && a.N % kBC == 0;
+  const bool full = a.spd_vec && a.Sk % kBC == 0;
   if (d == 64) {
     if (full)
       hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, QB, true, true>), grid, dim3(kThreads), 0, s, a);

@@ -27,13 +27,19 @@ struct FwdArgs {
   int32_t spd_vec;        // every 16-byte spd group is 16-byte aligned
 };
 
+// Backward of a query block (Sq rows: q, o, d_o, lse, dq and the workspace
+// rows) against a key block (Sk rows: k, v, dk, dv). The full backward has
+// Sq = Sk = N and zero offsets; a context-parallel ring step has the rank's
+// query shard, the KV block it holds and their global spd offsets.
 struct BwdArgs {
   const void* q;
   const void* k;
   const void* v;
-  const uint8_t* spd;
-  const uint8_t* spd_t;   // transpose of spd (same ld), or null: gather columns
+  const uint8_t* spd;     // (query i, key j) at spd[(row_off + i) * ld_spd + col_off + j]
+  const uint8_t* spd_t;   // transpose of spd (same ld, zero offsets), or null: gather columns
   int64_t ld_spd;
+  int64_t row_off;
+  int64_t col_off;
   const float* table;
   int32_t n_buckets;
   const void* o;
@@ -45,11 +51,14 @@ struct BwdArgs {
   float* dtable;
   float* lse2;            // workspace [H, N]: LSE * log2(e), +inf for empty rows
   float* dlt;             // workspace [H, N]: rowsum(dO * O)
-  float* nmax;            // workspace [H, ceil(N/256), 2]: block max of |dO_i|^2, |V_i|^2
+  float* nmax;            // workspace [H, ceil(max(Sq, Sk)/256), 4]: per block of 256 rows the
+                          // max of |dO_i|^2, |V_j|^2, |Dlt_i| (and one pad)
   int32_t H;
-  int64_t N;
+  int64_t Sq;
+  int64_t Sk;
   float scale;
-  int32_t spd_vec;
+  int32_t spd_vec;        // every 16-byte spd group of the block is 16-byte aligned
+  int32_t accumulate;     // 1: dq, dk, dv are fp32 and receive +=; dtable is not cleared
 };
 
 struct MergeArgs {

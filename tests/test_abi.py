@@ -26,6 +26,7 @@ def test_library_exports_every_declared_symbol():
     L = gt.lib()
     syms = declared_symbols()
     assert {"gt_attn_fwd", "gt_attn_bwd", "gt_attn_ring_step", "gt_attn_merge",
+            "gt_attn_bwd_ring_step", "gt_attn_bwd_ring_workspace_size",
             "gt_attn_bwd_workspace_size", "gt_status_string"} <= set(syms)
     for s in syms:
         assert hasattr(L, s), s
@@ -107,10 +108,57 @@ def test_bwd_validation(kw, code):
 
 def test_bwd_workspace_size():
     L = gt.lib()
-    # two fp32 [H, N] arrays and fp32 [H, ceil(N/256), 2], each padded to 256 bytes
-    assert L.gt_attn_bwd_workspace_size(8, 131072, 64, BF16) == 2 * 8 * 131072 * 4 + 8 * 512 * 2 * 4
+    # two fp32 [H, N] arrays and fp32 [H, ceil(N/256), 4], each padded to 256 bytes
+    assert L.gt_attn_bwd_workspace_size(8, 131072, 64, BF16) == 2 * 8 * 131072 * 4 + 8 * 512 * 4 * 4
     assert L.gt_attn_bwd_workspace_size(1, 7, 32, F32) == 3 * 256
     assert L.gt_attn_bwd_workspace_size(0, 7, 32, F32) == 0
+
+
+def _bwd_ring(**kw):
+    H, Sq, Sk, d = 4, 100, 64, 64
+    need = gt.lib().gt_attn_bwd_ring_workspace_size(H, Sq, Sk, d, BF16)
+    a = dict(q=FAKE, o=FAKE, lse=FAKE, do=FAKE, Sq=Sq, k=FAKE, v=FAKE, Sk=Sk, spd=FAKE, ld=4096,
+             ro=0, co=128, table=FAKE, nb=32, dq=FAKE, dk=FAKE, dv=FAKE, dt=FAKE, ws=FAKE, wsb=need,
+             H=H, d=d, dtype=BF16, scale=0.125)
+    a.update(kw)
+    return gt.lib().gt_attn_bwd_ring_step(
+        a["q"], a["o"], a["lse"], a["do"], a["Sq"], a["k"], a["v"], a["Sk"], a["spd"], a["ld"],
+        a["ro"], a["co"], a["table"], a["nb"], a["dq"], a["dk"], a["dv"], a["dt"], a["ws"], a["wsb"],
+        a["H"], a["d"], a["dtype"], a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(Sq=0), INVALID), (dict(Sk=-1), INVALID), (dict(ro=-1), INVALID), (dict(co=-1), INVALID),
+    (dict(ld=191), INVALID),                      # ld < col_off + Sk
+    (dict(ld=(1 << 25) + 16), UNSUPPORTED),
+    (dict(q=None), INVALID), (dict(o=None), INVALID), (dict(lse=None), INVALID),
+    (dict(do=None), INVALID), (dict(table=None), INVALID), (dict(dq=None), INVALID),
+    (dict(dt=None), INVALID), (dict(k=None), INVALID), (dict(v=None), INVALID),
+    (dict(spd=None), INVALID), (dict(dk=None), INVALID), (dict(dv=None), INVALID),
+    (dict(nb=0), INVALID), (dict(nb=257), INVALID), (dict(scale=float("inf")), INVALID),
+    (dict(d=16), UNSUPPORTED), (dict(dtype=3), UNSUPPORTED),
+    (dict(q=MIS), INVALID), (dict(do=MIS), INVALID), (dict(dq=MIS), INVALID), (dict(dk=MIS), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(wsb=0), WORKSPACE), (dict(ws=FAKE + 16), WORKSPACE),
+])
+def test_bwd_ring_step_validation(kw, code):
+    assert _bwd_ring(**kw) == code
+
+
+def test_bwd_ring_step_empty_block_touches_nothing():
+    """Sk = 0 is valid and launches nothing: the key-side pointers may be NULL
+    (the call returns before any HIP call, so it runs without a device)."""
+    assert _bwd_ring(Sk=0, k=None, v=None, spd=None, dk=None, dv=None) == OK
+
+
+def test_bwd_ring_workspace_size():
+    L = gt.lib()
+    # two fp32 [H, Sq] arrays and fp32 [H, ceil(max(Sq, Sk)/256), 4], each padded to 256 bytes
+    assert L.gt_attn_bwd_ring_workspace_size(8, 16384, 16384, 64, BF16) == \
+        2 * 8 * 16384 * 4 + 8 * 64 * 4 * 4
+    assert L.gt_attn_bwd_ring_workspace_size(2, 100, 1000, 64, BF16) == 2 * 1024 + 256
+    assert L.gt_attn_bwd_ring_workspace_size(2, 1000, 0, 32, F32) == 2 * 8192 + 256
+    assert L.gt_attn_bwd_ring_workspace_size(1, 0, 5, 32, F32) == 0
+    assert L.gt_attn_bwd_ring_workspace_size(1, 4, -1, 32, F32) == 0
 
 
 @pytest.mark.parametrize("kw,code", [
