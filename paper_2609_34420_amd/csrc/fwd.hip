@@ -4,14 +4,32 @@
 // for a ring step), softmax statistics updated block by block with the bias
 // already inside the scores (Section III-A-1 part 3).
 //
-// bf16 path (gfx950 matrix cores). Each wave owns 32*QB queries and computes
-// the TRANSPOSED score tile S^T = K Q^T, so every lane owns one query
-// (lane & 31) and 16 consecutive keys per 32-key block: row max and row sum
-// are lane-local plus one exchange between the two lane halves, and the
-// lane's 16 spd bytes are one 16-byte load. P^T then feeds O^T += V^T P^T
-// straight from registers. K and V tiles are staged row-major in LDS and
-// shared by the 4 waves (V^T is read with transposing LDS reads); the
-// per-head table (times log2 e) lives in LDS.
+// bf16 path (gfx950 matrix cores). Each wave owns 64 queries (two 32-query
+// blocks) and computes the TRANSPOSED score tiles S^T = K Q^T, so every lane
+// owns one query (lane & 31) and 16 consecutive keys per 32-key block: the
+// row sum is lane-local plus one exchange between the lane halves at the
+// end, and the lane's 16 spd bytes are one 16-byte load. P^T then feeds
+// O^T += V^T P^T straight from registers. K and V tiles are staged row-major
+// in LDS and shared by the 8 waves; each operand read serves both query
+// blocks of a wave (V^T through transposing LDS reads).
+//
+// The bias enters as the starting value of the score accumulator: the table
+// is kept in LDS as bias / scale, so the matrix cores produce
+// bias / scale + q.k and one FMA per element gives the base-2 exponent
+// (q.k scale + bias) log2(e) - m. The table has one copy per lane (entry
+// (b, lane) at byte 256 b + 4 lane): a single byte permute turns a spd byte
+// into the lane's entry address, every byte value 0..255 has an entry (0 past
+// n_buckets), and the reads are free of bank conflicts.
+//
+// Softmax reference: the reference max m of a row only moves when needed.
+// The bf16 row sum of each 16-key half block is computed anyway (it is the
+// sum of exactly the P that P V uses); while it stays at or below 256 every
+// p of the block is at most 256 and the block is accepted as is. Otherwise
+// (or while a row has no finite score yet) the wave takes the exact path:
+// the block max moves the reference, the accumulator and sum are rescaled
+// and the block is recomputed. Accepted blocks therefore never hold p > 256,
+// and the reference is always a score the row attained, so the final sum is
+// at least 1 and nothing that matters underflows.
 #include <type_traits>
 
 #include "common.hpp"
@@ -22,21 +40,18 @@ namespace gt {
 
 namespace {
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
-constexpr int kBC = 64;          // keys per LDS tile
-constexpr float kRescaleSlack = 8.0f;   // log2 units the running max may lag
+constexpr int kBC = 64;            // keys per LDS tile
+constexpr int kQB = 2;             // 32-query blocks per wave
+constexpr int kKB = kBC / 32;      // 32-key blocks per tile
+constexpr float kBlockSumLimit = 256.0f;
 
-// Running softmax state of one 32-query block. Scores are kept relative to
-// a reference max: the S^T accumulator starts at -msafe / (scale log2 e), so
-// x = s * scale log2 e + bias is already x_abs - msafe and p = 2^x. The
-// reference only moves (with a rescale of the accumulator) when a score
-// passes it by more than the slack, which needs the one exchange between
-// the lane halves; otherwise no cross-lane step is needed.
+// Softmax state of one 32-query block (per lane: one query, one lane half).
 struct SoftmaxState {
   float m;        // reference max (log2 units), -inf before any finite score
+  float mneg;     // -m, or 0 while m = -inf
   float l;        // this lane half's partial row sum, relative to m
-  f32x16 init;    // -msafe / (scale log2 e), msafe = m or 0 while m = -inf
 };
 
 // Per-lane LDS element offsets of the operand reads (tile-relative; the
@@ -55,124 +70,159 @@ struct FwdOffsets {
   }
 };
 
-// Both 32-key blocks' score products are issued before the first block's
-// softmax, so the matrix cores work on block 1 while the vector ALUs work on
-// block 0. A reference move in block 0 shifts the already computed block-1
-// scores by the same amount.
-template <int D, int QB, bool MASK>
-__device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV, const float* sT,
-                                         const FwdOffsets<D>& off,
-                                         const bf16x8 (&qf)[QB][D / 16],
-                                         const uint32_t (&w)[QB][kBC / 32][4], int64_t j0,
-                                         int64_t Sk, float sl2, float inv_sl2,
-                                         SoftmaxState (&st)[QB], f32x16 (&acc)[QB][D / 32]) {
-  constexpr int KB = kBC / 32;
-  constexpr int NKC = D / 16;
+// Bias entries of this lane's 16 keys (4 spd words) loaded into the score
+// accumulator: entry address 256 b + 4 lane from one byte permute.
+__device__ __forceinline__ void load_bias(const float* tab, const uint32_t (&w)[4], uint32_t lane4,
+                                          f32x16& s) {
+  const uint8_t* tb = reinterpret_cast<const uint8_t*>(tab);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const uint32_t addr = __builtin_amdgcn_perm(w[r >> 2], lane4, 0x0c0c0000u | ((4u + (r & 3)) << 8));
+    s[r] = *reinterpret_cast<const float*>(tb + addr);
+  }
+}
+
+// p = 2^x for the lane's 16 keys, as two bf16x8 operands, and their sum.
+__device__ __forceinline__ float exp_block(const float (&x)[16], bf16x8& p0, bf16x8& p1) {
+  float p[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) p[r] = exp2_fast(x[r]);
+  p0 = cvt_bf16x8(p);
+  p1 = cvt_bf16x8(p + 8);
+  return sum_bf16x8(p1, sum_bf16x8(p0, 0.0f));
+}
+
+// Softmax of one 32x32 score block s (accumulated as bias/scale + q.k) and
+// its P^T V product into acc. The exact path runs only when some lane's
+// block sum exceeds the limit (or is not finite) or a row has no reference.
+template <int D, bool MASK>
+__device__ __forceinline__ void softmax_pv(const f32x16& s, const bf16x8 (&vop)[2][D / 32],
+                                           int64_t jrem, float sl2, SoftmaxState& st,
+                                           f32x16 (&acc)[D / 32]) {
   constexpr int NCB = D / 32;
-  const int lane = threadIdx.x & 63;
-  const int g = lane >> 5;
+  const int g = (threadIdx.x >> 5) & 1;
+  float x[16];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    f32x16 s[KB];
-    float tb[KB][16];
+  for (int r = 0; r < 16; ++r) {
+    const float xv = fmaf(s[r], sl2, st.mneg);
+    if constexpr (MASK)
+      x[r] = (16 * g + r < jrem) ? xv : -INFINITY;
+    else
+      x[r] = xv;
+  }
+  bf16x8 p0, p1;
+  float bs = exp_block(x, p0, p1);
+  if (__any(!(bs <= kBlockSumLimit) || st.m == -INFINITY)) {
+    // Exact path: move the reference to the row max of this block. x holds
+    // scores relative to the old reference (absolute while there is none).
+    float mx = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, x[r]);
+    mx -= st.mneg;
+    const float mall = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(st.m, mall);
+    const float alpha = (mnew == -INFINITY) ? 1.0f : exp2_fast(st.m - mnew);
+    st.l *= alpha;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) tb[kb][r] = sT[(w[qb][kb][r >> 2] >> (8 * (r & 3))) & 0xffu];
-      s[kb] = st[qb].init;
+    for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-      for (int kc = 0; kc < NKC; ++kc)
-        s[kb] = mfma32(lds_b128(sK + kb * 32 * D + off.k[kc]), qf[qb][kc], s[kb]);
-    }
+      for (int r = 0; r < 16; ++r) acc[cb][r] *= alpha;
+    const float mneg_new = (mnew == -INFINITY) ? 0.0f : -mnew;
+    const float shift = mneg_new - st.mneg;
+    st.m = mnew;
+    st.mneg = mneg_new;
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      float x[16];
+    for (int r = 0; r < 16; ++r) x[r] += shift;
+    bs = exp_block(x, p0, p1);
+  }
+  st.l += bs;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float xv = fmaf(s[kb][r], sl2, tb[kb][r]);
-        if constexpr (MASK)
-          x[r] = (j0 + kb * 32 + 16 * g + r < Sk) ? xv : -INFINITY;
-        else
-          x[r] = xv;
-      }
-      float mx = x[0];
+  for (int cb = 0; cb < NCB; ++cb) {
+    acc[cb] = mfma32(vop[0][cb], p0, acc[cb]);
+    acc[cb] = mfma32(vop[1][cb], p1, acc[cb]);
+  }
+}
+
+// Score product of one 32x32 unit: bias entries into the accumulator, then
+// the K operands of key block kb (read from the staged tile) times the
+// unit's Q^T.
+template <int D>
+__device__ __forceinline__ void issue_scores(const float* tab, const uint32_t (&w)[4], uint32_t lane4,
+                                             const uint16_t* sK, const int (&koff)[D / 16], int kb,
+                                             const bf16x8 (&q)[D / 16], f32x16& s) {
+  load_bias(tab, w, lane4, s);
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[r]);
-      const float thr = (st[qb].m == -INFINITY) ? -INFINITY : kRescaleSlack;
-      if (__any(mx > thr)) {
-        // Move the reference: both halves agree on the new max.
-        const float mall = fmaxf(mx, __shfl_xor(mx, 32));
-        const float msafe_old = (st[qb].m == -INFINITY) ? 0.0f : st[qb].m;
-        const float mnew = fmaxf(st[qb].m, mall + msafe_old);
-        const float alpha = (mnew == -INFINITY) ? 1.0f : exp2_fast(st[qb].m - mnew);
-        st[qb].l *= alpha;
+  for (int kc = 0; kc < D / 16; ++kc) s = mfma32(lds_b128(sK + kb * 32 * D + koff[kc]), q[kc], s);
+}
+
+template <int D>
+__device__ __forceinline__ void read_v(const uint16_t* sV, const FwdOffsets<D>& off, int kb,
+                                       bf16x8 (&vop)[2][D / 32]) {
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb)
+  for (int q = 0; q < 2; ++q)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) acc[qb][cb][r] *= alpha;
-        const float msafe_new = (mnew == -INFINITY) ? 0.0f : mnew;
-        const float shift = msafe_new - msafe_old;
+    for (int cb = 0; cb < D / 32; ++cb)
+      vop[q][cb] = lds_tr_operand(sV + (kb * 32 + 8 * q) * D, off.v[0][cb], off.v[1][cb]);
+}
+
+// Unpipelined tile (ragged or unaligned shapes): for each 32-key block the
+// score products of both query blocks, then their softmax and P V.
+template <int D, bool MASK>
+__device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV, const float* tab,
+                                         const FwdOffsets<D>& off,
+                                         const bf16x8 (&qf)[kQB][D / 16],
+                                         const uint32_t (&w)[kQB][kKB][4], uint32_t lane4,
+                                         int64_t jrem, float sl2, SoftmaxState (&st)[kQB],
+                                         f32x16 (&acc)[kQB][D / 32]) {
+  constexpr int NCB = D / 32;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) x[r] -= shift;
-        // later blocks of this tile were started from the old reference
-        const float ds = shift * inv_sl2;
+  for (int kb = 0; kb < kKB; ++kb) {
+    f32x16 s[kQB];
 #pragma unroll
-        for (int kb2 = kb + 1; kb2 < KB; ++kb2)
+    for (int qb = 0; qb < kQB; ++qb) issue_scores<D>(tab, w[qb][kb], lane4, sK, off.k, kb, qf[qb], s[qb]);
+    bf16x8 vop[2][NCB];
+    read_v<D>(sV, off, kb, vop);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) s[kb2][r] -= ds;
-        st[qb].m = mnew;
-        const float iv = -msafe_new * inv_sl2;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) st[qb].init[r] = iv;
-      }
-      float ls = st[qb].l;
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        float p[8];
-#pragma unroll
-        for (int r = 0; r < 8; ++r) p[r] = exp2_fast(x[8 * q + r]);
-        const bf16x8 pb = cvt_bf16x8(p);
-        ls = sum_bf16x8(pb, ls);       // the row sum of exactly the P that P V uses
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-          const uint16_t* vt = sV + (kb * 32 + 8 * q) * D;
-          acc[qb][cb] = mfma32(lds_tr_operand(vt, off.v[0][cb], off.v[1][cb]), pb, acc[qb][cb]);
-        }
-      }
-      st[qb].l = ls;
-    }
+    for (int qb = 0; qb < kQB; ++qb)
+      softmax_pv<D, MASK>(s[qb], vop, jrem - kb * 32, sl2, st[qb], acc[qb]);
   }
 }
 
 // VEC: spd rows are 16-byte aligned. FULL: VEC and Sk a multiple of the key
 // tile, so every spd group is loaded whole and no tile needs masking.
-template <int D, int QB, bool OUT_F32, bool VEC, bool FULL>
-__global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
-  constexpr int KB = kBC / 32;
+template <int D, bool OUT_F32, bool VEC, bool FULL>
+__global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
-  constexpr int BR = kWaves * 32 * QB;
+  constexpr int BR = kWaves * 32 * kQB;
   using Dma = TileDma<D, kWaves>;     // K and V
   static_assert(kBC == kTileRows, "key tile is one staged tile");
 
   // Three-stage ring of K / V tiles, one array per stage so that no read of
-  // one stage can be taken to alias the copy into another.
+  // one stage can be taken to alias the copy into another; the bias table,
+  // one copy per lane: entry (b, lane) at float index 64 b + lane.
   __shared__ __attribute__((aligned(16))) uint16_t sK0[kBC * D], sK1[kBC * D], sK2[kBC * D];
   __shared__ __attribute__((aligned(16))) uint16_t sV0[kBC * D], sV1[kBC * D], sV2[kBC * D];
-  __shared__ float sT[256];
+  __shared__ __attribute__((aligned(16))) float sTab[256 * 64];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = wave_id();
   const int col = lane & 31, g = lane >> 5;
+  const uint32_t lane4 = (uint32_t)lane * 4u;
 
   const int64_t nqb = (a.Sq + BR - 1) / BR;
   const int64_t lid = xcd_remap(blockIdx.x, nqb * a.H);
   const int h = (int)(lid % a.H);
   const int64_t qblk = lid / a.H;
-  const int64_t qbase = qblk * BR + (int64_t)wave * 32 * QB;
+  const int64_t qbase = qblk * BR + (int64_t)wave * 32 * kQB;
 
-  for (int t = tid; t < 256; t += kThreads)
-    sT[t] = (t < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + t] * kLog2e : 0.0f;
+  {
+    const float inv_scale = 1.0f / a.scale;
+    for (int t = tid; t < 256 * 64; t += kThreads) {
+      const int b = t >> 6;
+      sTab[t] = (b < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + b] * inv_scale : 0.0f;
+    }
+  }
 
   const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)h * a.Sq * D;
   const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + (int64_t)h * a.Sk * D;
@@ -181,10 +231,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
 
   // Q^T operands; rows past Sq load the clamped row Sq-1 (their output is
   // not stored).
-  bf16x8 qf[QB][NKC];
-  int64_t qrow[QB];
+  bf16x8 qf[kQB][NKC];
+  int64_t qrow[kQB];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
+  for (int qb = 0; qb < kQB; ++qb) {
     const int64_t i = qbase + qb * 32 + col;
     qrow[qb] = i < a.Sq ? i : a.Sq - 1;
 #pragma unroll
@@ -198,33 +248,32 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
   const int64_t ld = a.ld_spd;
   const int64_t rb = qbase < a.Sq ? qbase : a.Sq - 1;
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.spd + (a.row_off + rb) * ld + a.col_off);
-  uint32_t voff[QB];
+  uint32_t voff[kQB];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) voff[qb] = (uint32_t)((qrow[qb] - rb) * ld) + 16u * g;
-  auto fetch_spd = [&](int64_t jt, uint32_t (&w)[QB][KB][4]) {
+  for (int qb = 0; qb < kQB; ++qb) voff[qb] = (uint32_t)((qrow[qb] - rb) * ld) + 16u * g;
+  auto fetch_spd = [&](int64_t jt, uint32_t (&w)[kQB][kKB][4]) {
     if (FULL || (VEC && jt + kBC <= a.Sk)) {
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
+      for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) buf_u128(rs, voff[qb], (uint32_t)(jt + kb * 32), w[qb][kb]);
+        for (int kb = 0; kb < kKB; ++kb) buf_u128(rs, voff[qb], (uint32_t)(jt + kb * 32), w[qb][kb]);
     } else {
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
+      for (int qb = 0; qb < kQB; ++qb) {
         const uint8_t* row = a.spd + (a.row_off + qrow[qb]) * ld + a.col_off;
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) load_spd16_bytes(row, jt + kb * 32 + 16 * g, a.Sk, w[qb][kb]);
+        for (int kb = 0; kb < kKB; ++kb) load_spd16_bytes(row, jt + kb * 32 + 16 * g, a.Sk, w[qb][kb]);
       }
     }
   };
 
-  const float inv_sl2 = 1.0f / sl2;
-  SoftmaxState sm[QB];
-  f32x16 acc[QB][NCB];
+  SoftmaxState sm[kQB];
+  f32x16 acc[kQB][NCB];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
+  for (int qb = 0; qb < kQB; ++qb) {
     sm[qb].m = -INFINITY;
+    sm[qb].mneg = 0.0f;
     sm[qb].l = 0.0f;
-    sm[qb].init = zero_f32x16();
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) acc[qb][cb] = zero_f32x16();
   }
@@ -232,69 +281,138 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(FwdArgs a) {
   const int64_t ntiles = (a.Sk + kBC - 1) / kBC;
   const FwdOffsets<D> off;
   const Dma dma(wave);
-  uint32_t w0[QB][KB][4], w1[QB][KB][4], w2[QB][KB][4];   // spd words, by tile % 3
-
-  // Copy tile t (clamped to the last tile) into stage s and fetch its spd
-  // words: Dma::NLOADS + SPD_LOADS vector-memory ops per wave.
-  constexpr int SPD_LOADS = QB * KB;
-#define GT_FWD_ISSUE(t_, S_)                                                                    \
-  {                                                                                            \
-    const int64_t j_ = ((t_) < ntiles ? (t_) : ntiles - 1) * kBC;                              \
-    dma.load(tile_rsrc<D>(kh, j_, a.Sk), tile_rsrc<D>(vh, j_, a.Sk),                          \
-             (S_) == 0 ? sK0 : ((S_) == 1 ? sK1 : sK2), (S_) == 0 ? sV0 : ((S_) == 1 ? sV1 : sV2)); \
-    fetch_spd(j_, (S_) == 0 ? w0 : ((S_) == 1 ? w1 : w2));                                    \
-  }
+  constexpr int SPD_LOADS = kQB * kKB;
+#define GT_FWD_STAGE(S_, K_, V_)                                                                \
+  uint16_t* K_ = (S_) == 0 ? sK0 : ((S_) == 1 ? sK1 : sK2);                                   \
+  uint16_t* V_ = (S_) == 0 ? sV0 : ((S_) == 1 ? sV1 : sV2);
+  // K/V tiles: a three-stage LDS ring, tile t in stage t % 3, copied two
+  // tiles ahead (Dma::NLOADS vector-memory ops per wave); tiles past the
+  // end are clamped to the last one.
+  auto copy_tile = [&](int64_t tt, auto stagec) {
+    constexpr int S = decltype(stagec)::value;
+    GT_FWD_STAGE(S, k_s, v_s)
+    const int64_t j_ = (tt < ntiles ? tt : ntiles - 1) * kBC;
+    dma.load(tile_rsrc<D>(kh, j_, a.Sk), tile_rsrc<D>(vh, j_, a.Sk), k_s, v_s);
+  };
+  auto spd_of = [&](int64_t tt, uint32_t (&w)[kQB][kKB][4]) {
+    fetch_spd((tt < ntiles ? tt : ntiles - 1) * kBC, w);
+  };
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
   using S2 = std::integral_constant<int, 2>;
-  if (ntiles > 0) {
-    GT_FWD_ISSUE(0, 0)
-    GT_FWD_ISSUE(1, 1)
-  }
-  __syncthreads();     // table, and the copy of tile 0 (waits for every load)
 
-  // Tile t from stage S = t % 3: copy tile t + 2 into stage (S + 2) % 3
-  // (last read in step t - 1, before that step's barrier), compute, then
-  // wait until this wave's copy of tile t + 1 has landed (only the spd
-  // words of tile t + 1 and this step's loads may still be in flight) and
-  // meet the other waves at the barrier.
-  auto step = [&](int64_t t, auto stagec, auto maskc) {
-    constexpr int S = decltype(stagec)::value;
-    constexpr bool MASK = decltype(maskc)::value;
-    GT_FWD_ISSUE(t + 2, (S + 2) % 3)
-    sched_fence();
-    auto& w = S == 0 ? w0 : (S == 1 ? w1 : w2);
-    const uint16_t* k_s = S == 0 ? sK0 : (S == 1 ? sK1 : sK2);
-    const uint16_t* v_s = S == 0 ? sV0 : (S == 1 ? sV1 : sV2);
-    fwd_tile<D, QB, MASK>(k_s, v_s, sT, off, qf, w, t * kBC, a.Sk, sl2, inv_sl2, sm, acc);
-    if constexpr (FULL)
-      wait_vmcnt<2 * SPD_LOADS + Dma::NLOADS>();
-    else
-      wait_vmcnt<0>();     // the unaligned spd path issues a variable number of loads
-    __builtin_amdgcn_s_barrier();
-  };
-  using Full = std::false_type;     // every key of the tile exists
-  using Part = std::true_type;      // keys past Sk masked
-  const int64_t nfull = FULL ? ntiles : a.Sk / kBC;
-  int64_t t = 0;
-  for (; t + 3 <= nfull; t += 3) {
-    step(t, S0(), Full());
-    step(t + 1, S1(), Full());
-    step(t + 2, S2(), Full());
-  }
-  // At most two full tiles and the partial one remain, in stages 0, 1, 2.
   if constexpr (FULL) {
-    if (t < ntiles) step(t, S0(), Full());
-    if (t + 1 < ntiles) step(t + 1, S1(), Full());
+    // spd words: two register sets, tile t in set t % 2, fetched one tile
+    // ahead (SPD_LOADS vector-memory ops per wave).
+    uint32_t wA[kQB][kKB][4], wB[kQB][kKB][4];
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    f32x16 s0;        // score accumulator of the current tile's first unit
+    if (ntiles > 0) {
+      copy_tile(0, S0());
+      copy_tile(1, S1());
+      copy_tile(2, S2());
+      spd_of(0, wA);
+      spd_of(1, wB);
+      wait_vmcnt<0>();
+      __syncthreads();     // table, and tiles 0..2
+      issue_scores<D>(sTab, wA[0][0], lane4, sK0, off.k, 0, qf[0], s0);
+    }
+    // Tile t from stage S = t % 3 and spd set P = t % 2; units u = (key
+    // block, query block) in the order (0,0), (0,1), (1,0), (1,1). The score
+    // product of unit u + 1 is issued before the softmax of unit u, so the
+    // matrix cores work while the vector ALUs do the softmax. Before the
+    // softmax of the last unit the wave has issued every LDS read of stage S:
+    // it waits for tile t + 1 (copied two steps ago, spd fetched one step
+    // ago), meets the other waves at the barrier, refills stage S with tile
+    // t + 3 and issues the first score product of tile t + 1.
+    auto step = [&](int64_t t, auto stagec, auto setc) {
+      constexpr int S = decltype(stagec)::value;
+      constexpr int SN = (S + 1) % 3;
+      constexpr int P = decltype(setc)::value;
+      GT_FWD_STAGE(S, k_s, v_s)
+      GT_FWD_STAGE(SN, k_n, v_n)
+      auto& w = P == 0 ? wA : wB;
+      auto& w_n = P == 0 ? wB : wA;
+      bf16x8 vop[2][NCB];
+      f32x16 s1, s2, s3;
+      issue_scores<D>(sTab, w[1][0], lane4, k_s, off.k, 0, qf[1], s1);
+      read_v<D>(v_s, off, 0, vop);
+      softmax_pv<D, false>(s0, vop, kBC, sl2, sm[0], acc[0]);
+      issue_scores<D>(sTab, w[0][1], lane4, k_s, off.k, 1, qf[0], s2);
+      softmax_pv<D, false>(s1, vop, kBC, sl2, sm[1], acc[1]);
+      issue_scores<D>(sTab, w[1][1], lane4, k_s, off.k, 1, qf[1], s3);
+      read_v<D>(v_s, off, 1, vop);
+      spd_of(t + 2, w);      // set P is free: tile t + 2's words
+      sched_fence();
+      softmax_pv<D, false>(s2, vop, kBC, sl2, sm[0], acc[0]);
+      // Tile boundary: tile t + 1 must have landed; only tile t + 2's copy
+      // (issued one step ago) and spd words (just issued) may be in flight.
+      wait_vmcnt<SPD_LOADS + Dma::NLOADS>();
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS reads of stage S done
+      __builtin_amdgcn_s_barrier();
+      copy_tile(t + 3, stagec);
+      sched_fence();
+      issue_scores<D>(sTab, w_n[0][0], lane4, k_n, off.k, 0, qf[0], s0);
+      softmax_pv<D, false>(s3, vop, kBC, sl2, sm[1], acc[1]);
+    };
+    int64_t t = 0;
+    for (; t + 6 <= ntiles; t += 6) {
+      step(t, S0(), P0());
+      step(t + 1, S1(), P1());
+      step(t + 2, S2(), P0());
+      step(t + 3, S0(), P1());
+      step(t + 4, S1(), P0());
+      step(t + 5, S2(), P1());
+    }
+    if (t < ntiles) step(t, S0(), P0());
+    if (t + 1 < ntiles) step(t + 1, S1(), P1());
+    if (t + 2 < ntiles) step(t + 2, S2(), P0());
+    if (t + 3 < ntiles) step(t + 3, S0(), P1());
+    if (t + 4 < ntiles) step(t + 4, S1(), P0());
   } else {
+    // Ragged or unaligned: spd words fetched two tiles ahead in three sets,
+    // one tile computed per step, every wait drains the loads.
+    uint32_t w0[kQB][kKB][4], w1[kQB][kKB][4], w2[kQB][kKB][4];
+    if (ntiles > 0) {
+      copy_tile(0, S0());
+      spd_of(0, w0);
+      copy_tile(1, S1());
+      spd_of(1, w1);
+    }
+    wait_vmcnt<0>();
+    __syncthreads();     // table, and the copy of tile 0
+    auto step = [&](int64_t t, auto stagec, auto maskc) {
+      constexpr int S = decltype(stagec)::value;
+      constexpr bool MASK = decltype(maskc)::value;
+      GT_FWD_STAGE(S, k_s, v_s)
+      copy_tile(t + 2, std::integral_constant<int, (S + 2) % 3>());
+      spd_of(t + 2, S == 0 ? w2 : (S == 1 ? w0 : w1));
+      sched_fence();
+      auto& w = S == 0 ? w0 : (S == 1 ? w1 : w2);
+      fwd_tile<D, MASK>(k_s, v_s, sTab, off, qf, w, lane4, a.Sk - t * kBC, sl2, sm, acc);
+      wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+    };
+    using Full = std::false_type;
+    using Part = std::true_type;
+    const int64_t nfull = a.Sk / kBC;
+    int64_t t = 0;
+    for (; t + 3 <= nfull; t += 3) {
+      step(t, S0(), Full());
+      step(t + 1, S1(), Full());
+      step(t + 2, S2(), Full());
+    }
     if (t < ntiles) step(t, S0(), Part());
     if (t + 1 < ntiles) step(t + 1, S1(), Part());
     if (t + 2 < ntiles) step(t + 2, S2(), Part());
   }
+  wait_vmcnt<0>();     // drain the clamped copies issued past the last tile
+#undef GT_FWD_STAGE
 
   // Epilogue: O = O_acc / l, LSE = (m + log2 l) ln 2.
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
+  for (int qb = 0; qb < kQB; ++qb) {
     const float lt = sm[qb].l + __shfl_xor(sm[qb].l, 32);
     const int64_t i = qbase + qb * 32 + col;
     if (i >= a.Sq) continue;
@@ -387,17 +505,17 @@ __global__ __launch_bounds__(128) void fwd_f32_kernel(FwdArgs a) {
   a.lse[(int64_t)h * a.Sq + i] = l > 0.0f ? m + logf(l) : -INFINITY;
 }
 
-template <int D, int QB, bool OUT_F32>
+template <int D, bool OUT_F32>
 hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t s) {
-  constexpr int BR = kWaves * 32 * QB;
+  constexpr int BR = kWaves * 32 * kQB;
   const int64_t nqb = (a.Sq + BR - 1) / BR;
   const dim3 grid((unsigned)(nqb * a.H));
   if (a.spd_vec && a.Sk % kBC == 0)
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, QB, OUT_F32, true, true>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, true>), grid, dim3(kThreads), 0, s, a);
   else if (a.spd_vec)
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, QB, OUT_F32, true, false>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, false>), grid, dim3(kThreads), 0, s, a);
   else
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, QB, OUT_F32, false, false>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, false, false>), grid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -412,8 +530,8 @@ hipError_t launch_fwd_f32(const FwdArgs& a, hipStream_t s) {
 
 hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStream_t s) {
   if (bf16) {
-    if (d == 64) return out_f32 ? launch_fwd_bf16<64, 1, true>(a, s) : launch_fwd_bf16<64, 1, false>(a, s);
-    return out_f32 ? launch_fwd_bf16<32, 2, true>(a, s) : launch_fwd_bf16<32, 2, false>(a, s);
+    if (d == 64) return out_f32 ? launch_fwd_bf16<64, true>(a, s) : launch_fwd_bf16<64, false>(a, s);
+    return out_f32 ? launch_fwd_bf16<32, true>(a, s) : launch_fwd_bf16<32, false>(a, s);
   }
   return d == 64 ? launch_fwd_f32<64>(a, s) : launch_fwd_f32<32>(a, s);
 }
