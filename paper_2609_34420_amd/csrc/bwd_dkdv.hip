@@ -45,24 +45,32 @@ constexpr int kBK = kNW * 32;       // keys per workgroup
 constexpr int kBQ = 64;             // queries per staged tile
 constexpr int kThreads = kNW * 64;
 // Table / histogram copies: lane & (CPY - 1); 32 copies (two lanes per copy)
-// for up to 128 buckets, else 16.
+// in the 128-bucket layout, else 16.
 template <int NB>
 constexpr int copies() { return NB <= 128 ? 32 : 16; }
 
-// All LDS of the kernel in one block, table and histogram first so that
-// their offsets stay small: the one per-element address register serves
-// both with immediate offsets. NB (64, 128 or 256) bounds n_buckets; at 64
-// the tiles also stay below 64 KiB, inside the reach of the DS immediate.
-template <int D, int NB>
-struct DkdvSmem {
-  static constexpr int ENT = NB * copies<NB>();   // entry (b, c) = b * CPY + c
-  uint2 tabw[ENT];                  // table copies (fp32 bits, 8-byte stride)
-  unsigned long long hist[ENT];     // gradient histogram copies, same index
+// All LDS of the kernel in one block, at LDS address 0: the staged tiles
+// first (their offsets stay inside the reach of the DS immediate), then,
+// from byte 64 KiB, the table copies and right after them the histogram
+// copies. The per-element address register holds the absolute address of
+// the table entry (bucket, copy); the histogram entry is at a fixed
+// immediate offset (ENT * 8) from it. NB (128 or 256) bounds the byte
+// values the layout covers.
+template <int D>
+struct DkdvTiles {
   uint16_t q[2][kBQ * D];
   uint16_t o[2][kBQ * D];
   float init_s[2][kBQ];             // -LSE log2 e / (scale log2 e); -inf for empty rows
   float init_p[2][kBQ];             // -Dlt 2^F
   float red[3][kNW];
+};
+constexpr uint32_t kTabBase = 65536;
+template <int D, int NB>
+struct DkdvSmem : DkdvTiles<D> {
+  static constexpr int ENT = NB * copies<NB>();   // entry (b, c) = b * CPY + c
+  uint8_t pad[kTabBase - sizeof(DkdvTiles<D>)];
+  uint2 tabw[ENT];                  // table copies (fp32 bits, 8-byte stride)
+  unsigned long long hist[ENT];     // gradient histogram copies, same index
 };
 
 // Per-lane LDS element offsets of the operand reads (tile-relative; the
@@ -153,6 +161,38 @@ __device__ __forceinline__ int round_to_int(float x) {
   return r;
 }
 
+// The 128-bucket layout is used only when n_buckets <= 127, so bucket 127
+// is padding (bias 0, gradient discarded) and any byte of 128 or more, which
+// has no entry in that layout, can be mapped to it. Valid inputs (buckets
+// below n_buckets) never take the mapping branch.
+template <int NB>
+__device__ __forceinline__ void clamp_buckets(uint32_t (&w)[4]) {
+  if constexpr (NB <= 128) {
+    if (__any(((w[0] | w[1] | w[2] | w[3]) & 0x80808080u) != 0)) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        uint32_t x = w[u];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if ((x >> (8 * k + 7)) & 1u) x = (x & ~(0xffu << (8 * k))) | (0x7fu << (8 * k));
+        w[u] = x;
+      }
+    }
+  }
+}
+template <int NB>
+__device__ __forceinline__ void clamp_buckets(uint8_t (&b)[16]) {
+  if constexpr (NB <= 128) {
+    uint32_t any = 0;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) any |= b[r];
+    if (__any((any & 0x80u) != 0)) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) b[r] = (b[r] & 0x80u) ? (uint8_t)0x7f : b[r];
+    }
+  }
+}
+
 // b: this lane's 16 bucket indices, as 16 bytes (gathered from spd columns)
 // or as 4 words (a 16-byte row segment of spd_t).
 template <int D, int NB, bool KTAIL, int BUF, int QS, typename BT>
@@ -185,10 +225,12 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOff
   // Lane: key; registers r: queries. dp holds (dO.V - Dlt) 2^F, so ds below
   // is dS 2^F.
   float p[16], ds[16];
-  uint32_t addr[16];   // byte offset of entry (bucket, copy) in tabw and in hist
+  uint32_t addr[16];   // absolute LDS address of table entry (bucket, copy)
   float tb[16];
   constexpr int CPY = copies<NB>();
-  const uint32_t cpy8 = (uint32_t)(lane & (CPY - 1)) * 8u;
+  // copy offset with the table base: kTabBase = 1 << 16 is byte 2, so a
+  // byte permute can put the bucket into byte 1 and keep both
+  const uint32_t cpyb = (uint32_t)(lane & (CPY - 1)) * 8u | kTabBase;
   if constexpr (sizeof(BT) == 4) {
     uint32_t w[4];
 #pragma unroll
@@ -196,27 +238,37 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOff
       w[u] = b[u];
       opaque(w[u]);                                // keep the load's wait here
     }
+    clamp_buckets<NB>(w);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      if constexpr (CPY == 32)   // byte (r & 3) of w[r >> 2] times 256, plus cpy8
-        addr[r] = __builtin_amdgcn_perm(w[r >> 2], cpy8, 0x0c0c0000u | ((4u + (r & 3)) << 8));
+      if constexpr (CPY == 32)   // byte (r & 3) of w[r >> 2] times 256, plus copy and base
+        addr[r] = __builtin_amdgcn_perm(w[r >> 2], cpyb, 0x0c020000u | ((4u + (r & 3)) << 8));
       else
-        addr[r] = (((w[r >> 2] >> (8 * (r & 3))) & 0xffu) << 7) | cpy8;
+        addr[r] = (((w[r >> 2] >> (8 * (r & 3))) & 0xffu) << 7) | cpyb;
     }
   } else {
+    uint8_t bb[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       uint32_t bk = b[r];
       opaque(bk);                                  // keep the byte's wait here
+      bb[r] = (uint8_t)bk;
+    }
+    clamp_buckets<NB>(bb);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const uint32_t bk = bb[r];
       if constexpr (CPY == 32)
-        addr[r] = __builtin_amdgcn_perm(bk, cpy8, 0x0c0c0400u);   // byte0(bk) * 256 + cpy8
+        addr[r] = __builtin_amdgcn_perm(bk, cpyb, 0x0c020400u);   // byte0(bk) * 256 + copy + base
       else
-        addr[r] = (bk << 7) | cpy8;
+        addr[r] = (bk << 7) | cpyb;
     }
   }
+  const uint8_t* lds0 = reinterpret_cast<const uint8_t*>(&sm);
 #pragma unroll
-  for (int r = 0; r < 16; ++r)
-    tb[r] = *reinterpret_cast<const float*>(reinterpret_cast<const uint8_t*>(sm.tabw) + addr[r]);
+  for (int r = 0; r < 16; ++r) {
+    tb[r] = *reinterpret_cast<const float*>(lds0 + addr[r]);
+  }
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const float x = fmaf(s[r], sl2, tb[r]);
@@ -225,10 +277,13 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOff
     p[r] = pv;
     ds[r] = pv * dp[r];
   }
+  constexpr uint32_t kHistOff = DkdvSmem<D, NB>::ENT * 8;
 #pragma unroll
-  for (int r = 0; r < 16; ++r)
-    atomicAdd(reinterpret_cast<unsigned long long*>(reinterpret_cast<uint8_t*>(sm.hist) + addr[r]),
-              (unsigned long long)(long long)round_to_int(ds[r]));
+  for (int r = 0; r < 16; ++r) {
+    unsigned long long* hp = reinterpret_cast<unsigned long long*>(const_cast<uint8_t*>(lds0) + addr[r] + kHistOff);
+    const unsigned long long v = (unsigned long long)(long long)round_to_int(ds[r]);
+    atomicAdd(hp, v);
+  }
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const bf16x8 pb = cvt_bf16x8(p + 8 * q);
@@ -473,12 +528,21 @@ hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s) {
         hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D_, NB_, false, false>), grid, dim3(kThreads), 0, s, a);\
     }                                                                                               \
   }
-  // Every spd byte value must index the table (values at or past n_buckets
-  // read bias 0 and their gradient is dropped), so the full 256-bucket table.
-  if (d == 64)
-    GT_DKDV_LAUNCH(64, 256)
-  else
-    GT_DKDV_LAUNCH(32, 256)
+  // Byte values at or past n_buckets read bias 0 and their gradient is
+  // dropped. Up to 127 buckets the 128-bucket layout (one byte permute per
+  // address) is used, with larger bytes mapped to its padding bucket 127;
+  // otherwise the full 256-bucket layout.
+  if (a.n_buckets <= 127) {
+    if (d == 64)
+      GT_DKDV_LAUNCH(64, 128)
+    else
+      GT_DKDV_LAUNCH(32, 128)
+  } else {
+    if (d == 64)
+      GT_DKDV_LAUNCH(64, 256)
+    else
+      GT_DKDV_LAUNCH(32, 256)
+  }
 #undef GT_DKDV_LAUNCH
   return hipGetLastError();
 }
