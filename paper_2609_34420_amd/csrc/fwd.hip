@@ -70,17 +70,6 @@ struct FwdOffsets {
   }
 };
 
-// Bias entries of this lane's 16 keys (4 spd words) loaded into the score
-// accumulator: entry address 256 b + 4 lane from one byte permute.
-__device__ __forceinline__ void load_bias(const float* tab, const uint32_t (&w)[4], uint32_t lane4,
-                                          f32x16& s) {
-  const uint8_t* tb = reinterpret_cast<const uint8_t*>(tab);
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const uint32_t addr = __builtin_amdgcn_perm(w[r >> 2], lane4, 0x0c0c0000u | ((4u + (r & 3)) << 8));
-    s[r] = *reinterpret_cast<const float*>(tb + addr);
-  }
-}
 
 // p = 2^x for the lane's 16 keys, as two bf16x8 operands, and their sum.
 __device__ __forceinline__ float exp_block(const float (&x)[16], bf16x8& p0, bf16x8& p1) {
@@ -203,7 +192,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   // one copy per lane: entry (b, lane) at float index 64 b + lane.
   __shared__ __attribute__((aligned(16))) uint16_t sK0[kBC * D], sK1[kBC * D], sK2[kBC * D];
   __shared__ __attribute__((aligned(16))) uint16_t sV0[kBC * D], sV1[kBC * D], sV2[kBC * D];
-  __shared__ __attribute__((aligned(16))) float sTab[256 * 64];
+  __shared__ __attribute__((aligned(16))) float sTab[kLaneTableFloats];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = wave_id();
@@ -216,13 +205,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   const int64_t qblk = lid / a.H;
   const int64_t qbase = qblk * BR + (int64_t)wave * 32 * kQB;
 
-  {
-    const float inv_scale = 1.0f / a.scale;
-    for (int t = tid; t < 256 * 64; t += kThreads) {
-      const int b = t >> 6;
-      sTab[t] = (b < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + b] * inv_scale : 0.0f;
-    }
-  }
+  fill_lane_table(sTab, a.table + (int64_t)h * a.n_buckets, a.n_buckets, a.scale, kThreads);
 
   const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)h * a.Sq * D;
   const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + (int64_t)h * a.Sk * D;

@@ -188,4 +188,33 @@ __device__ __forceinline__ bf16x8 lds_tr_operand(const uint16_t* tile, int off0,
   return __builtin_bit_cast(bf16x8, c);
 }
 
+
+// Per-lane bias table in LDS for the query-stationary kernels: every byte
+// value 0..255 has an entry (0 at or past n_buckets), one copy per lane,
+// entry (b, lane) at byte 256 b + 4 lane, holding table[h, b] / scale. A
+// score accumulator started from these entries and advanced by the matrix
+// cores holds bias / scale + q.k.
+constexpr int kLaneTableFloats = 256 * 64;
+
+__device__ __forceinline__ void fill_lane_table(float* tab, const float* table_h, int n_buckets,
+                                                float scale, int nthreads) {
+  const float inv_scale = 1.0f / scale;
+  for (int t = (int)threadIdx.x; t < kLaneTableFloats; t += nthreads) {
+    const int b = t >> 6;
+    tab[t] = (b < n_buckets) ? table_h[b] * inv_scale : 0.0f;
+  }
+}
+
+// Bias entries of this lane's 16 keys (4 spd words) loaded into a score
+// accumulator: entry address 256 b + 4 lane from one byte permute.
+__device__ __forceinline__ void load_bias(const float* tab, const uint32_t (&w)[4], uint32_t lane4,
+                                          f32x16& s) {
+  const uint8_t* tb = reinterpret_cast<const uint8_t*>(tab);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const uint32_t addr = __builtin_amdgcn_perm(w[r >> 2], lane4, 0x0c0c0000u | ((4u + (r & 3)) << 8));
+    s[r] = *reinterpret_cast<const float*>(tb + addr);
+  }
+}
+
 }  // namespace gt

@@ -246,3 +246,23 @@ def test_spd_transpose_ignored_when_unaligned():
     got = _run_full(q, k, v, do, table, spd, "bf16", scale, spd_t=spd_t)
     ref = _oracle_full(q, k, v, do, table, spd, scale)
     check_grads("spd_t unaligned", got, ref, "bf16")
+
+
+@pytest.mark.parametrize("spd_t_kind", ["none", "transposed"])
+@pytest.mark.parametrize("nb", [32, 127, 128, 200])
+def test_every_byte_value(nb, spd_t_kind):
+    """spd bytes drawn from the whole range 0..255: bytes at or past
+    n_buckets give bias 0 and no gradient. With at most 127 buckets the
+    key-stationary stage maps bytes of 128 or more to its padding bucket;
+    past that it uses the full 256-entry layout. N = 320 spans several
+    query and key tiles with a partial last key block."""
+    H, N, d = 2, 320, 64
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=nb * 3 + len(spd_t_kind), dt="bf16", hi=256)
+    spd_t = np.ascontiguousarray(spd.T) if spd_t_kind == "transposed" else None
+    scale = 1.0 / math.sqrt(d)
+    tag = f"all bytes nb={nb} spd_t={spd_t_kind}"
+    say(tag)
+    got = _run_full(q, k, v, do, table, spd, "bf16", scale, spd_t=spd_t)
+    ref = _oracle_full(q, k, v, do, table, spd, scale)
+    check_fwd(tag, got["o"], got["lse"], ref["o"], ref["lse"], "bf16")
+    check_grads(tag, got, ref, "bf16")
