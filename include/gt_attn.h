@@ -144,6 +144,33 @@ gt_status_t gt_attn_ring_step(const void* q_shard, int64_t Sq,
                               int32_t H, int32_t d, gt_dtype_t dtype,
                               float scale, void* stream);
 
+/* One context-parallel step merged in place into a running result (the
+ * running max/sum update of Section III-A-1 part 3, applied per KV block):
+ * the step of gt_attn_ring_step, whose partial (O_p, LSE_p) is combined with
+ * the state (o_acc, lse_acc) in the same kernel,
+ *   LSE = log(exp(lse_acc) + exp(LSE_p)),
+ *   O   = exp(lse_acc - LSE) o_acc + exp(LSE_p - LSE) O_p,
+ * and written back. After the last step (o_acc, lse_acc) is the merged O
+ * (normalised, fp32) and LSE of the shard's rows over every block seen, so no
+ * per-step partial buffer and no separate merge pass are needed (cast O with
+ * gt_attn_merge, n_parts = 1, if the dtype is wanted).
+ *   o_acc    [H, Sq, d] fp32, read and written; lse_acc [H, Sq] fp32, read and
+ *            written. Start from the first step's gt_attn_ring_step output
+ *            (o_part, lse_part), or from o_acc = 0, lse_acc = -inf (no block).
+ *            Rows whose running LSE and step LSE are both -inf stay O = 0,
+ *            LSE = -inf.
+ * Other arguments, validation and errors as gt_attn_ring_step (Sk = 0 leaves
+ * the state unchanged). Steps on one state must be ordered (one stream);
+ * the result depends on the order only through fp32 rounding. */
+gt_status_t gt_attn_ring_step_acc(const void* q_shard, int64_t Sq,
+                                  const void* k_shard, const void* v_shard, int64_t Sk,
+                                  const uint8_t* spd, int64_t ld_spd,
+                                  int64_t row_off, int64_t col_off,
+                                  const float* table, int32_t n_buckets,
+                                  float* o_acc, float* lse_acc,
+                                  int32_t H, int32_t d, gt_dtype_t dtype,
+                                  float scale, void* stream);
+
 /* Combine n_parts block partials into the attention over all of their keys
  * (Section III-A-1 part 3: every partial's softmax statistics already hold
  * its bias slice, so the combination is exact):

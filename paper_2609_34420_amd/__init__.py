@@ -10,6 +10,8 @@ If the library is missing or cannot be loaded, every call raises.
     dq, dk, dv, dtable = gt_attn_bwd(q, k, v, spd, table, o, lse, d_o)
     o_p, lse_p = gt_attn_ring_step(q_sh, k_sh, v_sh, spd_shard, row_off, col_off, table)
     o, lse = gt_attn_merge(o_parts, lse_parts, dtype=torch.bfloat16)
+    state = gt_attn_ring_step(...)                      # first step: a running state
+    gt_attn_ring_step_acc(q_sh, k_sh, v_sh, spd_shard, row_off, col_off, table, state)
     dq, dk, dv, dt = gt_attn_bwd_ring_step(q_sh, o_sh, lse_sh, do_sh, k_blk, v_blk, spd_shard,
                                            row_off, col_off, table, acc=(dq, dk, dv, dt))
 """
@@ -21,7 +23,8 @@ from pathlib import Path
 
 import torch
 
-__all__ = ["gt_attn_fwd", "gt_attn_bwd", "gt_attn_bwd_phase", "gt_attn_ring_step", "gt_attn_merge",
+__all__ = ["gt_attn_fwd", "gt_attn_bwd", "gt_attn_bwd_phase", "gt_attn_ring_step",
+           "gt_attn_ring_step_acc", "gt_attn_merge",
            "gt_attn_bwd_ring_step", "gt_attn_bwd_workspace_size", "gt_attn_bwd_ring_workspace_size",
            "gt_status_string", "gt_attn_version",
            "GTError", "lib", "LIB_PATH"]
@@ -66,6 +69,8 @@ def lib() -> ctypes.CDLL:
         L.gt_attn_ring_step.restype = _I32
         L.gt_attn_ring_step.argtypes = [_P, _I64, _P, _P, _I64, _P, _I64, _I64, _I64, _P, _I32,
                                         _P, _P, _I32, _I32, _I32, _F, _P]
+        L.gt_attn_ring_step_acc.restype = _I32
+        L.gt_attn_ring_step_acc.argtypes = L.gt_attn_ring_step.argtypes
         L.gt_attn_bwd_ring_workspace_size.restype = ctypes.c_size_t
         L.gt_attn_bwd_ring_workspace_size.argtypes = [_I32, _I64, _I64, _I32, _I32]
         L.gt_attn_bwd_ring_step.restype = _I32
@@ -211,6 +216,32 @@ def gt_attn_ring_step(q_shard, k_shard, v_shard, spd, row_off: int, col_off: int
                                  scale, _stream(stream))
     _check(st, "gt_attn_ring_step")
     return out, lse
+
+
+def gt_attn_ring_step_acc(q_shard, k_shard, v_shard, spd, row_off: int, col_off: int, table,
+                          state, scale: float | None = None, stream=None):
+    """One context-parallel step merged in place into the running state
+    (o_acc fp32 [H, Sq, d], lse_acc fp32 [H, Sq]) (C ABI
+    gt_attn_ring_step_acc); returns the state. The first step's
+    gt_attn_ring_step output is a valid starting state."""
+    H, Sq, d = q_shard.shape
+    Sk = k_shard.shape[1] if k_shard is not None else 0
+    o_acc, lse_acc = state
+    _dev_contig(q_shard, k_shard, v_shard, table, o_acc, lse_acc)
+    _need(spd is None or (spd.dtype == torch.uint8 and spd.dim() == 2 and spd.stride(1) == 1),
+          "spd must be a uint8 2-D tensor with unit column stride")
+    _need(o_acc.dtype == torch.float32 and tuple(o_acc.shape) == (H, Sq, d),
+          "o_acc must be fp32 [H, Sq, d]")
+    _need(lse_acc.dtype == torch.float32 and tuple(lse_acc.shape) == (H, Sq),
+          "lse_acc must be fp32 [H, Sq]")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ld = spd.stride(0) if spd is not None else 0
+    st = lib().gt_attn_ring_step_acc(_ptr(q_shard), Sq, _ptr(k_shard), _ptr(v_shard), Sk,
+                                     _ptr(spd), ld, int(row_off), int(col_off), _ptr(table),
+                                     table.shape[1], _ptr(o_acc), _ptr(lse_acc), H, d,
+                                     _dt(q_shard), scale, _stream(stream))
+    _check(st, "gt_attn_ring_step_acc")
+    return o_acc, lse_acc
 
 
 def gt_attn_bwd_ring_workspace_size(H: int, Sq: int, Sk: int, d: int, dtype=torch.bfloat16) -> int:

@@ -48,12 +48,12 @@ const char* gt_status_string(gt_status_t s) {
 
 int32_t gt_attn_version(void) { return 100; }
 
-gt_status_t gt_attn_ring_step(const void* q_shard, int64_t Sq, const void* k_shard,
-                              const void* v_shard, int64_t Sk, const uint8_t* spd,
-                              int64_t ld_spd, int64_t row_off, int64_t col_off,
-                              const float* table, int32_t n_buckets, float* o_part,
-                              float* lse_part, int32_t H, int32_t d, gt_dtype_t dtype,
-                              float scale, void* stream) {
+static gt_status_t ring_impl(const void* q_shard, int64_t Sq, const void* k_shard,
+                             const void* v_shard, int64_t Sk, const uint8_t* spd,
+                             int64_t ld_spd, int64_t row_off, int64_t col_off,
+                             const float* table, int32_t n_buckets, float* o_part,
+                             float* lse_part, int32_t H, int32_t d, gt_dtype_t dtype,
+                             float scale, void* stream, int32_t accumulate) {
   if (!dtype_ok(dtype)) return GT_ERR_UNSUPPORTED;
   if (!dims_ok(d)) return GT_ERR_UNSUPPORTED;
   if (H < 1 || Sq < 1 || Sk < 0 || row_off < 0 || col_off < 0) return GT_ERR_INVALID;
@@ -72,7 +72,28 @@ gt_status_t gt_attn_ring_step(const void* q_shard, int64_t Sq, const void* k_sha
   a.o = o_part; a.lse = lse_part;
   a.H = H; a.Sq = Sq; a.Sk = Sk; a.scale = scale;
   a.spd_vec = Sk > 0 ? spd_vec(spd, ld_spd, row_off, col_off) : 0;
+  a.accumulate = accumulate;
   return launched(gt::launch_fwd(a, d, dtype == GT_BF16, true, static_cast<hipStream_t>(stream)));
+}
+
+gt_status_t gt_attn_ring_step(const void* q_shard, int64_t Sq, const void* k_shard,
+                              const void* v_shard, int64_t Sk, const uint8_t* spd,
+                              int64_t ld_spd, int64_t row_off, int64_t col_off,
+                              const float* table, int32_t n_buckets, float* o_part,
+                              float* lse_part, int32_t H, int32_t d, gt_dtype_t dtype,
+                              float scale, void* stream) {
+  return ring_impl(q_shard, Sq, k_shard, v_shard, Sk, spd, ld_spd, row_off, col_off, table,
+                   n_buckets, o_part, lse_part, H, d, dtype, scale, stream, 0);
+}
+
+gt_status_t gt_attn_ring_step_acc(const void* q_shard, int64_t Sq, const void* k_shard,
+                                  const void* v_shard, int64_t Sk, const uint8_t* spd,
+                                  int64_t ld_spd, int64_t row_off, int64_t col_off,
+                                  const float* table, int32_t n_buckets, float* o_acc,
+                                  float* lse_acc, int32_t H, int32_t d, gt_dtype_t dtype,
+                                  float scale, void* stream) {
+  return ring_impl(q_shard, Sq, k_shard, v_shard, Sk, spd, ld_spd, row_off, col_off, table,
+                   n_buckets, o_acc, lse_acc, H, d, dtype, scale, stream, 1);
 }
 
 gt_status_t gt_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* spd,

@@ -97,6 +97,25 @@ __device__ __forceinline__ float sum_bf16x8(const bf16x8& v, float acc) {
   return acc;
 }
 
+// Weights of a pairwise LSE merge (Section III-A-1 part 3): a running state
+// with log-sum-exp lo and a new block with lb combine to
+// O = wo O_running + wb O_block, LSE = out. Two -inf inputs give weights 0 and
+// out = -inf.
+__device__ __forceinline__ void lse_merge_weights(float lo, float lb, float& wo, float& wb, float& out) {
+  const float mx = fmaxf(lo, lb);
+  if (mx == -INFINITY) {
+    wo = 0.0f;
+    wb = 0.0f;
+    out = -INFINITY;
+    return;
+  }
+  const float eo = expf(lo - mx), eb = expf(lb - mx);
+  const float tot = eo + eb;
+  wo = eo / tot;
+  wb = eb / tot;
+  out = mx + logf(tot);
+}
+
 __device__ __forceinline__ uint16_t f2bf(float x) {
   __bf16 b = (__bf16)x;
   return __builtin_bit_cast(uint16_t, b);

@@ -399,16 +399,32 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
     const float lt = sm[qb].l + __shfl_xor(sm[qb].l, 32);
     const int64_t i = qbase + qb * 32 + col;
     if (i >= a.Sq) continue;
-    const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
+    float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
+    float lse_out = lt > 0.0f ? (sm[qb].m + __log2f(lt)) * kLn2 : -INFINITY;
+    float wo = 0.0f;     // weight of the running state (accumulate mode)
+    if constexpr (OUT_F32) {
+      if (a.accumulate) {
+        float wb;
+        lse_merge_weights(a.lse[(int64_t)h * a.Sq + i], lse_out, wo, wb, lse_out);
+        inv *= wb;
+      }
+    }
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int c = cb * 32 + 8 * u + 4 * g;
-        const float o0 = acc[qb][cb][4 * u + 0] * inv, o1 = acc[qb][cb][4 * u + 1] * inv;
-        const float o2 = acc[qb][cb][4 * u + 2] * inv, o3 = acc[qb][cb][4 * u + 3] * inv;
+        float o0 = acc[qb][cb][4 * u + 0] * inv, o1 = acc[qb][cb][4 * u + 1] * inv;
+        float o2 = acc[qb][cb][4 * u + 2] * inv, o3 = acc[qb][cb][4 * u + 3] * inv;
         if constexpr (OUT_F32) {
           float* op = reinterpret_cast<float*>(a.o) + ((int64_t)h * a.Sq + i) * D + c;
+          if (wo != 0.0f) {
+            const float4 old = *reinterpret_cast<const float4*>(op);
+            o0 = fmaf(old.x, wo, o0);
+            o1 = fmaf(old.y, wo, o1);
+            o2 = fmaf(old.z, wo, o2);
+            o3 = fmaf(old.w, wo, o3);
+          }
           *reinterpret_cast<float4*>(op) = make_float4(o0, o1, o2, o3);
         } else {
           uint16_t* op = reinterpret_cast<uint16_t*>(a.o) + ((int64_t)h * a.Sq + i) * D + c;
@@ -419,8 +435,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
         }
       }
     }
-    if (g == 0)
-      a.lse[(int64_t)h * a.Sq + i] = lt > 0.0f ? (sm[qb].m + __log2f(lt)) * kLn2 : -INFINITY;
+    if (g == 0) a.lse[(int64_t)h * a.Sq + i] = lse_out;
   }
 }
 
@@ -481,11 +496,18 @@ __global__ __launch_bounds__(128) void fwd_f32_kernel(FwdArgs a) {
     }
   }
   if (!ok) return;
-  const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+  float inv = l > 0.0f ? 1.0f / l : 0.0f;
+  float lse_out = l > 0.0f ? m + logf(l) : -INFINITY;
+  float wo = 0.0f;     // weight of the running state (accumulate mode)
+  if (a.accumulate) {
+    float wb;
+    lse_merge_weights(a.lse[(int64_t)h * a.Sq + i], lse_out, wo, wb, lse_out);
+    inv *= wb;
+  }
   float* op = reinterpret_cast<float*>(a.o) + ((int64_t)h * a.Sq + i) * D;
 #pragma unroll
-  for (int c = 0; c < D; ++c) op[c] = acc[c] * inv;
-  a.lse[(int64_t)h * a.Sq + i] = l > 0.0f ? m + logf(l) : -INFINITY;
+  for (int c = 0; c < D; ++c) op[c] = wo != 0.0f ? fmaf(op[c], wo, acc[c] * inv) : acc[c] * inv;
+  a.lse[(int64_t)h * a.Sq + i] = lse_out;
 }
 
 template <int D, bool OUT_F32>

@@ -25,6 +25,8 @@ struct FwdArgs {
   int64_t Sk;
   float scale;            // multiplies Q K^T
   int32_t spd_vec;        // every 16-byte spd group is 16-byte aligned
+  int32_t accumulate;     // 1 (fp32 outputs only): o, lse hold a running merged state and
+                          // this block is merged into it in place
 };
 
 // Backward of a query block (Sq rows: q, o, d_o, lse, dq and the workspace

@@ -25,7 +25,7 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol():
     L = gt.lib()
     syms = declared_symbols()
-    assert {"gt_attn_fwd", "gt_attn_bwd", "gt_attn_ring_step", "gt_attn_merge",
+    assert {"gt_attn_fwd", "gt_attn_bwd", "gt_attn_ring_step", "gt_attn_ring_step_acc", "gt_attn_merge",
             "gt_attn_bwd_ring_step", "gt_attn_bwd_ring_workspace_size",
             "gt_attn_bwd_workspace_size", "gt_status_string"} <= set(syms)
     for s in syms:
@@ -62,13 +62,13 @@ def test_fwd_validation(kw, code):
     assert _fwd(**kw) == code
 
 
-def _ring(**kw):
+def _ring(entry="gt_attn_ring_step", **kw):
     a = dict(q=FAKE, Sq=100, k=FAKE, v=FAKE, Sk=64, spd=FAKE, ld=4096, ro=0, co=128, table=FAKE,
              nb=32, o=FAKE, lse=FAKE, H=8, d=64, dt=BF16, scale=0.125)
     a.update(kw)
-    return gt.lib().gt_attn_ring_step(a["q"], a["Sq"], a["k"], a["v"], a["Sk"], a["spd"], a["ld"],
-                                      a["ro"], a["co"], a["table"], a["nb"], a["o"], a["lse"],
-                                      a["H"], a["d"], a["dt"], a["scale"], None)
+    return getattr(gt.lib(), entry)(a["q"], a["Sq"], a["k"], a["v"], a["Sk"], a["spd"], a["ld"],
+                                    a["ro"], a["co"], a["table"], a["nb"], a["o"], a["lse"],
+                                    a["H"], a["d"], a["dt"], a["scale"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -79,8 +79,9 @@ def _ring(**kw):
     (dict(table=None), INVALID), (dict(nb=300), INVALID), (dict(d=16), UNSUPPORTED),
     (dict(scale=0.0), INVALID), (dict(k=MIS), INVALID),
 ])
-def test_ring_step_validation(kw, code):
-    assert _ring(**kw) == code
+@pytest.mark.parametrize("entry", ["gt_attn_ring_step", "gt_attn_ring_step_acc"])
+def test_ring_step_validation(entry, kw, code):
+    assert _ring(entry, **kw) == code
 
 
 def _bwd(**kw):

@@ -175,6 +175,17 @@ def test_context_parallel_share_cp256k():
     e_l = max_abs(to_np(L), to_np(L_full))
     say(f"cp256k: merged vs unsharded step O {e_o:.2e} LSE {e_l:.2e}")
     assert e_o <= TOL["bf16"]["o"] and e_l <= 1e-4
+    # the same ring with the in-place running merge (state started by step 0)
+    state = (parts_o[0].clone(), parts_l[0].clone())
+    for t in range(1, P):
+        c0 = ((rank - t) % P) * S
+        gt.gt_attn_ring_step_acc(Qs, K[:, c0:c0 + S].contiguous(), V[:, c0:c0 + S].contiguous(),
+                                 spd_sh, 0, c0, T, state, scale=scale)
+    torch.cuda.synchronize()
+    e_o2 = max_abs(to_np(state[0]), to_np(O_full))
+    e_l2 = max_abs(to_np(state[1]), to_np(L_full))
+    say(f"cp256k: accumulated ring vs unsharded step O {e_o2:.2e} LSE {e_l2:.2e}")
+    assert e_o2 <= TOL["bf16"]["o"] and e_l2 <= 1e-4
     R = w.sample_rows(62, lo=r0, hi=r0 + S)
     spd_R = w.spd_rows(R)
     o_ref, l_ref = oracle.block_attention(q[:, R], k, v, spd_R, table, scale)

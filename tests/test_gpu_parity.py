@@ -193,6 +193,76 @@ def test_context_parallel_ring_small(dt):
         check_fwd(f"cp rank {r}", to_np(O), to_np(L), O_ref[:, r0:r1], L_ref[:, r0:r1], dt)
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_context_parallel_ring_accumulate(dt):
+    """The same ring with the in-place running merge: the first step's
+    partial starts the state, every later step is merged into it by the
+    kernel. Equals the unsharded oracle forward and, within fp32 rounding,
+    the merge of the separate partials. Rows 0..5 only see -inf buckets in
+    block 0 and nowhere else; rows 6..8 see -inf buckets everywhere."""
+    H, N, d, nb = 2, 1000, 64, 16
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=13, dt=dt)
+    table[:, :4] = -np.inf
+    bounds = [0, 240, 500, 777, 1000]
+    spd[:6, bounds[0]:bounds[1]] = 1
+    spd[6:9] = 2
+    td = tdtype(dt)
+    Q, K, V, T = to_dev(q, td), to_dev(k, td), to_dev(v, td), to_dev(table)
+    O_ref, L_ref = oracle.forward(q, k, v, spd, table, 0.125)
+    P = len(bounds) - 1
+    for r in range(P):
+        r0, r1 = bounds[r], bounds[r + 1]
+        shard = to_dev(spd[r0:r1], torch.uint8)
+        Qr = Q[:, r0:r1].contiguous()
+        parts_o, parts_l, state = [], [], None
+        for t in range(P):
+            b = (r - t) % P
+            c0, c1 = bounds[b], bounds[b + 1]
+            Kb, Vb = K[:, c0:c1].contiguous(), V[:, c0:c1].contiguous()
+            o_p, l_p = gt.gt_attn_ring_step(Qr, Kb, Vb, shard, 0, c0, T, scale=0.125)
+            parts_o.append(o_p)
+            parts_l.append(l_p)
+            if state is None:
+                state = (o_p.clone(), l_p.clone())
+            else:
+                gt.gt_attn_ring_step_acc(Qr, Kb, Vb, shard, 0, c0, T, state, scale=0.125)
+        O_m, L_m = gt.gt_attn_merge(torch.stack(parts_o), torch.stack(parts_l), dtype=torch.float32)
+        torch.cuda.synchronize()
+        say(f"cp accumulate {dt} rank {r}")
+        o_acc, l_acc = to_np(state[0]), to_np(state[1])
+        assert np.isfinite(o_acc).all()
+        check_fwd(f"cp acc rank {r}", o_acc, l_acc, O_ref[:, r0:r1], L_ref[:, r0:r1], dt)
+        assert max_abs(o_acc, to_np(O_m)) <= 1e-5 and max_abs(l_acc, to_np(L_m)) <= 1e-5
+        if r == 0:
+            assert np.isneginf(l_acc[:, 6:9]).all() and np.all(o_acc[:, 6:9] == 0)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_ring_step_acc_from_empty_state_and_empty_block(dt):
+    """A state at O = 0, LSE = -inf plus one step equals that step's partial;
+    a step with no keys (Sk = 0) leaves the state bit for bit unchanged."""
+    H, Sq, Sk, d, nb = 3, 200, 150, 32, 8
+    g = np.random.default_rng(3)
+    q = g.standard_normal((H, Sq, d)).astype(np.float32) * 0.2
+    k = g.standard_normal((H, Sk, d)).astype(np.float32) * 0.2
+    v = g.standard_normal((H, Sk, d)).astype(np.float32)
+    spd = g.integers(0, nb, size=(Sq, Sk)).astype(np.uint8)
+    table = (g.standard_normal((H, nb)) * 0.5).astype(np.float32)
+    td = tdtype(dt)
+    Q, K, V, S, T = to_dev(q, td), to_dev(k, td), to_dev(v, td), to_dev(spd, torch.uint8), to_dev(table)
+    say(f"ring acc empty state {dt}")
+    o_p, l_p = gt.gt_attn_ring_step(Q, K, V, S, 0, 0, T, scale=0.2)
+    state = (torch.zeros((H, Sq, d), device=DEV), torch.full((H, Sq), -math.inf, device=DEV))
+    gt.gt_attn_ring_step_acc(Q, K, V, S, 0, 0, T, state, scale=0.2)
+    torch.cuda.synchronize()
+    assert max_abs(to_np(state[0]), to_np(o_p)) <= 1e-6
+    assert max_abs(to_np(state[1]), to_np(l_p)) <= 1e-6
+    before = (state[0].clone(), state[1].clone())
+    gt.gt_attn_ring_step_acc(Q, None, None, None, 0, 0, T, state, scale=0.2)
+    torch.cuda.synchronize()
+    assert torch.equal(state[0], before[0]) and torch.equal(state[1], before[1])
+
+
 def test_forward_is_deterministic():
     H, N, d, nb = 4, 777, 64, 20
     q, k, v, do, table, spd = _case(H, N, d, nb, seed=21, dt="bf16")
