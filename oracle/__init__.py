@@ -18,5 +18,8 @@ from .attention import (  # noqa: F401
     ring_forward,
     ring_backward_step,
     ring_backward,
+    super_shard_rows,
+    ring_forward_super,
+    ring_backward_super,
     lse_bias_only,
 )

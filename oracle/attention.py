@@ -30,7 +30,7 @@ import numpy as np
 
 __all__ = ["bias_block", "block_attention", "block_backward", "forward", "backward",
            "ring_step", "merge", "ring_forward", "ring_backward_step", "ring_backward",
-           "lse_bias_only"]
+           "super_shard_rows", "ring_forward_super", "ring_backward_super", "lse_bias_only"]
 
 
 def _f64(x):
@@ -299,6 +299,98 @@ def ring_backward(q, k, v, spd, table, scale, d_out, bounds):
             a, b, c, e = ring_backward_step(q[:, r0:r1], O[:, r0:r1], L[:, r0:r1], d_out[:, r0:r1],
                                             k[:, c0:c1], v[:, c0:c1], spd_rows, 0, c0, table, scale)
             dq[:, r0:r1] += a
+            dk[:, c0:c1] += b
+            dv[:, c0:c1] += c
+            dt += e
+    return dq, dk, dv, dt
+
+
+def super_shard_rows(bounds, n_total, n_super, r):
+    """Global node ids of rank r's query shard when the batch holds
+    N' = n_total - n_super regular nodes (ids 0..N'-1, split by bounds over
+    [0, N']) and n_super global super nodes (ids N'..n_total-1): the rank's
+    regular nodes followed by every super node (Section III-A-1 part 1: the
+    regular nodes are partitioned, the super nodes replicated)."""
+    n_reg = n_total - n_super
+    return np.concatenate([np.arange(bounds[r], bounds[r + 1]), np.arange(n_reg, n_total)])
+
+
+def ring_forward_super(q, k, v, spd, table, scale, bounds, n_super):
+    """Simulate every rank of the ring when the batch has super nodes.
+
+    Rank r keeps the query rows super_shard_rows(...) and only those spd rows
+    (its bias shard [N'/P + N_s, N' + N_s], Section III-A-1 part 2). It visits
+    the P regular KV blocks in ring order (block (r - t) mod P, columns
+    [b_j, b_{j+1})) and, once, the super-node KV block (columns [N', N)),
+    then merges the P + 1 partials. Every super-node key thus enters each
+    query's softmax exactly once (the reading taken where the paper puts the
+    super nodes in every KV block). Returns O [H, N, d] and LSE [H, N] (the
+    super rows from rank 0) and, per rank, the super rows' (O, LSE), which
+    every rank computes."""
+    q, k, v, spd = np.asarray(q), np.asarray(k), np.asarray(v), np.asarray(spd)
+    P = len(bounds) - 1
+    H, N, _ = q.shape
+    n_reg = N - n_super
+    O = np.zeros((H, N, v.shape[2]))
+    L = np.zeros((H, N))
+    per_rank_super = []
+    for r in range(P):
+        rows = super_shard_rows(bounds, N, n_super, r)
+        spd_rows = spd[rows]
+        qs = q[:, rows]
+        parts_o, parts_l = [], []
+        for t in range(P):
+            blk = (r - t) % P
+            c0, c1 = bounds[blk], bounds[blk + 1]
+            o_p, l_p = ring_step(qs, k[:, c0:c1], v[:, c0:c1], spd_rows, 0, c0, table, scale)
+            parts_o.append(o_p)
+            parts_l.append(l_p)
+        if n_super > 0:
+            o_p, l_p = ring_step(qs, k[:, n_reg:], v[:, n_reg:], spd_rows, 0, n_reg, table, scale)
+            parts_o.append(o_p)
+            parts_l.append(l_p)
+        o_r, l_r = merge(np.stack(parts_o), np.stack(parts_l))
+        nr = bounds[r + 1] - bounds[r]
+        O[:, bounds[r]:bounds[r + 1]] = o_r[:, :nr]
+        L[:, bounds[r]:bounds[r + 1]] = l_r[:, :nr]
+        per_rank_super.append((o_r[:, nr:], l_r[:, nr:]))
+        if r == 0:
+            O[:, n_reg:] = o_r[:, nr:]
+            L[:, n_reg:] = l_r[:, nr:]
+    return O, L, per_rank_super
+
+
+def ring_backward_super(q, k, v, spd, table, scale, d_out, bounds, n_super):
+    """Backward of ring_forward_super on every rank. The super-node query rows
+    are replicated, so their loss terms must be counted once: rank 0 carries
+    their dO and every other rank passes dO = 0 for them (then their dS is 0
+    there: dP = 0 and Dlt = 0). Each rank visits the regular KV blocks and the
+    super block with ring_backward_step, accumulating its rows' dQ and each
+    block's dK, dV and dTable. Returns dQ, dK, dV [H, N, d] and dTable."""
+    q, k, v, spd, d_out = (np.asarray(x) for x in (q, k, v, spd, d_out))
+    P = len(bounds) - 1
+    H, N, _ = q.shape
+    n_reg = N - n_super
+    O, L, _ = ring_forward_super(q, k, v, spd, table, scale, bounds, n_super)
+    dq = np.zeros(q.shape)
+    dk = np.zeros(k.shape)
+    dv = np.zeros(v.shape)
+    dt = np.zeros(table.shape)
+    blocks = [(bounds[j], bounds[j + 1]) for j in range(P)]
+    for r in range(P):
+        rows = super_shard_rows(bounds, N, n_super, r)
+        spd_rows = spd[rows]
+        do_r = d_out[:, rows].copy()
+        nr = bounds[r + 1] - bounds[r]
+        if r != 0:
+            do_r[:, nr:] = 0.0
+        steps = [blocks[(r - t) % P] for t in range(P)]
+        if n_super > 0:
+            steps.append((n_reg, N))
+        for c0, c1 in steps:
+            a, b, c, e = ring_backward_step(q[:, rows], O[:, rows], L[:, rows], do_r,
+                                            k[:, c0:c1], v[:, c0:c1], spd_rows, 0, c0, table, scale)
+            dq[:, rows] += a
             dk[:, c0:c1] += b
             dv[:, c0:c1] += c
             dt += e

@@ -13,7 +13,7 @@ import torch
 import oracle
 import paper_2609_34420_amd as gt
 import synth
-from gpu_common import DEV, TOL, check_grads, rel_l2, say, tdtype, to_dev, to_np
+from gpu_common import DEV, TOL, check_fwd, check_grads, rel_l2, say, tdtype, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -195,3 +195,73 @@ def test_context_parallel_ring_backward(N, bounds, dt):
     ref = dict(zip(NAMES, oracle.backward(q, k, v, spd, table, scale, do)))
     got = dict(dq=to_np(dq), dk=to_np(dk), dv=to_np(dv), dtable=to_np(dtab))
     check_grads(f"cp ring backward N={N} P={P}", got, ref, dt)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("n_reg,n_super,bounds", [
+    (900, 37, [0, 300, 612, 900]),       # uneven shards, unaligned spd columns
+    (960, 64, [0, 320, 640, 960]),       # N = 1024: 16-byte aligned slices
+])
+def test_context_parallel_super_nodes(n_reg, n_super, bounds, dt):
+    """Super nodes (Section III-A-1 parts 1-2): each rank's query shard is
+    its regular rows plus every super-node row, with those spd rows only.
+    Forward: the running merge over the P regular KV blocks in ring order and
+    the super-node block once. Backward: the same steps, rank 0 carrying the
+    super rows' dO (zero on the other ranks), dK/dV per block, the super
+    block's accumulated by every rank. Both equal the unsharded oracle over
+    all N = N' + N_s nodes, and every rank computes the same super rows."""
+    H, d, nb = 2, 64, 16
+    N = n_reg + n_super
+    q, k, v, do, table, spd = _ring_case(H, N, d, nb, seed=N + 1, dt=dt)
+    scale = 1.0 / math.sqrt(d)
+    td = tdtype(dt)
+    Q, K, V, dO, T = to_dev(q, td), to_dev(k, td), to_dev(v, td), to_dev(do, td), to_dev(table)
+    P = len(bounds) - 1
+    blocks = [(bounds[j], bounds[j + 1]) for j in range(P)]
+    O_ref, L_ref = oracle.forward(q, k, v, spd, table, scale)
+    dq = torch.zeros(H, N, d, device=DEV)
+    dk = torch.zeros(H, N, d, device=DEV)
+    dv = torch.zeros(H, N, d, device=DEV)
+    dtab = torch.zeros(H, nb, device=DEV)
+    acc_k = {c: torch.zeros(H, e - c, d, device=DEV) for c, e in blocks + [(n_reg, N)]}
+    acc_v = {c: torch.zeros(H, e - c, d, device=DEV) for c, e in blocks + [(n_reg, N)]}
+    o_sup = []
+    for r in range(P):
+        rows = oracle.super_shard_rows(bounds, N, n_super, r)
+        nr = bounds[r + 1] - bounds[r]
+        idx = torch.from_numpy(rows).to(DEV)
+        shard = to_dev(spd[rows], torch.uint8)
+        q_r = Q[:, idx].contiguous()
+        steps = [blocks[(r - t) % P] for t in range(P)] + [(n_reg, N)]
+        state = None
+        for c0, c1 in steps:
+            Kb, Vb = K[:, c0:c1].contiguous(), V[:, c0:c1].contiguous()
+            if state is None:
+                state = gt.gt_attn_ring_step(q_r, Kb, Vb, shard, 0, c0, T, scale=scale)
+            else:
+                gt.gt_attn_ring_step_acc(q_r, Kb, Vb, shard, 0, c0, T, state, scale=scale)
+        O_r, L_r = gt.gt_attn_merge(state[0][None].contiguous(), state[1][None].contiguous(), dtype=td)
+        torch.cuda.synchronize()
+        say(f"super nodes {dt} N'={n_reg} Ns={n_super} rank {r}: forward")
+        check_fwd(f"super rank {r}", to_np(state[0]), to_np(state[1]), O_ref[:, rows], L_ref[:, rows], dt)
+        o_sup.append(to_np(state[0])[:, nr:])
+        do_r = dO[:, idx].contiguous()
+        if r != 0:
+            do_r[:, nr:] = 0
+        dq_r = torch.zeros(H, len(rows), d, device=DEV)
+        for c0, c1 in steps:
+            gt.gt_attn_bwd_ring_step(q_r, O_r, L_r, do_r, K[:, c0:c1].contiguous(),
+                                     V[:, c0:c1].contiguous(), shard, 0, c0, T, scale=scale,
+                                     acc=(dq_r, acc_k[c0], acc_v[c0], dtab))
+        dq[:, bounds[r]:bounds[r + 1]] += dq_r[:, :nr]
+        dq[:, n_reg:] += dq_r[:, nr:]
+    for c0, c1 in blocks + [(n_reg, N)]:
+        dk[:, c0:c1] = acc_k[c0]
+        dv[:, c0:c1] = acc_v[c0]
+    torch.cuda.synchronize()
+    for o_s in o_sup[1:]:
+        assert np.abs(o_s - o_sup[0]).max() <= 1e-5
+    say(f"super nodes {dt} N'={n_reg} Ns={n_super}: backward")
+    ref = dict(zip(NAMES, oracle.backward(q, k, v, spd, table, scale, do)))
+    got = dict(dq=to_np(dq), dk=to_np(dk), dv=to_np(dv), dtable=to_np(dtab))
+    check_grads(f"super nodes N'={n_reg} Ns={n_super}", got, ref, dt)

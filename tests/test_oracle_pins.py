@@ -442,3 +442,79 @@ def test_ring_backward_step_masked_rows_and_offsets():
     b = spd[np.ix_(rows, cols)]
     ref = np.array([dS[b == j].sum() for j in range(7)])
     np.testing.assert_allclose(dt[0], ref, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Super nodes (regular nodes partitioned, super nodes replicated)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("bounds,n_super", [([0, 40], 7), ([0, 11, 40], 7), ([0, 5, 19, 40], 1),
+                                            ([0, 3, 9, 10, 22, 30, 33, 37, 40], 10),
+                                            ([0, 13, 40], 0)])
+def test_ring_super_equals_unsharded(bounds, n_super):
+    """Each rank's shard = its regular rows plus every super-node row; the
+    ring visits the P regular KV blocks and the super-node block once. The
+    merged result equals the unsharded forward over all N = N' + N_s nodes,
+    and every rank computes the same super-node rows."""
+    N = 40 + n_super
+    q, k, v, _, table, spd = _rand_case(H=2, N=N, d=8, nb=6, seed=31, out_of_range=True)
+    s = 0.35
+    O, L = oracle.forward(q, k, v, spd, table, s)
+    Or, Lr, sup = oracle.ring_forward_super(q, k, v, spd, table, s, bounds, n_super)
+    np.testing.assert_allclose(Or, O, atol=1e-12)
+    np.testing.assert_allclose(Lr, L, atol=1e-12)
+    for o_s, l_s in sup:
+        np.testing.assert_allclose(o_s, O[:, 40:], atol=1e-12)
+        np.testing.assert_allclose(l_s, L[:, 40:], atol=1e-12)
+    if n_super == 0:
+        O0, L0 = oracle.ring_forward(q, k, v, spd, table, s, bounds)
+        np.testing.assert_allclose(Or, O0, atol=1e-14)
+
+
+def test_super_nodes_in_every_block_are_counted_per_block():
+    """Putting the super-node columns into every KV block (each block =
+    regular columns plus the super columns) counts each super node P times:
+    every row's total weight on the super nodes is multiplied by P, so for
+    P = 3 the merged LSE of every row sits between the unsharded LSE and
+    the unsharded LSE + ln 3, strictly above it, and differs from the
+    count-once ring. With P = 1 the two coincide."""
+    n_reg, n_super = 30, 5
+    N = n_reg + n_super
+    q, k, v, _, table, spd = _rand_case(H=2, N=N, d=8, nb=6, seed=32)
+    s = 0.35
+    O, L = oracle.forward(q, k, v, spd, table, s)
+    for bounds in ([0, 30], [0, 9, 20, 30]):
+        P = len(bounds) - 1
+        for r in range(P):
+            rows = oracle.super_shard_rows(bounds, N, n_super, r)
+            parts_o, parts_l = [], []
+            for t in range(P):
+                c0, c1 = bounds[(r - t) % P], bounds[(r - t) % P + 1]
+                cols = np.concatenate([np.arange(c0, c1), np.arange(n_reg, N)])
+                o_p, l_p = oracle.block_attention(q[:, rows], k[:, cols], v[:, cols],
+                                                  spd[np.ix_(rows, cols)], table, s)
+                parts_o.append(o_p)
+                parts_l.append(l_p)
+            On, Ln = oracle.merge(np.stack(parts_o), np.stack(parts_l))
+            if P == 1:
+                np.testing.assert_allclose(Ln, L[:, rows], atol=1e-12)
+                np.testing.assert_allclose(On, O[:, rows], atol=1e-12)
+            else:
+                assert np.all(Ln > L[:, rows] + 1e-9)
+                assert np.all(Ln < L[:, rows] + math.log(P) + 1e-9)
+                assert np.abs(On - O[:, rows]).max() > 1e-3
+
+
+@pytest.mark.parametrize("bounds,n_super", [([0, 40], 6), ([0, 11, 40], 6),
+                                            ([0, 3, 9, 22, 30, 40], 9)])
+def test_ring_backward_super_equals_unsharded(bounds, n_super):
+    """Backward with super nodes: rank 0 carries the super rows' dO, the other
+    ranks pass zero for them; dQ per rank, dK/dV/dTable per block (super
+    block included) add up to the unsharded backward."""
+    N = 40 + n_super
+    q, k, v, do, table, spd = _rand_case(H=2, N=N, d=8, nb=6, seed=33, out_of_range=True)
+    s = 0.35
+    ref = oracle.backward(q, k, v, spd, table, s, do)
+    got = oracle.ring_backward_super(q, k, v, spd, table, s, do, bounds, n_super)
+    for a, b in zip(got, ref):
+        np.testing.assert_allclose(a, b, atol=1e-11)
