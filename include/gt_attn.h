@@ -65,6 +65,26 @@ gt_status_t gt_attn_fwd(const void* q, const void* k, const void* v,
                         int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
                         float scale, void* stream);
 
+/* A batch of B graphs (sequences) of N nodes each, H heads per graph, every
+ * graph with its own spd and all sharing one table (a training batch of b
+ * sampled sequences, as in the memory model of Section III-B, Eqs. (6)-(7),
+ * and the batch sizes of Section IV-A; Eq. (1) per graph):
+ *   q, k, v  [B, H, N, d] dtype          o [B, H, N, d] dtype (written)
+ *   spd      graph b's [N, N] uint8 matrix at spd + b * spd_bstride
+ *            (spd_bstride = N * N for a dense [B, N, N] array; 0 lets every
+ *            graph share one spd); the caller keeps every graph's N * N bytes
+ *            inside its allocation
+ *   table    [H, n_buckets] fp32, shared by the batch
+ *   lse      [B, H, N] fp32 (written)
+ * B >= 1, spd_bstride >= 0; otherwise as gt_attn_fwd, which is this call
+ * with B = 1. Deterministic. */
+gt_status_t gt_attn_fwd_batch(const void* q, const void* k, const void* v,
+                              const uint8_t* spd, int64_t spd_bstride,
+                              const float* table, int32_t n_buckets,
+                              void* o, float* lse,
+                              int32_t B, int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
+                              float scale, void* stream);
+
 /* Bytes of device workspace gt_attn_bwd needs for these sizes. */
 size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dtype);
 
@@ -98,6 +118,21 @@ gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v,
                         void* workspace, size_t workspace_bytes,
                         int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
                         float scale, void* stream);
+
+/* Backward of gt_attn_fwd_batch: dq, dk, dv [B, H, N, d] dtype (overwritten);
+ * dtable [H, n_buckets] fp32 (overwritten) sums the gradient over every graph
+ * of the batch, since they share the table. spd_t (optional) holds graph b's
+ * transpose at spd_t + b * spd_bstride. workspace: at least
+ * gt_attn_bwd_workspace_size(B * H, N, d, dtype) bytes. Otherwise as
+ * gt_attn_bwd, which is this call with B = 1. */
+gt_status_t gt_attn_bwd_batch(const void* q, const void* k, const void* v,
+                              const uint8_t* spd, const uint8_t* spd_t, int64_t spd_bstride,
+                              const float* table, int32_t n_buckets,
+                              const void* o, const float* lse, const void* d_o,
+                              void* dq, void* dk, void* dv, float* dtable,
+                              void* workspace, size_t workspace_bytes,
+                              int32_t B, int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
+                              float scale, void* stream);
 
 /* The backward split into its three stages, for callers that schedule them
  * (e.g. the two independent stages on two streams) or time them:

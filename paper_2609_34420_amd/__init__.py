@@ -8,6 +8,7 @@ If the library is missing or cannot be loaded, every call raises.
 
     o, lse = gt_attn_fwd(q, k, v, spd, table)                     # [H,N,d], [H,N]
     dq, dk, dv, dtable = gt_attn_bwd(q, k, v, spd, table, o, lse, d_o)
+    o, lse = gt_attn_fwd_batch(q_b, k_b, v_b, spd_b, table)      # [B,H,N,d], spd [B,N,N]
     o_p, lse_p = gt_attn_ring_step(q_sh, k_sh, v_sh, spd_shard, row_off, col_off, table)
     o, lse = gt_attn_merge(o_parts, lse_parts, dtype=torch.bfloat16)
     state = gt_attn_ring_step(...)                      # first step: a running state
@@ -71,6 +72,13 @@ def lib() -> ctypes.CDLL:
                                         _P, _P, _I32, _I32, _I32, _F, _P]
         L.gt_attn_ring_step_acc.restype = _I32
         L.gt_attn_ring_step_acc.argtypes = L.gt_attn_ring_step.argtypes
+        L.gt_attn_fwd_batch.restype = _I32
+        L.gt_attn_fwd_batch.argtypes = [_P, _P, _P, _P, _I64, _P, _I32, _P, _P, _I32, _I32, _I64,
+                                        _I32, _I32, _F, _P]
+        L.gt_attn_bwd_batch.restype = _I32
+        L.gt_attn_bwd_batch.argtypes = [_P, _P, _P, _P, _P, _I64, _P, _I32, _P, _P, _P, _P, _P, _P,
+                                        _P, _P, ctypes.c_size_t, _I32, _I32, _I64, _I32, _I32, _F,
+                                        _P]
         L.gt_attn_bwd_ring_workspace_size.restype = ctypes.c_size_t
         L.gt_attn_bwd_ring_workspace_size.argtypes = [_I32, _I64, _I64, _I32, _I32]
         L.gt_attn_bwd_ring_step.restype = _I32
@@ -191,6 +199,66 @@ def gt_attn_bwd_phase(phase: int, q, k, v, spd, table, o, lse, d_o, scale: float
         _check(lib().gt_attn_bwd(*args), "gt_attn_bwd")
     else:
         _check(lib().gt_attn_bwd_phase(int(phase), *args), "gt_attn_bwd_phase")
+    return dq, dk, dv, dtable
+
+
+def _batch_spd(spd, B, N):
+    _need(spd.dtype == torch.uint8 and spd.dim() in (2, 3) and tuple(spd.shape[-2:]) == (N, N),
+          "spd must be uint8 [B, N, N] or [N, N] (shared by the batch)")
+    if spd.dim() == 2:
+        return 0
+    _need(spd.shape[0] == B, "spd must hold one [N, N] matrix per graph")
+    return spd.stride(0) if B > 1 else 0
+
+
+def gt_attn_fwd_batch(q, k, v, spd, table, scale: float | None = None, out=None, lse=None,
+                      stream=None):
+    """O, LSE of a batch of graphs (C ABI gt_attn_fwd_batch). q, k, v
+    [B, H, N, d]; spd [B, N, N] uint8 (or [N, N] shared); table [H, nb]."""
+    B, H, N, d = q.shape
+    _dev_contig(q, k, v, spd, table, out, lse)
+    stride = _batch_spd(spd, B, N)
+    _need(table.dtype == torch.float32 and table.dim() == 2 and table.shape[0] == H,
+          "table must be fp32 [H, n_buckets]")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, N), device=q.device, dtype=torch.float32)
+    st = lib().gt_attn_fwd_batch(_ptr(q), _ptr(k), _ptr(v), _ptr(spd), stride, _ptr(table),
+                                 table.shape[1], _ptr(out), _ptr(lse), B, H, N, d, _dt(q), scale,
+                                 _stream(stream))
+    _check(st, "gt_attn_fwd_batch")
+    return out, lse
+
+
+def gt_attn_bwd_batch(q, k, v, spd, table, o, lse, d_o, scale: float | None = None,
+                      workspace=None, grads=None, stream=None, spd_t=None):
+    """dQ, dK, dV [B, H, N, d] and dTable [H, nb] summed over the batch (C ABI
+    gt_attn_bwd_batch); spd_t, if given, has spd's shape."""
+    B, H, N, d = q.shape
+    _dev_contig(q, k, v, spd, table, o, lse, d_o)
+    stride = _batch_spd(spd, B, N)
+    if spd_t is not None:
+        _dev_contig(spd_t)
+        _need(tuple(spd_t.shape) == tuple(spd.shape) and spd_t.dtype == spd.dtype and
+              spd_t.stride() == spd.stride(), "spd_t must have the shape and layout of spd")
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    if grads is None:
+        grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
+                 torch.empty_like(table))
+    dq, dk, dv, dtable = grads
+    _dev_contig(dq, dk, dv, dtable)
+    need = gt_attn_bwd_workspace_size(B * H, N, d, q.dtype)
+    if workspace is None:
+        workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
+    st = lib().gt_attn_bwd_batch(_ptr(q), _ptr(k), _ptr(v), _ptr(spd),
+                                 None if spd_t is None else _ptr(spd_t), stride, _ptr(table),
+                                 table.shape[1], _ptr(o), _ptr(lse), _ptr(d_o), _ptr(dq), _ptr(dk),
+                                 _ptr(dv), _ptr(dtable), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), B, H, N, d, _dt(q),
+                                 scale, _stream(stream))
+    _check(st, "gt_attn_bwd_batch")
     return dq, dk, dv, dtable
 
 

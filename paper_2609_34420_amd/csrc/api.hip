@@ -73,6 +73,7 @@ static gt_status_t ring_impl(const void* q_shard, int64_t Sq, const void* k_shar
   a.H = H; a.Sq = Sq; a.Sk = Sk; a.scale = scale;
   a.spd_vec = Sk > 0 ? spd_vec(spd, ld_spd, row_off, col_off) : 0;
   a.accumulate = accumulate;
+  a.hpb = H; a.spd_bstride = 0;
   return launched(gt::launch_fwd(a, d, dtype == GT_BF16, true, static_cast<hipStream_t>(stream)));
 }
 
@@ -96,25 +97,45 @@ gt_status_t gt_attn_ring_step_acc(const void* q_shard, int64_t Sq, const void* k
                    n_buckets, o_acc, lse_acc, H, d, dtype, scale, stream, 1);
 }
 
-gt_status_t gt_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* spd,
-                        const float* table, int32_t n_buckets, void* o, float* lse,
-                        int32_t H, int64_t N, int32_t d, gt_dtype_t dtype, float scale,
-                        void* stream) {
+// B sequences of N nodes, H heads each, run as B * H heads; sequence b reads
+// its spd at spd + b * spd_bstride.
+static gt_status_t fwd_impl(const void* q, const void* k, const void* v, const uint8_t* spd,
+                            int64_t spd_bstride, const float* table, int32_t n_buckets, void* o,
+                            float* lse, int32_t B, int32_t H, int64_t N, int32_t d,
+                            gt_dtype_t dtype, float scale, void* stream) {
   if (!dtype_ok(dtype)) return GT_ERR_UNSUPPORTED;
   if (!dims_ok(d)) return GT_ERR_UNSUPPORTED;
-  if (H < 1 || N < 1 || n_buckets < 1 || n_buckets > 256 || !scale_ok(scale)) return GT_ERR_INVALID;
+  if (B < 1 || H < 1 || N < 1 || spd_bstride < 0) return GT_ERR_INVALID;
+  if (n_buckets < 1 || n_buckets > 256 || !scale_ok(scale)) return GT_ERR_INVALID;
   if (!q || !k || !v || !spd || !table || !o || !lse) return GT_ERR_INVALID;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return GT_ERR_INVALID;
-  if ((N + 127) / 128 * (int64_t)H > kMaxGrid) return GT_ERR_INVALID;
+  const int64_t HT = (int64_t)B * H;
+  if (HT > 0x7fffffff || (N + 127) / 128 * HT > kMaxGrid) return GT_ERR_INVALID;
   if (N > kMaxLd) return GT_ERR_UNSUPPORTED;
   gt::FwdArgs a{};
   a.q = q; a.k = k; a.v = v;
   a.spd = spd; a.ld_spd = N; a.row_off = 0; a.col_off = 0;
   a.table = table; a.n_buckets = n_buckets;
   a.o = o; a.lse = lse;
-  a.H = H; a.Sq = N; a.Sk = N; a.scale = scale;
-  a.spd_vec = spd_vec(spd, N, 0, 0);
+  a.H = (int32_t)HT; a.Sq = N; a.Sk = N; a.scale = scale;
+  a.hpb = H; a.spd_bstride = spd_bstride;
+  a.spd_vec = spd_vec(spd, N, 0, 0) && spd_bstride % 16 == 0;
   return launched(gt::launch_fwd(a, d, dtype == GT_BF16, dtype == GT_F32, static_cast<hipStream_t>(stream)));
+}
+
+gt_status_t gt_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* spd,
+                        const float* table, int32_t n_buckets, void* o, float* lse,
+                        int32_t H, int64_t N, int32_t d, gt_dtype_t dtype, float scale,
+                        void* stream) {
+  return fwd_impl(q, k, v, spd, 0, table, n_buckets, o, lse, 1, H, N, d, dtype, scale, stream);
+}
+
+gt_status_t gt_attn_fwd_batch(const void* q, const void* k, const void* v, const uint8_t* spd,
+                              int64_t spd_bstride, const float* table, int32_t n_buckets, void* o,
+                              float* lse, int32_t B, int32_t H, int64_t N, int32_t d,
+                              gt_dtype_t dtype, float scale, void* stream) {
+  return fwd_impl(q, k, v, spd, spd_bstride, table, n_buckets, o, lse, B, H, N, d, dtype, scale,
+                  stream);
 }
 
 size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dtype) {
@@ -127,15 +148,18 @@ size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dt
 }
 
 static gt_status_t bwd_impl(int32_t phase, const void* q, const void* k, const void* v,
-                            const uint8_t* spd, const uint8_t* spd_t, const float* table,
-                            int32_t n_buckets,
+                            const uint8_t* spd, const uint8_t* spd_t, int64_t spd_bstride,
+                            const float* table, int32_t n_buckets,
                             const void* o, const float* lse, const void* d_o, void* dq,
                             void* dk, void* dv, float* dtable, void* workspace,
-                            size_t workspace_bytes, int32_t H, int64_t N, int32_t d,
+                            size_t workspace_bytes, int32_t B, int32_t Hh, int64_t N, int32_t d,
                             gt_dtype_t dtype, float scale, void* stream) {
   if (!dtype_ok(dtype)) return GT_ERR_UNSUPPORTED;
   if (!dims_ok(d)) return GT_ERR_UNSUPPORTED;
-  if (H < 1 || N < 1 || n_buckets < 1 || n_buckets > 256 || !scale_ok(scale)) return GT_ERR_INVALID;
+  if (B < 1 || Hh < 1 || N < 1 || spd_bstride < 0) return GT_ERR_INVALID;
+  if ((int64_t)B * Hh > 0x7fffffff) return GT_ERR_INVALID;
+  const int32_t H = B * Hh;   // heads of the whole batch
+  if (n_buckets < 1 || n_buckets > 256 || !scale_ok(scale)) return GT_ERR_INVALID;
   if (!q || !k || !v || !spd || !table || !o || !lse || !d_o || !dq || !dk || !dv || !dtable)
     return GT_ERR_INVALID;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(d_o) ||
@@ -158,10 +182,12 @@ static gt_status_t bwd_impl(int32_t phase, const void* q, const void* k, const v
   a.nmax = reinterpret_cast<float*>(static_cast<char*>(workspace) + 2 * align_up(rows * sizeof(float)));
   a.H = H; a.Sq = N; a.Sk = N; a.scale = scale;
   a.row_off = 0; a.col_off = 0; a.accumulate = 0;
-  a.spd_vec = spd_vec(spd, N, 0, 0);
+  a.hpb = Hh; a.spd_bstride = spd_bstride;
+  a.spd_vec = spd_vec(spd, N, 0, 0) && spd_bstride % 16 == 0;
   // The transpose is used only where its rows can be read 16 bytes at a time
   // and one key block's rows (256 of them) stay within 32-bit offsets.
-  a.spd_t = (spd_t && spd_vec(spd_t, N, 0, 0) && 256 * N < (int64_t(1) << 31)) ? spd_t : nullptr;
+  a.spd_t = (spd_t && spd_vec(spd_t, N, 0, 0) && spd_bstride % 16 == 0 &&
+             256 * N < (int64_t(1) << 31)) ? spd_t : nullptr;
   return launched(gt::launch_bwd(a, d, dtype == GT_BF16, phase, static_cast<hipStream_t>(stream)));
 }
 
@@ -170,8 +196,18 @@ gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v, const uint8
                         const float* lse, const void* d_o, void* dq, void* dk, void* dv,
                         float* dtable, void* workspace, size_t workspace_bytes, int32_t H,
                         int64_t N, int32_t d, gt_dtype_t dtype, float scale, void* stream) {
-  return bwd_impl(-1, q, k, v, spd, spd_t, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
-                  workspace, workspace_bytes, H, N, d, dtype, scale, stream);
+  return bwd_impl(-1, q, k, v, spd, spd_t, 0, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
+                  workspace, workspace_bytes, 1, H, N, d, dtype, scale, stream);
+}
+
+gt_status_t gt_attn_bwd_batch(const void* q, const void* k, const void* v, const uint8_t* spd,
+                              const uint8_t* spd_t, int64_t spd_bstride, const float* table,
+                              int32_t n_buckets, const void* o, const float* lse, const void* d_o,
+                              void* dq, void* dk, void* dv, float* dtable, void* workspace,
+                              size_t workspace_bytes, int32_t B, int32_t H, int64_t N, int32_t d,
+                              gt_dtype_t dtype, float scale, void* stream) {
+  return bwd_impl(-1, q, k, v, spd, spd_t, spd_bstride, table, n_buckets, o, lse, d_o, dq, dk, dv,
+                  dtable, workspace, workspace_bytes, B, H, N, d, dtype, scale, stream);
 }
 
 gt_status_t gt_attn_bwd_phase(int32_t phase, const void* q, const void* k, const void* v,
@@ -182,8 +218,8 @@ gt_status_t gt_attn_bwd_phase(int32_t phase, const void* q, const void* k, const
                               size_t workspace_bytes, int32_t H, int64_t N, int32_t d,
                               gt_dtype_t dtype, float scale, void* stream) {
   if (phase < 0 || phase > 2) return GT_ERR_INVALID;
-  return bwd_impl(phase, q, k, v, spd, spd_t, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
-                  workspace, workspace_bytes, H, N, d, dtype, scale, stream);
+  return bwd_impl(phase, q, k, v, spd, spd_t, 0, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
+                  workspace, workspace_bytes, 1, H, N, d, dtype, scale, stream);
 }
 
 size_t gt_attn_bwd_ring_workspace_size(int32_t H, int64_t Sq, int64_t Sk, int32_t d,
@@ -232,6 +268,7 @@ gt_status_t gt_attn_bwd_ring_step(const void* q_shard, const void* o_shard, cons
   a.lse2 = static_cast<float*>(workspace);
   a.dlt = reinterpret_cast<float*>(static_cast<char*>(workspace) + align_up(rows * sizeof(float)));
   a.nmax = reinterpret_cast<float*>(static_cast<char*>(workspace) + 2 * align_up(rows * sizeof(float)));
+  a.hpb = H; a.spd_bstride = 0;
   a.H = H; a.Sq = Sq; a.Sk = Sk; a.scale = scale;
   a.accumulate = 1;
   a.spd_vec = spd_vec(spd, ld_spd, row_off, col_off);

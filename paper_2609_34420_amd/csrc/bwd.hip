@@ -34,7 +34,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs a) {
   const int h = blockIdx.y;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (blockIdx.x == 0 && blockIdx.y == 0 && !a.accumulate) {
-    for (int t = threadIdx.x; t < a.H * a.n_buckets; t += 256) a.dtable[t] = 0.0f;
+    for (int t = threadIdx.x; t < a.hpb * a.n_buckets; t += 256) a.dtable[t] = 0.0f;
   }
   float nd = 0.0f, nv = 0.0f, nl = 0.0f;
   if (i < a.Sq) {
@@ -128,7 +128,7 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
   const int h = (int)(blockIdx.x / nqb);
   const int64_t i = (blockIdx.x % nqb) * 128 + tid;
   for (int t = tid; t < 256; t += 128) {
-    sT[t] = (t < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + t] : 0.0f;
+    sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
     sH[t] = 0.0f;
   }
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
@@ -146,7 +146,7 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
   }
   const float L = ok ? a.lse[(int64_t)h * a.Sq + i] : -INFINITY;
   const float dlt = ok ? a.dlt[(int64_t)h * a.Sq + i] : 0.0f;
-  const uint8_t* srow = ok ? a.spd + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
+  const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
     __syncthreads();
     for (int t = tid; t < TK * D; t += 128) {
@@ -180,7 +180,7 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
   }
   __syncthreads();
   for (int t = tid; t < a.n_buckets; t += 128)
-    if (sH[t] != 0.0f) atomicAdd(&a.dtable[(int64_t)h * a.n_buckets + t], sH[t]);
+    if (sH[t] != 0.0f) atomicAdd(&a.dtable[(int64_t)table_row(a, h) * a.n_buckets + t], sH[t]);
 }
 
 template <int D>
@@ -195,13 +195,13 @@ __global__ __launch_bounds__(128) void bwd_dkdv_f32_kernel(BwdArgs a) {
   const int h = (int)(blockIdx.x / nkb);
   const int64_t j = (blockIdx.x % nkb) * 128 + tid;
   for (int t = tid; t < 256; t += 128)
-    sT[t] = (t < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + t] : 0.0f;
+    sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
   const float* qh = reinterpret_cast<const float*>(a.q) + hq;
   const float* kh = reinterpret_cast<const float*>(a.k) + hk;
   const float* vh = reinterpret_cast<const float*>(a.v) + hk;
   const float* oh = reinterpret_cast<const float*>(a.d_o) + hq;
-  const uint8_t* sbase = a.spd + a.row_off * a.ld_spd + a.col_off;
+  const uint8_t* sbase = seq_spd(a, h) + a.row_off * a.ld_spd + a.col_off;
   const bool ok = j < a.Sk;
   float kv[D], vv[D], dk[D], dv[D];
 #pragma unroll

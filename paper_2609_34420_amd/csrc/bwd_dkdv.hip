@@ -337,7 +337,7 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   const int64_t ld = a.ld_spd;
   const int64_t jc = jok ? j : a.Sk - 1;
   const uint32_t key_off = (uint32_t)(jc - key0);
-  const uint8_t* spd_cols = a.spd + a.row_off * ld + a.col_off + key0;
+  const uint8_t* spd_cols = seq_spd(a, h) + a.row_off * ld + a.col_off + key0;
   const int64_t ntiles = (a.Sq + kBQ - 1) / kBQ;
   const DkdvOffsets<D> off;
 
@@ -347,7 +347,7 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   using BT = std::conditional_t<TR, uint32_t, uint8_t>;
   constexpr int NBT = TR ? 4 : 16;
   const __amdgpu_buffer_rsrc_t rs_t =
-      make_rsrc_n(TR ? a.spd_t + key0 * ld : a.spd, ((a.Sk - key0 < kBK ? a.Sk - key0 : kBK)) * ld);
+      make_rsrc_n(TR ? seq_spd_t(a, h) + key0 * ld : seq_spd(a, h), ((a.Sk - key0 < kBK ? a.Sk - key0 : kBK)) * ld);
   const uint32_t voff_t = (uint32_t)((jc - key0) * ld) + 16u * (uint32_t)g;
   auto fetch = [&](int64_t i_base, BT* dst) {
     if constexpr (TR) {
@@ -448,7 +448,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
 
   for (int t = tid; t < DkdvSmem<D, NB>::ENT; t += kThreads) {
     const int bkt = t / CPY;
-    const float tv = (bkt < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + bkt] * kLog2e : 0.0f;
+    const float tv = (bkt < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + bkt] * kLog2e : 0.0f;
     tabw[t] = make_uint2(__float_as_uint(tv), 0u);
     hist[t] = 0ull;
   }
@@ -504,7 +504,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
     long long t = 0;
 #pragma unroll
     for (int c = 0; c < CPY; ++c) t += (long long)hist[bkt * CPY + ((c + bkt) & (CPY - 1))];
-    if (t != 0) atomicAdd(&a.dtable[(int64_t)h * a.n_buckets + bkt], (float)((double)t * unscale));
+    if (t != 0) atomicAdd(&a.dtable[(int64_t)table_row(a, h) * a.n_buckets + bkt], (float)((double)t * unscale));
   }
 }
 

@@ -131,7 +131,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
   const int64_t qblk = lid / a.H;
   const int64_t qbase = qblk * BR + (int64_t)wave * 32;
 
-  fill_lane_table(sTab, a.table + (int64_t)h * a.n_buckets, a.n_buckets, a.scale, kThreads);
+  fill_lane_table(sTab, a.table + (int64_t)table_row(a, h) * a.n_buckets, a.n_buckets, a.scale, kThreads);
 
   const int64_t hq = (int64_t)h * a.Sq * D;   // query-side rows
   const int64_t hk = (int64_t)h * a.Sk * D;   // key-side rows
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
   // slices.
   const int64_t ld = a.ld_spd;
   const int64_t rb = qbase < a.Sq ? qbase : a.Sq - 1;
-  const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.spd + (a.row_off + rb) * ld + a.col_off);
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(seq_spd(a, h) + (a.row_off + rb) * ld + a.col_off);
   const uint32_t voff = (uint32_t)((qrow - rb) * ld) + 16u * g;
   const int64_t ntiles = (a.Sk + kBC - 1) / kBC;
   auto fetch_spd = [&](int64_t tt, uint32_t (&w)[kKB][4]) {
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
 #pragma unroll
       for (int kb = 0; kb < kKB; ++kb) buf_u128(rs, voff, (uint32_t)(jt + kb * 32), w[kb]);
     } else {
-      const uint8_t* row = a.spd + (a.row_off + qrow) * ld + a.col_off;
+      const uint8_t* row = seq_spd(a, h) + (a.row_off + qrow) * ld + a.col_off;
 #pragma unroll
       for (int kb = 0; kb < kKB; ++kb) load_spd16_bytes(row, jt + kb * 32 + 16 * g, a.Sk, w[kb]);
     }

@@ -205,7 +205,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   const int64_t qblk = lid / a.H;
   const int64_t qbase = qblk * BR + (int64_t)wave * 32 * kQB;
 
-  fill_lane_table(sTab, a.table + (int64_t)h * a.n_buckets, a.n_buckets, a.scale, kThreads);
+  fill_lane_table(sTab, a.table + (int64_t)table_row(a, h) * a.n_buckets, a.n_buckets, a.scale, kThreads);
 
   const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)h * a.Sq * D;
   const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + (int64_t)h * a.Sk * D;
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   // offset), or byte loads for the partial last tile and unaligned slices.
   const int64_t ld = a.ld_spd;
   const int64_t rb = qbase < a.Sq ? qbase : a.Sq - 1;
-  const __amdgpu_buffer_rsrc_t rs = make_rsrc(a.spd + (a.row_off + rb) * ld + a.col_off);
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(seq_spd(a, h) + (a.row_off + rb) * ld + a.col_off);
   uint32_t voff[kQB];
 #pragma unroll
   for (int qb = 0; qb < kQB; ++qb) voff[qb] = (uint32_t)((qrow[qb] - rb) * ld) + 16u * g;
@@ -243,7 +243,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
     } else {
 #pragma unroll
       for (int qb = 0; qb < kQB; ++qb) {
-        const uint8_t* row = a.spd + (a.row_off + qrow[qb]) * ld + a.col_off;
+        const uint8_t* row = seq_spd(a, h) + (a.row_off + qrow[qb]) * ld + a.col_off;
 #pragma unroll
         for (int kb = 0; kb < kKB; ++kb) load_spd16_bytes(row, jt + kb * 32 + 16 * g, a.Sk, w[qb][kb]);
       }
@@ -452,7 +452,7 @@ __global__ __launch_bounds__(128) void fwd_f32_kernel(FwdArgs a) {
   const int h = (int)(blockIdx.x / nqb);
   const int64_t i = (blockIdx.x % nqb) * 128 + tid;
   for (int t = tid; t < 256; t += 128)
-    sT[t] = (t < a.n_buckets) ? a.table[(int64_t)h * a.n_buckets + t] : 0.0f;
+    sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
   const float* qh = reinterpret_cast<const float*>(a.q) + (int64_t)h * a.Sq * D;
   const float* kh = reinterpret_cast<const float*>(a.k) + (int64_t)h * a.Sk * D;
   const float* vh = reinterpret_cast<const float*>(a.v) + (int64_t)h * a.Sk * D;
@@ -463,7 +463,7 @@ __global__ __launch_bounds__(128) void fwd_f32_kernel(FwdArgs a) {
     qv[c] = ok ? qh[i * D + c] * a.scale : 0.0f;
     acc[c] = 0.0f;
   }
-  const uint8_t* srow = ok ? a.spd + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
+  const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
   float m = -INFINITY, l = 0.0f;
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
     __syncthreads();

@@ -27,6 +27,8 @@ struct FwdArgs {
   int32_t spd_vec;        // every 16-byte spd group is 16-byte aligned
   int32_t accumulate;     // 1 (fp32 outputs only): o, lse hold a running merged state and
                           // this block is merged into it in place
+  int32_t hpb;            // heads per sequence: "head" h of H is head h % hpb of sequence h / hpb
+  int64_t spd_bstride;    // bytes from one sequence's spd to the next (0: one spd for all)
 };
 
 // Backward of a query block (Sq rows: q, o, d_o, lse, dq and the workspace
@@ -61,7 +63,22 @@ struct BwdArgs {
   float scale;
   int32_t spd_vec;        // every 16-byte spd group of the block is 16-byte aligned
   int32_t accumulate;     // 1: dq, dk, dv are fp32 and receive +=; dtable is not cleared
+  int32_t hpb;            // heads per sequence: "head" h of H is head h % hpb of sequence h / hpb
+                          // (table and dtable rows are per head, shared by the sequences)
+  int64_t spd_bstride;    // bytes from one sequence's spd (and spd_t) to the next (0: shared)
 };
+
+// A batch of sequences runs as H = B * hpb "heads": the table row of head h
+// and the spd (spd_t) of its sequence.
+template <typename Args>
+__device__ __forceinline__ int table_row(const Args& a, int h) { return h % a.hpb; }
+template <typename Args>
+__device__ __forceinline__ const uint8_t* seq_spd(const Args& a, int h) {
+  return a.spd + (int64_t)(h / a.hpb) * a.spd_bstride;
+}
+__device__ __forceinline__ const uint8_t* seq_spd_t(const BwdArgs& a, int h) {
+  return a.spd_t + (int64_t)(h / a.hpb) * a.spd_bstride;
+}
 
 struct MergeArgs {
   const float* o_parts;   // [P, H, S, d]

@@ -62,6 +62,49 @@ def test_fwd_validation(kw, code):
     assert _fwd(**kw) == code
 
 
+def _fwd_batch(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, spd=FAKE, bs=512 * 512, table=FAKE, nb=22, o=FAKE, lse=FAKE,
+             B=3, H=4, N=512, d=32, dt=F32, scale=0.125)
+    a.update(kw)
+    return gt.lib().gt_attn_fwd_batch(a["q"], a["k"], a["v"], a["spd"], a["bs"], a["table"],
+                                      a["nb"], a["o"], a["lse"], a["B"], a["H"], a["N"], a["d"],
+                                      a["dt"], a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), INVALID), (dict(B=-2), INVALID), (dict(bs=-1), INVALID), (dict(H=0), INVALID),
+    (dict(N=0), INVALID), (dict(q=None), INVALID), (dict(spd=None), INVALID),
+    (dict(lse=None), INVALID), (dict(nb=257), INVALID), (dict(scale=float("nan")), INVALID),
+    (dict(d=48), UNSUPPORTED), (dict(dt=7), UNSUPPORTED), (dict(o=MIS), INVALID),
+    (dict(B=70000, H=70000), INVALID),            # B * H past 2^31
+])
+def test_fwd_batch_validation(kw, code):
+    assert _fwd_batch(**kw) == code
+
+
+def _bwd_batch(**kw):
+    B, H, N, d = 3, 2, 100, 64
+    need = gt.lib().gt_attn_bwd_workspace_size(B * H, N, d, BF16)
+    a = dict(q=FAKE, k=FAKE, v=FAKE, spd=FAKE, spd_t=None, bs=N * N, table=FAKE, nb=8, o=FAKE,
+             lse=FAKE, do=FAKE, dq=FAKE, dk=FAKE, dv=FAKE, dt=FAKE, ws=FAKE, wsb=need, B=B, H=H,
+             N=N, d=d, dtype=BF16, scale=0.125)
+    a.update(kw)
+    return gt.lib().gt_attn_bwd_batch(a["q"], a["k"], a["v"], a["spd"], a["spd_t"], a["bs"],
+                                      a["table"], a["nb"], a["o"], a["lse"], a["do"], a["dq"],
+                                      a["dk"], a["dv"], a["dt"], a["ws"], a["wsb"], a["B"], a["H"],
+                                      a["N"], a["d"], a["dtype"], a["scale"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), INVALID), (dict(bs=-16), INVALID), (dict(dt=None), INVALID),
+    (dict(do=None), INVALID), (dict(ws=None), WORKSPACE),
+    (dict(wsb=gt.lib().gt_attn_bwd_workspace_size(2, 100, 64, BF16)), WORKSPACE),  # sized for one graph
+    (dict(d=16), UNSUPPORTED), (dict(dq=MIS), INVALID),
+])
+def test_bwd_batch_validation(kw, code):
+    assert _bwd_batch(**kw) == code
+
+
 def _ring(entry="gt_attn_ring_step", **kw):
     a = dict(q=FAKE, Sq=100, k=FAKE, v=FAKE, Sk=64, spd=FAKE, ld=4096, ro=0, co=128, table=FAKE,
              nb=32, o=FAKE, lse=FAKE, H=8, d=64, dt=BF16, scale=0.125)

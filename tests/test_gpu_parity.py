@@ -263,6 +263,51 @@ def test_ring_step_acc_from_empty_state_and_empty_block(dt):
     assert torch.equal(state[0], before[0]) and torch.equal(state[1], before[1])
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("B,N,d,spd_kind", [
+    (4, 200, 64, "per_graph"),      # ragged tiles, unaligned spd rows
+    (3, 256, 32, "per_graph_t"),    # aligned, with per-graph transposes
+    (5, 96, 64, "shared"),          # one spd for every graph (stride 0)
+])
+def test_batch_of_graphs(B, N, d, spd_kind, dt):
+    """A batch of graphs, each with its own spd, sharing the table: every
+    graph's O, LSE, dQ, dK, dV equal the oracle on that graph alone, and
+    dtable equals the sum of the graphs' oracle dtables."""
+    H, nb = 3, 12
+    g = np.random.default_rng(B * N + d)
+    shape = (B, H, N, d)
+    q, k, v = (g.standard_normal(shape).astype(np.float32) / np.float32(math.sqrt(d)) for _ in range(3))
+    do = g.standard_normal(shape).astype(np.float32)
+    if dt == "bf16":
+        q, k, v, do = (synth.round_bf16(x) for x in (q, k, v, do))
+    table = (g.standard_normal((H, nb)) * 0.5).astype(np.float32)
+    if spd_kind == "shared":
+        spd = g.integers(0, nb + 2, size=(N, N)).astype(np.uint8)
+        spd_b = [spd] * B
+    else:
+        spd = g.integers(0, nb + 2, size=(B, N, N)).astype(np.uint8)
+        spd_b = list(spd)
+    td = tdtype(dt)
+    Q, K, V, dO = (to_dev(x, td) for x in (q, k, v, do))
+    T = to_dev(table)
+    S = to_dev(spd, torch.uint8)
+    St = to_dev(np.ascontiguousarray(np.swapaxes(spd, -1, -2)), torch.uint8) if spd_kind == "per_graph_t" else None
+    scale = 1.0 / math.sqrt(d)
+    say(f"batch {dt} B={B} N={N} d={d} {spd_kind}")
+    O, L = gt.gt_attn_fwd_batch(Q, K, V, S, T, scale=scale)
+    dq, dk, dv, dtab = gt.gt_attn_bwd_batch(Q, K, V, S, T, O, L, dO, scale=scale, spd_t=St)
+    torch.cuda.synchronize()
+    dt_ref = np.zeros((H, nb))
+    for b in range(B):
+        ref = _oracle_full(q[b], k[b], v[b], do[b], table, spd_b[b], scale)
+        got = dict(o=to_np(O[b]), lse=to_np(L[b]), dq=to_np(dq[b]), dk=to_np(dk[b]),
+                   dv=to_np(dv[b]))
+        check_fwd(f"batch graph {b}", got["o"], got["lse"], ref["o"], ref["lse"], dt)
+        check_grads(f"batch graph {b}", got, ref, dt)
+        dt_ref += ref["dtable"]
+    assert rel_l2(to_np(dtab), dt_ref) <= TOL[dt]["grad"]
+
+
 def test_forward_is_deterministic():
     H, N, d, nb = 4, 777, 64, 20
     q, k, v, do, table, spd = _case(H, N, d, nb, seed=21, dt="bf16")
