@@ -16,7 +16,7 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-inline bool dims_ok(int32_t d) { return d == 32 || d == 64; }
+inline bool dims_ok(int32_t d) { return d == 8 || d == 16 || d == 32 || d == 64; }
 
 inline bool dtype_ok(gt_dtype_t t) { return t == GT_F32 || t == GT_BF16; }
 

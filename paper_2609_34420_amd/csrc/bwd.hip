@@ -114,10 +114,24 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// fp32 path (small workloads): one thread per query row / key column.
+// Vector-ALU path: one thread per query row / key column, fp32 math. Serves
+// fp32 inputs and bf16 inputs with head dims below 32 (IN_BF16: q, k, v, dO
+// are bf16, and so are dq, dk, dv unless the call accumulates into fp32).
 // ---------------------------------------------------------------------------
-template <int D>
-__global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
+template <int D, bool IN_BF16>
+__device__ __forceinline__ void store_grad(void* base, int64_t idx, float x, bool accumulate) {
+  if (accumulate) {
+    float* p = reinterpret_cast<float*>(base) + idx;
+    *p += x;
+  } else if constexpr (IN_BF16) {
+    reinterpret_cast<uint16_t*>(base)[idx] = f2bf(x);
+  } else {
+    reinterpret_cast<float*>(base)[idx] = x;
+  }
+}
+
+template <int D, bool IN_BF16>
+__global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
   constexpr int TK = 32;
   __shared__ float sK[TK][D];
   __shared__ float sV[TK][D];
@@ -132,16 +146,12 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
     sH[t] = 0.0f;
   }
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
-  const float* qh = reinterpret_cast<const float*>(a.q) + hq;
-  const float* kh = reinterpret_cast<const float*>(a.k) + hk;
-  const float* vh = reinterpret_cast<const float*>(a.v) + hk;
-  const float* oh = reinterpret_cast<const float*>(a.d_o) + hq;
   const bool ok = i < a.Sq;
   float qv[D], dov[D], acc[D];
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    qv[c] = ok ? qh[i * D + c] * a.scale : 0.0f;
-    dov[c] = ok ? oh[i * D + c] : 0.0f;
+    qv[c] = ok ? load_elem<IN_BF16>(a.q, hq + i * D + c) * a.scale : 0.0f;
+    dov[c] = ok ? load_elem<IN_BF16>(a.d_o, hq + i * D + c) : 0.0f;
     acc[c] = 0.0f;
   }
   const float L = ok ? a.lse[(int64_t)h * a.Sq + i] : -INFINITY;
@@ -152,8 +162,8 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
     for (int t = tid; t < TK * D; t += 128) {
       const int r = t / D, c = t % D;
       const bool in = j0 + r < a.Sk;
-      sK[r][c] = in ? kh[(j0 + r) * D + c] : 0.0f;
-      sV[r][c] = in ? vh[(j0 + r) * D + c] : 0.0f;
+      sK[r][c] = in ? load_elem<IN_BF16>(a.k, hk + (j0 + r) * D + c) : 0.0f;
+      sV[r][c] = in ? load_elem<IN_BF16>(a.v, hk + (j0 + r) * D + c) : 0.0f;
     }
     __syncthreads();
     if (!ok || L == -INFINITY) continue;
@@ -174,17 +184,16 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(BwdArgs a) {
     }
   }
   if (ok) {
-    float* dqp = reinterpret_cast<float*>(a.dq) + hq + i * D;
 #pragma unroll
-    for (int c = 0; c < D; ++c) dqp[c] = (a.accumulate ? dqp[c] : 0.0f) + acc[c] * a.scale;
+    for (int c = 0; c < D; ++c) store_grad<D, IN_BF16>(a.dq, hq + i * D + c, acc[c] * a.scale, a.accumulate);
   }
   __syncthreads();
   for (int t = tid; t < a.n_buckets; t += 128)
     if (sH[t] != 0.0f) atomicAdd(&a.dtable[(int64_t)table_row(a, h) * a.n_buckets + t], sH[t]);
 }
 
-template <int D>
-__global__ __launch_bounds__(128) void bwd_dkdv_f32_kernel(BwdArgs a) {
+template <int D, bool IN_BF16>
+__global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
   constexpr int TQ = 32;
   __shared__ float sQ[TQ][D];
   __shared__ float sO[TQ][D];
@@ -197,17 +206,13 @@ __global__ __launch_bounds__(128) void bwd_dkdv_f32_kernel(BwdArgs a) {
   for (int t = tid; t < 256; t += 128)
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
-  const float* qh = reinterpret_cast<const float*>(a.q) + hq;
-  const float* kh = reinterpret_cast<const float*>(a.k) + hk;
-  const float* vh = reinterpret_cast<const float*>(a.v) + hk;
-  const float* oh = reinterpret_cast<const float*>(a.d_o) + hq;
   const uint8_t* sbase = seq_spd(a, h) + a.row_off * a.ld_spd + a.col_off;
   const bool ok = j < a.Sk;
   float kv[D], vv[D], dk[D], dv[D];
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    kv[c] = ok ? kh[j * D + c] * a.scale : 0.0f;
-    vv[c] = ok ? vh[j * D + c] : 0.0f;
+    kv[c] = ok ? load_elem<IN_BF16>(a.k, hk + j * D + c) * a.scale : 0.0f;
+    vv[c] = ok ? load_elem<IN_BF16>(a.v, hk + j * D + c) : 0.0f;
     dk[c] = 0.0f;
     dv[c] = 0.0f;
   }
@@ -216,8 +221,8 @@ __global__ __launch_bounds__(128) void bwd_dkdv_f32_kernel(BwdArgs a) {
     for (int t = tid; t < TQ * D; t += 128) {
       const int r = t / D, c = t % D;
       const bool in = i0 + r < a.Sq;
-      sQ[r][c] = in ? qh[(i0 + r) * D + c] : 0.0f;
-      sO[r][c] = in ? oh[(i0 + r) * D + c] : 0.0f;
+      sQ[r][c] = in ? load_elem<IN_BF16>(a.q, hq + (i0 + r) * D + c) : 0.0f;
+      sO[r][c] = in ? load_elem<IN_BF16>(a.d_o, hq + (i0 + r) * D + c) : 0.0f;
     }
     for (int t = tid; t < TQ; t += 128) {
       const bool in = i0 + t < a.Sq;
@@ -245,12 +250,10 @@ __global__ __launch_bounds__(128) void bwd_dkdv_f32_kernel(BwdArgs a) {
     }
   }
   if (!ok) return;
-  float* dkp = reinterpret_cast<float*>(a.dk) + hk + j * D;
-  float* dvp = reinterpret_cast<float*>(a.dv) + hk + j * D;
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    dkp[c] = (a.accumulate ? dkp[c] : 0.0f) + dk[c] * a.scale;
-    dvp[c] = (a.accumulate ? dvp[c] : 0.0f) + dv[c];
+    store_grad<D, IN_BF16>(a.dk, hk + j * D + c, dk[c] * a.scale, a.accumulate);
+    store_grad<D, IN_BF16>(a.dv, hk + j * D + c, dv[c], a.accumulate);
   }
 }
 
@@ -266,7 +269,7 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
       hipLaunchKernelGGL((bwd_prep_kernel<D, false>), grid, dim3(256), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if (bf16) {
+  if (bf16 && D >= 32) {
     if (phase < 0 || phase == 1) {
       if ((e = launch_dkdv_bf16(a, D, s)) != hipSuccess) return e;
     }
@@ -275,14 +278,20 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
     }
     return e;
   }
-  // fp32: dK/dV in phase 1, dQ and dtable in phase 2
+  // vector-ALU path: dK/dV in phase 1, dQ and dtable in phase 2
   const int64_t nkb = (a.Sk + 127) / 128, nqb = (a.Sq + 127) / 128;
   if (phase < 0 || phase == 1) {
-    hipLaunchKernelGGL((bwd_dkdv_f32_kernel<D>), dim3((unsigned)(nkb * a.H)), dim3(128), 0, s, a);
+    if (bf16)
+      hipLaunchKernelGGL((bwd_dkdv_valu_kernel<D, true>), dim3((unsigned)(nkb * a.H)), dim3(128), 0, s, a);
+    else
+      hipLaunchKernelGGL((bwd_dkdv_valu_kernel<D, false>), dim3((unsigned)(nkb * a.H)), dim3(128), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (phase < 0 || phase == 2) {
-    hipLaunchKernelGGL((bwd_dq_f32_kernel<D>), dim3((unsigned)(nqb * a.H)), dim3(128), 0, s, a);
+    if (bf16)
+      hipLaunchKernelGGL((bwd_dq_valu_kernel<D, true>), dim3((unsigned)(nqb * a.H)), dim3(128), 0, s, a);
+    else
+      hipLaunchKernelGGL((bwd_dq_valu_kernel<D, false>), dim3((unsigned)(nqb * a.H)), dim3(128), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return e;
@@ -291,7 +300,12 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_bwd(const BwdArgs& a, int d, bool bf16, int phase, hipStream_t s) {
-  return d == 64 ? launch_bwd_t<64>(a, bf16, phase, s) : launch_bwd_t<32>(a, bf16, phase, s);
+  switch (d) {
+    case 8: return launch_bwd_t<8>(a, bf16, phase, s);
+    case 16: return launch_bwd_t<16>(a, bf16, phase, s);
+    case 32: return launch_bwd_t<32>(a, bf16, phase, s);
+    default: return launch_bwd_t<64>(a, bf16, phase, s);
+  }
 }
 
 }  // namespace gt

@@ -125,6 +125,15 @@ __device__ __forceinline__ float bf2f(uint16_t x) {
   return __uint_as_float(((uint32_t)x) << 16);
 }
 
+// Element idx of a tensor of bf16 (BF) or fp32 values, as fp32.
+template <bool BF>
+__device__ __forceinline__ float load_elem(const void* p, int64_t idx) {
+  if constexpr (BF)
+    return bf2f(reinterpret_cast<const uint16_t*>(p)[idx]);
+  else
+    return reinterpret_cast<const float*>(p)[idx];
+}
+
 // Workgroup id -> logical id so that consecutive logical ids (the H heads of
 // one row block, which share their spd tiles) land on the same XCD at about
 // the same time. Workgroups are handed to the 8 XCDs round robin.

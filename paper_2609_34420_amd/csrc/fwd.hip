@@ -439,10 +439,14 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   }
 }
 
-// fp32 path: one thread per query row, keys staged through LDS, exact fp32
-// math with expf/logf. Written for the small fp32 workloads.
-template <int D>
-__global__ __launch_bounds__(128) void fwd_f32_kernel(FwdArgs a) {
+// Vector-ALU path: one thread per query row, keys staged through LDS as fp32,
+// fp32 math with expf/logf. Serves fp32 inputs (any head dim) and bf16
+// inputs with head dims below the 32 the matrix-core kernels tile by, where
+// the work per score element is the bias gather and the softmax, not the
+// products. IN_BF16: q, k, v are bf16; OUT_F32: o is fp32 (else the input
+// type).
+template <int D, bool IN_BF16, bool OUT_F32>
+__global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   constexpr int TK = 32;
   __shared__ float sK[TK][D];
   __shared__ float sV[TK][D];
@@ -453,14 +457,12 @@ __global__ __launch_bounds__(128) void fwd_f32_kernel(FwdArgs a) {
   const int64_t i = (blockIdx.x % nqb) * 128 + tid;
   for (int t = tid; t < 256; t += 128)
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
-  const float* qh = reinterpret_cast<const float*>(a.q) + (int64_t)h * a.Sq * D;
-  const float* kh = reinterpret_cast<const float*>(a.k) + (int64_t)h * a.Sk * D;
-  const float* vh = reinterpret_cast<const float*>(a.v) + (int64_t)h * a.Sk * D;
+  const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
   const bool ok = i < a.Sq;
   float qv[D], acc[D];
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    qv[c] = ok ? qh[i * D + c] * a.scale : 0.0f;
+    qv[c] = ok ? load_elem<IN_BF16>(a.q, hq + i * D + c) * a.scale : 0.0f;
     acc[c] = 0.0f;
   }
   const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
@@ -470,8 +472,8 @@ __global__ __launch_bounds__(128) void fwd_f32_kernel(FwdArgs a) {
     for (int t = tid; t < TK * D; t += 128) {
       const int r = t / D, c = t % D;
       const bool in = j0 + r < a.Sk;
-      sK[r][c] = in ? kh[(j0 + r) * D + c] : 0.0f;
-      sV[r][c] = in ? vh[(j0 + r) * D + c] : 0.0f;
+      sK[r][c] = in ? load_elem<IN_BF16>(a.k, hk + (j0 + r) * D + c) : 0.0f;
+      sV[r][c] = in ? load_elem<IN_BF16>(a.v, hk + (j0 + r) * D + c) : 0.0f;
     }
     __syncthreads();
     if (!ok) continue;
@@ -504,9 +506,15 @@ __global__ __launch_bounds__(128) void fwd_f32_kernel(FwdArgs a) {
     lse_merge_weights(a.lse[(int64_t)h * a.Sq + i], lse_out, wo, wb, lse_out);
     inv *= wb;
   }
-  float* op = reinterpret_cast<float*>(a.o) + ((int64_t)h * a.Sq + i) * D;
+  if constexpr (IN_BF16 && !OUT_F32) {
+    uint16_t* op = reinterpret_cast<uint16_t*>(a.o) + hq + i * D;
 #pragma unroll
-  for (int c = 0; c < D; ++c) op[c] = wo != 0.0f ? fmaf(op[c], wo, acc[c] * inv) : acc[c] * inv;
+    for (int c = 0; c < D; ++c) op[c] = f2bf(acc[c] * inv);
+  } else {
+    float* op = reinterpret_cast<float*>(a.o) + hq + i * D;
+#pragma unroll
+    for (int c = 0; c < D; ++c) op[c] = wo != 0.0f ? fmaf(op[c], wo, acc[c] * inv) : acc[c] * inv;
+  }
   a.lse[(int64_t)h * a.Sq + i] = lse_out;
 }
 
@@ -525,20 +533,28 @@ hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t s) {
 }
 
 template <int D>
-hipError_t launch_fwd_f32(const FwdArgs& a, hipStream_t s) {
-  const int64_t nqb = (a.Sq + 127) / 128;
-  hipLaunchKernelGGL((fwd_f32_kernel<D>), dim3((unsigned)(nqb * a.H)), dim3(128), 0, s, a);
+hipError_t launch_fwd_valu(const FwdArgs& a, bool bf16, bool out_f32, hipStream_t s) {
+  const dim3 grid((unsigned)((a.Sq + 127) / 128 * a.H));
+  if (!bf16)
+    hipLaunchKernelGGL((fwd_valu_kernel<D, false, true>), grid, dim3(128), 0, s, a);
+  else if (out_f32)
+    hipLaunchKernelGGL((fwd_valu_kernel<D, true, true>), grid, dim3(128), 0, s, a);
+  else
+    hipLaunchKernelGGL((fwd_valu_kernel<D, true, false>), grid, dim3(128), 0, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStream_t s) {
-  if (bf16) {
-    if (d == 64) return out_f32 ? launch_fwd_bf16<64, true>(a, s) : launch_fwd_bf16<64, false>(a, s);
-    return out_f32 ? launch_fwd_bf16<32, true>(a, s) : launch_fwd_bf16<32, false>(a, s);
+  if (bf16 && d == 64) return out_f32 ? launch_fwd_bf16<64, true>(a, s) : launch_fwd_bf16<64, false>(a, s);
+  if (bf16 && d == 32) return out_f32 ? launch_fwd_bf16<32, true>(a, s) : launch_fwd_bf16<32, false>(a, s);
+  switch (d) {
+    case 8: return launch_fwd_valu<8>(a, bf16, out_f32, s);
+    case 16: return launch_fwd_valu<16>(a, bf16, out_f32, s);
+    case 32: return launch_fwd_valu<32>(a, bf16, out_f32, s);
+    default: return launch_fwd_valu<64>(a, bf16, out_f32, s);
   }
-  return d == 64 ? launch_fwd_f32<64>(a, s) : launch_fwd_f32<32>(a, s);
 }
 
 }  // namespace gt

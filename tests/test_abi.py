@@ -99,7 +99,7 @@ def _bwd_batch(**kw):
     (dict(B=0), INVALID), (dict(bs=-16), INVALID), (dict(dt=None), INVALID),
     (dict(do=None), INVALID), (dict(ws=None), WORKSPACE),
     (dict(wsb=gt.lib().gt_attn_bwd_workspace_size(2, 100, 64, BF16)), WORKSPACE),  # sized for one graph
-    (dict(d=16), UNSUPPORTED), (dict(dq=MIS), INVALID),
+    (dict(d=24), UNSUPPORTED), (dict(dq=MIS), INVALID),
 ])
 def test_bwd_batch_validation(kw, code):
     assert _bwd_batch(**kw) == code
@@ -119,7 +119,7 @@ def _ring(entry="gt_attn_ring_step", **kw):
     (dict(ld=191), INVALID),                      # ld < col_off + Sk
     (dict(k=None), INVALID), (dict(v=None), INVALID), (dict(spd=None), INVALID),
     (dict(q=None), INVALID), (dict(o=None), INVALID), (dict(lse=None), INVALID),
-    (dict(table=None), INVALID), (dict(nb=300), INVALID), (dict(d=16), UNSUPPORTED),
+    (dict(table=None), INVALID), (dict(nb=300), INVALID), (dict(d=24), UNSUPPORTED),
     (dict(scale=0.0), INVALID), (dict(k=MIS), INVALID),
 ])
 @pytest.mark.parametrize("entry", ["gt_attn_ring_step", "gt_attn_ring_step_acc"])
@@ -180,7 +180,7 @@ def _bwd_ring(**kw):
     (dict(dt=None), INVALID), (dict(k=None), INVALID), (dict(v=None), INVALID),
     (dict(spd=None), INVALID), (dict(dk=None), INVALID), (dict(dv=None), INVALID),
     (dict(nb=0), INVALID), (dict(nb=257), INVALID), (dict(scale=float("inf")), INVALID),
-    (dict(d=16), UNSUPPORTED), (dict(dtype=3), UNSUPPORTED),
+    (dict(d=24), UNSUPPORTED), (dict(dtype=3), UNSUPPORTED),
     (dict(q=MIS), INVALID), (dict(do=MIS), INVALID), (dict(dq=MIS), INVALID), (dict(dk=MIS), INVALID),
     (dict(ws=None), WORKSPACE), (dict(wsb=0), WORKSPACE), (dict(ws=FAKE + 16), WORKSPACE),
 ])
@@ -208,7 +208,7 @@ def test_bwd_ring_workspace_size():
 @pytest.mark.parametrize("kw,code", [
     (dict(P=0), INVALID), (dict(H=0), INVALID), (dict(S=0), INVALID), (dict(op=None), INVALID),
     (dict(lp=None), INVALID), (dict(o=None), INVALID), (dict(l=None), INVALID),
-    (dict(d=8), UNSUPPORTED), (dict(dt=5), UNSUPPORTED), (dict(op=MIS), INVALID),
+    (dict(d=12), UNSUPPORTED), (dict(dt=5), UNSUPPORTED), (dict(op=MIS), INVALID),
 ])
 def test_merge_validation(kw, code):
     a = dict(op=FAKE, lp=FAKE, P=8, o=FAKE, l=FAKE, H=8, S=1000, d=64, dt=BF16)

@@ -66,7 +66,7 @@ def test_tiny_workload_fp32():
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
-@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("d", [8, 16, 32, 64])
 @pytest.mark.parametrize("N", [1, 7, 33, 100, 1000])
 def test_ragged_sizes(N, d, dt):
     """Ragged N (not a tile multiple), asymmetric random spd with buckets past
@@ -105,16 +105,18 @@ def test_masked_rows_and_neg_inf_table(dt):
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
-@pytest.mark.parametrize("Sq,Sk,row_off,col_off,ld", [
-    (200, 300, 37, 91, 512),      # unaligned slice: byte loads
-    (256, 320, 64, 128, 512),     # 16-byte aligned slice: vector loads
-    (129, 1, 3, 500, 512),        # single key
-    (64, 77, 0, 0, 77),           # ld not a multiple of 16
+@pytest.mark.parametrize("Sq,Sk,row_off,col_off,ld,d", [
+    (200, 300, 37, 91, 512, 64),      # unaligned slice: byte loads
+    (256, 320, 64, 128, 512, 64),     # 16-byte aligned slice: vector loads
+    (129, 1, 3, 500, 512, 64),        # single key
+    (64, 77, 0, 0, 77, 64),           # ld not a multiple of 16
+    (100, 150, 5, 40, 256, 8),        # small head dims (vector-ALU path)
+    (70, 64, 0, 64, 128, 16),
 ])
-def test_ring_step_offsets(Sq, Sk, row_off, col_off, ld, dt):
+def test_ring_step_offsets(Sq, Sk, row_off, col_off, ld, d, dt):
     """One context-parallel step: bias slice spd[row_off + i, col_off + j] of an
     asymmetric spd; partial O (fp32) and LSE against the oracle's ring step."""
-    H, d, nb = 3, 64, 12
+    H, nb = 3, 12
     g = np.random.default_rng(Sq + Sk)
     rows = row_off + Sq
     spd = g.integers(0, nb + 2, size=(rows, ld)).astype(np.uint8)
@@ -125,7 +127,7 @@ def test_ring_step_offsets(Sq, Sk, row_off, col_off, ld, dt):
         q, k, v = (synth.round_bf16(x) for x in (q, k, v))
     table = (g.standard_normal((H, nb)) * 0.5).astype(np.float32)
     td = tdtype(dt)
-    say(f"ring step {dt} Sq={Sq} Sk={Sk} row_off={row_off} col_off={col_off} ld={ld}")
+    say(f"ring step {dt} Sq={Sq} Sk={Sk} row_off={row_off} col_off={col_off} ld={ld} d={d}")
     o, l = gt.gt_attn_ring_step(to_dev(q, td), to_dev(k, td), to_dev(v, td),
                                 to_dev(spd, torch.uint8), row_off, col_off, to_dev(table),
                                 scale=0.125)
@@ -268,6 +270,8 @@ def test_ring_step_acc_from_empty_state_and_empty_block(dt):
     (4, 200, 64, "per_graph"),      # ragged tiles, unaligned spd rows
     (3, 256, 32, "per_graph_t"),    # aligned, with per-graph transposes
     (5, 96, 64, "shared"),          # one spd for every graph (stride 0)
+    (16, 65, 8, "per_graph"),       # the paper's head dim: 8 heads over 64 features
+    (6, 128, 16, "per_graph_t"),
 ])
 def test_batch_of_graphs(B, N, d, spd_kind, dt):
     """A batch of graphs, each with its own spd, sharing the table: every

@@ -86,7 +86,7 @@ def test_bwd_ring_step_offsets(Sq, Sk, row_off, col_off, ld, dt):
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
-@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("d", [8, 16, 32, 64])
 def test_bwd_ring_step_masked_rows(d, dt):
     """Rows whose every bucket is -inf have LSE = -inf over the whole ring:
     P = 0, so they add nothing (their dQ accumulator rows stay as they were)."""
