@@ -11,7 +11,10 @@
 // the query-stationary dQ kernel (bwd_dkdv.hip, bwd_dq.hip for bf16; the
 // fp32 kernels below). Splitting dQ from dK/dV recomputes two products but
 // needs no atomics on dQ.
+#include <type_traits>
+
 #include "common.hpp"
+#include "dtable.hpp"
 #include "kernels.hpp"
 
 namespace gt {
@@ -132,19 +135,25 @@ __device__ __forceinline__ void store_grad(void* base, int64_t idx, float x, boo
 
 template <int D, bool IN_BF16>
 __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
-  constexpr int TK = 32;
-  __shared__ float sK[TK][D];
-  __shared__ float sV[TK][D];
+  constexpr int TK = 64;             // keys per LDS tile, in blocks of 16
+  __shared__ __attribute__((aligned(16))) float sK[TK][D];
+  __shared__ __attribute__((aligned(16))) float sV[TK][D];
   __shared__ float sT[256];
-  __shared__ float sH[256];
+  // dtable histogram: bf16 inputs add in fixed point (dtable.hpp), fp32
+  // inputs in fp32 (slow LDS float atomics, but no quantisation of dS)
+  using HistT = std::conditional_t<IN_BF16, unsigned long long, float>;
+  __shared__ HistT sH[256];
+  __shared__ float sRed[3][2];
   const int tid = threadIdx.x;
   const int64_t nqb = (a.Sq + 127) / 128;
   const int h = (int)(blockIdx.x / nqb);
   const int64_t i = (blockIdx.x % nqb) * 128 + tid;
   for (int t = tid; t < 256; t += 128) {
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
-    sH[t] = 0.0f;
+    sH[t] = HistT(0);
   }
+  const int fexp = IN_BF16 ? hist_exponent<2>(a, h, sRed) : 0;
+  const float sF = ldexpf(1.0f, fexp);
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
   const bool ok = i < a.Sq;
   float qv[D], dov[D], acc[D];
@@ -168,19 +177,36 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
     __syncthreads();
     if (!ok || L == -INFINITY) continue;
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
-    for (int r = 0; r < nk; ++r) {
-      float s = 0.0f, dp = 0.0f;
-#pragma unroll
-      for (int c = 0; c < D; ++c) {
-        s = fmaf(qv[c], sK[r][c], s);
-        dp = fmaf(dov[c], sV[r][c], dp);
+    // blocks of 16 keys: their spd bytes in one load
+    for (int r0 = 0; r0 < nk; r0 += 16) {
+      uint32_t w[4];
+      if (a.spd_vec && r0 + 16 <= nk) {
+        const uint4 v4 = *reinterpret_cast<const uint4*>(srow + j0 + r0);
+        w[0] = v4.x; w[1] = v4.y; w[2] = v4.z; w[3] = v4.w;
+      } else {
+        load_spd16_bytes(srow, j0 + r0, a.Sk, w);
       }
-      const uint32_t b = srow[j0 + r];
-      const float p = expf(s + sT[b] - L);
-      const float ds = p * (dp - dlt);
+      const int nr = nk - r0 < 16 ? nk - r0 : 16;
+      for (int r = 0; r < nr; ++r) {
+        const int key = r0 + r;
+        float sc = 0.0f, dp = 0.0f;
 #pragma unroll
-      for (int c = 0; c < D; ++c) acc[c] = fmaf(ds, sK[r][c], acc[c]);
-      if (b < (uint32_t)a.n_buckets) atomicAdd(&sH[b], ds);
+        for (int c = 0; c < D; ++c) {
+          sc = fmaf(qv[c], sK[key][c], sc);
+          dp = fmaf(dov[c], sV[key][c], dp);
+        }
+        const uint32_t b = (w[r >> 2] >> (8 * (r & 3))) & 0xffu;
+        const float p = exp2_fast((sc + sT[b] - L) * kLog2e);
+        const float ds = p * (dp - dlt);
+#pragma unroll
+        for (int c = 0; c < D; ++c) acc[c] = fmaf(ds, sK[key][c], acc[c]);
+        if (b < (uint32_t)a.n_buckets) {
+          if constexpr (IN_BF16)
+            atomicAdd(&sH[b], (unsigned long long)(long long)round_to_int(ds * sF));
+          else
+            atomicAdd(&sH[b], ds);
+        }
+      }
     }
   }
   if (ok) {
@@ -188,8 +214,13 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
     for (int c = 0; c < D; ++c) store_grad<D, IN_BF16>(a.dq, hq + i * D + c, acc[c] * a.scale, a.accumulate);
   }
   __syncthreads();
-  for (int t = tid; t < a.n_buckets; t += 128)
-    if (sH[t] != 0.0f) atomicAdd(&a.dtable[(int64_t)table_row(a, h) * a.n_buckets + t], sH[t]);
+  float* dth = a.dtable + (int64_t)table_row(a, h) * a.n_buckets;
+  if constexpr (IN_BF16) {
+    flush_hist<1>(sH, a.n_buckets, fexp, dth, 128);
+  } else {
+    for (int t = tid; t < a.n_buckets; t += 128)
+      if (sH[t] != 0.0f) atomicAdd(&dth[t], sH[t]);
+  }
 }
 
 template <int D, bool IN_BF16>
@@ -240,7 +271,7 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
         s = fmaf(sQ[r][c], kv[c], s);
         dp = fmaf(sO[r][c], vv[c], dp);
       }
-      const float p = expf(s + sT[sbase[(i0 + r) * a.ld_spd + j]] - sL[r]);
+      const float p = exp2_fast((s + sT[sbase[(i0 + r) * a.ld_spd + j]] - sL[r]) * kLog2e);
       const float ds = p * (dp - sD[r]);
 #pragma unroll
       for (int c = 0; c < D; ++c) {

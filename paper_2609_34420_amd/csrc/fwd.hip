@@ -447,9 +447,9 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
 // type).
 template <int D, bool IN_BF16, bool OUT_F32>
 __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
-  constexpr int TK = 32;
-  __shared__ float sK[TK][D];
-  __shared__ float sV[TK][D];
+  constexpr int TK = 64;             // keys per LDS tile, in blocks of 16
+  __shared__ __attribute__((aligned(16))) float sK[TK][D];
+  __shared__ __attribute__((aligned(16))) float sV[TK][D];
   __shared__ float sT[256];
   const int tid = threadIdx.x;
   const int64_t nqb = (a.Sq + 127) / 128;
@@ -466,7 +466,7 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
     acc[c] = 0.0f;
   }
   const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
-  float m = -INFINITY, l = 0.0f;
+  float m = -INFINITY, l = 0.0f;     // running max (natural units) and sum relative to it
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
     __syncthreads();
     for (int t = tid; t < TK * D; t += 128) {
@@ -478,23 +478,40 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
     __syncthreads();
     if (!ok) continue;
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
-    for (int r = 0; r < nk; ++r) {
-      float s = 0.0f;
+    // blocks of 16 keys: their spd bytes in one load, one running-max update
+    for (int r0 = 0; r0 < nk; r0 += 16) {
+      uint32_t w[4];
+      if (a.spd_vec && r0 + 16 <= nk) {
+        const uint4 v4 = *reinterpret_cast<const uint4*>(srow + j0 + r0);
+        w[0] = v4.x; w[1] = v4.y; w[2] = v4.z; w[3] = v4.w;
+      } else {
+        load_spd16_bytes(srow, j0 + r0, a.Sk, w);
+      }
+      float sc[16];
+      float bm = -INFINITY;
 #pragma unroll
-      for (int c = 0; c < D; ++c) s = fmaf(qv[c], sK[r][c], s);
-      s += sT[srow[j0 + r]];
-      if (s == -INFINITY) continue;
-      if (s > m) {
-        const float alpha = (m == -INFINITY) ? 0.0f : expf(m - s);
+      for (int r = 0; r < 16; ++r) {
+        float x = sT[(w[r >> 2] >> (8 * (r & 3))) & 0xffu];
+#pragma unroll
+        for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[r0 + r][c], x);
+        sc[r] = (r0 + r < nk) ? x : -INFINITY;
+        bm = fmaxf(bm, sc[r]);
+      }
+      if (bm == -INFINITY) continue;
+      if (bm > m) {
+        const float alpha = (m == -INFINITY) ? 0.0f : exp2_fast((m - bm) * kLog2e);
         l *= alpha;
 #pragma unroll
         for (int c = 0; c < D; ++c) acc[c] *= alpha;
-        m = s;
+        m = bm;
       }
-      const float p = expf(s - m);
-      l += p;
 #pragma unroll
-      for (int c = 0; c < D; ++c) acc[c] = fmaf(p, sV[r][c], acc[c]);
+      for (int r = 0; r < 16; ++r) {
+        const float p = exp2_fast((sc[r] - m) * kLog2e);
+        l += p;
+#pragma unroll
+        for (int c = 0; c < D; ++c) acc[c] = fmaf(p, sV[r0 + r][c], acc[c]);
+      }
     }
   }
   if (!ok) return;
