@@ -12,11 +12,19 @@
 //
 // Bias and table gradient: the table (times log2 e) is replicated in LDS
 // (copy = lane & 31 when there are at most 128 buckets, else lane & 15) and
-// the fixed-point bucket histogram of dS (dtable.hpp) has the same layout, so
+// the bucket histogram has the same layout, so
 // one address register serves the bias read and the gradient add. The
-// histogram's power-of-two scale 2^F enters for free through the V operand
-// of dP (and the dP accumulator start), so dS arrives already scaled; dK
-// takes 2^-F in its final multiply.
+// histogram is fixed point: LDS float atomics are slow on this hardware,
+// 64-bit integer adds are not. dS is accumulated as round(dS * 2^F), where
+// the power-of-two scale per head keeps every term below 2^30 in magnitude:
+// |dS_ij| <= |dO_i . V_j - Dlt_i| <= max_i |dO_i| max_j |V_j| + max_i |Dlt_i|
+// (P_ij <= 1, Cauchy-Schwarz), and the prepare stage records block maxima of
+// |dO_i|, |V_j| and |Dlt_i|. Dlt enters on its own because in a ring step O
+// mixes the values of every key block, not only of the keys at hand. The scale enters for free through the
+// V operand of dP (and the dP accumulator start), so dS arrives already
+// scaled; dK takes 2^-F in its final multiply. Sums of up to 2^32 terms fit
+// in 64 bits. The histogram is flushed once per workgroup, converted back
+// to fp32, with one global atomic per bucket.
 //
 // Query tiles (Q and dO row-major, statistics) are double buffered in LDS;
 // Q^T and dO^T are read with transposing LDS reads. The next tile's global
@@ -25,7 +33,6 @@
 #include <type_traits>
 
 #include "common.hpp"
-#include "dtable.hpp"
 #include "kernels.hpp"
 #include "stage.hpp"
 
@@ -146,6 +153,12 @@ __device__ __forceinline__ void load_bytes(const uint8_t* spd_cols, int64_t ld, 
       b[r] = (uint8_t)buf_u8(rs, (uint32_t)((row - ib) * ld) + key_off, 0u);
     }
   }
+}
+
+__device__ __forceinline__ int round_to_int(float x) {
+  int r;
+  asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(r) : "v"(x));   // floor(x + 0.5)
+  return r;
 }
 
 // The 128-bucket layout is used only when n_buckets <= 127, so bucket 127
@@ -440,7 +453,45 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
     hist[t] = 0ull;
   }
 
-  const int fexp = hist_exponent<kNW>(a, h, red);
+  // Fixed-point exponent F of this head: (max|dO| max|V| + max|Dlt|) 2^F
+  // <= 2^30 (a 1.5 % margin covers the rounding of P and of the products).
+  {
+    const int64_t nblk = ((a.Sq > a.Sk ? a.Sq : a.Sk) + 255) / 256;
+    const float* nm = a.nmax + (int64_t)h * nblk * 4;
+    float md = 0.0f, mv = 0.0f, ml = 0.0f;
+    for (int64_t t = tid; t < nblk; t += kThreads) {
+      md = fmaxf(md, nm[4 * t]);
+      mv = fmaxf(mv, nm[4 * t + 1]);
+      ml = fmaxf(ml, nm[4 * t + 2]);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      md = fmaxf(md, __shfl_xor(md, off));
+      mv = fmaxf(mv, __shfl_xor(mv, off));
+      ml = fmaxf(ml, __shfl_xor(ml, off));
+    }
+    if ((tid & 63) == 0) {
+      red[0][wave] = md;
+      red[1][wave] = mv;
+      red[2][wave] = ml;
+    }
+  }
+  __syncthreads();
+  float md = red[0][0], mv = red[1][0], ml = red[2][0];
+#pragma unroll
+  for (int w = 1; w < kNW; ++w) {
+    md = fmaxf(md, red[0][w]);
+    mv = fmaxf(mv, red[1][w]);
+    ml = fmaxf(ml, red[2][w]);
+  }
+  const float bound = 1.015f * (sqrtf(md) * sqrtf(mv) + ml);
+  int fexp = 40;
+  if (bound > 0.0f && bound < INFINITY) {
+    int e;
+    frexpf(bound, &e);                 // bound < 2^e
+    fexp = 30 - e;
+    fexp = fexp > 40 ? 40 : (fexp < -100 ? -100 : fexp);
+  }
 
   if ((kblk + 1) * kBK <= a.Sk)
     dkdv_main<D, NB, false, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
@@ -448,7 +499,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
     dkdv_main<D, NB, true, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
 
   __syncthreads();
-  flush_hist<CPY>(hist, a.n_buckets, fexp, a.dtable + (int64_t)table_row(a, h) * a.n_buckets, kThreads);
+  const double unscale = ldexp(1.0, -fexp);
+  for (int bkt = tid; bkt < a.n_buckets; bkt += kThreads) {
+    long long t = 0;
+#pragma unroll
+    for (int c = 0; c < CPY; ++c) t += (long long)hist[bkt * CPY + ((c + bkt) & (CPY - 1))];
+    if (t != 0) atomicAdd(&a.dtable[(int64_t)table_row(a, h) * a.n_buckets + bkt], (float)((double)t * unscale));
+  }
 }
 
 }  // namespace
