@@ -8,9 +8,9 @@
 //
 // Launch order: prepare (lse2 = LSE log2 e, +inf for an empty row so that
 // P = 0; Dlt; dtable = 0), then the key-stationary dK/dV/dtable kernel and
-// the query-stationary dQ kernel (bwd_dkdv.hip, bwd_dq.hip for bf16; the
-// fp32 kernels below). Splitting dQ from dK/dV recomputes two products but
-// needs no atomics on dQ.
+// the query-stationary dQ kernel (bwd_dkdv.hip, bwd_dq.hip for bf16 with
+// d >= 32; the vector-ALU kernels below for fp32 and for d < 32). Splitting dQ
+// from dK/dV recomputes two products but needs no atomics on dQ.
 #include <type_traits>
 
 #include "common.hpp"
@@ -20,8 +20,6 @@
 namespace gt {
 
 namespace {
-
-constexpr int kWaves = 4;
 
 // ---------------------------------------------------------------------------
 // Preprocess: lse2, Dlt; dtable = 0.
