@@ -49,6 +49,10 @@ def parse():
     p.add_argument("--cpu-rows", type=int, default=512,
                    help="query rows of the oracle CPU baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--hbm-probe", action="store_true",
+                   help="also time one read-only pass over the resident spd matrix (a torch "
+                        "reduction over it as int64 words: the achievable rate for the spd "
+                        "stream) and add it to the line")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run one plain 1 GiB device copy before the timed region (its "
                         "FETCH_SIZE / WRITE_SIZE counters calibrate the kernels')")
@@ -116,6 +120,23 @@ def run_gpu(w, args, dev):
             if ev is not None:
                 ev[2 + ph].record(stream)
 
+    probe = None
+    if args.hbm_probe:
+        spd = x["spd"]
+        words = spd.view(-1).view(torch.int64)     # the same bytes, 8 to a word
+        torch.sum(words)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(5):
+            torch.sum(words)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / 5
+        probe = {"what": "torch.sum over the spd matrix read as int64 words (read-only pass)",
+                 "bytes": spd.numel(), "ms": ms, "GB_per_s": spd.numel() / (ms * 1e-3) / 1e9}
+        log(f"HBM probe: {spd.numel() / 1e9:.2f} GB read in {ms:.3f} ms = {probe['GB_per_s']:.0f} GB/s")
+
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -147,7 +168,7 @@ def run_gpu(w, args, dev):
     log(f"timed {args.steps} steps: {total_ms:.1f} ms (events), {wall * 1e3:.1f} ms (wall)")
     for kname, v in per.items():
         log(f"  {kname:9s} mean {sum(v) / len(v):9.3f} ms  min {min(v):9.3f} ms")
-    return total_ms, wall, per
+    return total_ms, wall, per, probe
 
 
 _KERNEL_FILES = {"fwd": "fwd_bf16_kernel", "bwd_dkdv": "bwd_dkdv_bf16_kernel",
@@ -225,7 +246,7 @@ def main():
     w = synth.workload(args.workload)
     dev = "cuda:0"
     torch.cuda.set_device(0)
-    total_ms, wall, per = run_gpu(w, args, dev)
+    total_ms, wall, per, probe = run_gpu(w, args, dev)
     K = args.steps
     ms = total_ms / K
     flop = w.flops_fwd_bwd
@@ -274,6 +295,8 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if probe is not None:
+        out["hbm_probe"] = probe
     print(json.dumps(out), flush=True)
 
 
