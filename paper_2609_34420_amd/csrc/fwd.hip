@@ -448,7 +448,10 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
 template <int D, bool IN_BF16, bool OUT_F32>
 __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   constexpr int TK = 64;             // keys per LDS tile, in blocks of 16
-  __shared__ __attribute__((aligned(16))) float sK[TK][D];
+  constexpr int DP = D / 2;          // bf16 pairs per row
+  // K as fp32 (fp32 inputs) or as packed bf16 pairs for v_dot2 (bf16 inputs)
+  __shared__ __attribute__((aligned(16))) float sK[IN_BF16 ? 1 : TK][D];
+  __shared__ __attribute__((aligned(16))) uint32_t sKp[IN_BF16 ? TK : 1][DP];
   __shared__ __attribute__((aligned(16))) float sV[TK][D];
   __shared__ float sT[256];
   const int tid = threadIdx.x;
@@ -460,11 +463,15 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
   const bool ok = i < a.Sq;
   float qv[D], acc[D];
+  uint32_t qp[DP];                   // bf16 inputs: the query row as packed pairs
 #pragma unroll
   for (int c = 0; c < D; ++c) {
     qv[c] = ok ? load_elem<IN_BF16>(a.q, hq + i * D + c) * a.scale : 0.0f;
     acc[c] = 0.0f;
   }
+#pragma unroll
+  for (int c = 0; c < DP; ++c)
+    qp[c] = (IN_BF16 && ok) ? reinterpret_cast<const uint32_t*>(a.q)[(hq + i * D) / 2 + c] : 0u;
   const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
   float m = -INFINITY, l = 0.0f;     // running max (natural units) and sum relative to it
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
@@ -472,8 +479,14 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
     for (int t = tid; t < TK * D; t += 128) {
       const int r = t / D, c = t % D;
       const bool in = j0 + r < a.Sk;
-      sK[r][c] = in ? load_elem<IN_BF16>(a.k, hk + (j0 + r) * D + c) : 0.0f;
+      if constexpr (!IN_BF16) sK[r][c] = in ? load_elem<false>(a.k, hk + (j0 + r) * D + c) : 0.0f;
       sV[r][c] = in ? load_elem<IN_BF16>(a.v, hk + (j0 + r) * D + c) : 0.0f;
+    }
+    if constexpr (IN_BF16) {
+      for (int t = tid; t < TK * DP; t += 128) {
+        const int r = t / DP, c = t % DP;
+        sKp[r][c] = (j0 + r < a.Sk) ? reinterpret_cast<const uint32_t*>(a.k)[(hk + (j0 + r) * D) / 2 + c] : 0u;
+      }
     }
     __syncthreads();
     if (!ok) continue;
@@ -492,8 +505,12 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float x = sT[(w[r >> 2] >> (8 * (r & 3))) & 0xffu];
+        if constexpr (IN_BF16) {
+          x = fmaf(dot_bf16<DP>(qp, sKp[r0 + r], 0.0f), a.scale, x);
+        } else {
 #pragma unroll
-        for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[r0 + r][c], x);
+          for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[r0 + r][c], x);
+        }
         sc[r] = (r0 + r < nk) ? x : -INFINITY;
         bm = fmaxf(bm, sc[r]);
       }
