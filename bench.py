@@ -235,7 +235,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the context-parallel "
+        print(json.dumps({"error": "this benchmark runs on one GPU only; the context-parallel "
                           "ring across GPUs is not built (see the single-GPU ring step), "
                           f"asked for --gpus {args.gpus} / WORLD_SIZE {world}"}))
         sys.exit(2)

@@ -52,7 +52,7 @@ typedef enum { GT_F32 = 0, GT_BF16 = 1 } gt_dtype_t;
 typedef enum {
   GT_OK = 0,
   GT_ERR_INVALID = 1,     /* null pointer, bad size, bad offset, bad scale   */
-  GT_ERR_UNSUPPORTED = 2, /* head dim or dtype this build has no kernel for  */
+  GT_ERR_UNSUPPORTED = 2, /* head dim or dtype the library has no kernel for */
   GT_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required      */
   GT_ERR_LAUNCH = 4       /* the HIP runtime rejected a kernel launch        */
 } gt_status_t;

@@ -120,7 +120,7 @@ def test_ba16k_full_size():
     _free()
 
 
-def test_headline_sbm128k_full_size():
+def test_sbm128k_full_size():
     """N=131072, H=8, d=64 bf16, clustered planted-partition spd (clip 62,
     unreachable 63; 17.2 GB in HBM)."""
     w = synth.workload("sbm128k")
