@@ -198,11 +198,12 @@ def test_context_parallel_ring_backward(N, bounds, dt):
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
-@pytest.mark.parametrize("n_reg,n_super,bounds", [
-    (900, 37, [0, 300, 612, 900]),       # uneven shards, unaligned spd columns
-    (960, 64, [0, 320, 640, 960]),       # N = 1024: 16-byte aligned slices
+@pytest.mark.parametrize("n_reg,n_super,bounds,d", [
+    (900, 37, [0, 300, 612, 900], 64),       # uneven shards, unaligned spd columns
+    (960, 64, [0, 320, 640, 960], 64),       # N = 1024: 16-byte aligned slices
+    (500, 1, [0, 130, 250, 380, 500], 8),    # the paper's end-to-end shape: one global node, d = 8
 ])
-def test_context_parallel_super_nodes(n_reg, n_super, bounds, dt):
+def test_context_parallel_super_nodes(n_reg, n_super, bounds, d, dt):
     """Super nodes (Section III-A-1 parts 1-2): each rank's query shard is
     its regular rows plus every super-node row, with those spd rows only.
     Forward: the running merge over the P regular KV blocks in ring order and
@@ -210,7 +211,7 @@ def test_context_parallel_super_nodes(n_reg, n_super, bounds, dt):
     super rows' dO (zero on the other ranks), dK/dV per block, the super
     block's accumulated by every rank. Both equal the unsharded oracle over
     all N = N' + N_s nodes, and every rank computes the same super rows."""
-    H, d, nb = 2, 64, 16
+    H, nb = 2, 16
     N = n_reg + n_super
     q, k, v, do, table, spd = _ring_case(H, N, d, nb, seed=N + 1, dt=dt)
     scale = 1.0 / math.sqrt(d)
