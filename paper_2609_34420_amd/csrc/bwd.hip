@@ -31,65 +31,69 @@ namespace {
 // zeroes dtable unless the call accumulates.
 template <int D, bool BF16>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs a) {
+  // A row is read by TPR consecutive lanes, 16 bytes each, so a wave's loads
+  // cover whole rows contiguously; the block's 256 rows take TPR passes.
+  constexpr int EPC = BF16 ? 8 : 4;          // elements per 16-byte chunk
+  constexpr int TPR = D / EPC;               // lanes per row
+  constexpr int RPP = 256 / TPR;             // rows per pass
   __shared__ float red[3][4];
   const int h = blockIdx.y;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int sub = threadIdx.x % TPR;
   if (blockIdx.x == 0 && blockIdx.y == 0 && !a.accumulate) {
     for (int t = threadIdx.x; t < a.hpb * a.n_buckets; t += 256) a.dtable[t] = 0.0f;
   }
+  // dot products of one 16-byte chunk
+  auto chunk_dot = [](const void* x, const void* y, float& xy, float& yy) {
+    if constexpr (BF16) {
+      const uint4 xv = *reinterpret_cast<const uint4*>(x);
+      const uint4 yv = *reinterpret_cast<const uint4*>(y);
+      const uint16_t* xp = reinterpret_cast<const uint16_t*>(&xv);
+      const uint16_t* yp = reinterpret_cast<const uint16_t*>(&yv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float yf = bf2f(yp[e]);
+        xy = fmaf(bf2f(xp[e]), yf, xy);
+        yy = fmaf(yf, yf, yy);
+      }
+    } else {
+      const float4 xv = *reinterpret_cast<const float4*>(x);
+      const float4 yv = *reinterpret_cast<const float4*>(y);
+      xy = fmaf(xv.x, yv.x, fmaf(xv.y, yv.y, fmaf(xv.z, yv.z, fmaf(xv.w, yv.w, xy))));
+      yy = fmaf(yv.x, yv.x, fmaf(yv.y, yv.y, fmaf(yv.z, yv.z, fmaf(yv.w, yv.w, yy))));
+    }
+  };
+  using T = std::conditional_t<BF16, uint16_t, float>;
   float nd = 0.0f, nv = 0.0f, nl = 0.0f;
-  if (i < a.Sq) {
-    const int64_t row = (int64_t)h * a.Sq + i;
-    float acc = 0.0f;
-    if constexpr (BF16) {
-      const uint16_t* o = reinterpret_cast<const uint16_t*>(a.o) + row * D;
-      const uint16_t* d = reinterpret_cast<const uint16_t*>(a.d_o) + row * D;
 #pragma unroll
-      for (int c = 0; c < D; c += 8) {
-        const uint4 ov = *reinterpret_cast<const uint4*>(o + c);
-        const uint4 dv = *reinterpret_cast<const uint4*>(d + c);
-        const uint16_t* op = reinterpret_cast<const uint16_t*>(&ov);
-        const uint16_t* dp = reinterpret_cast<const uint16_t*>(&dv);
+  for (int pass = 0; pass < TPR; ++pass) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + pass * RPP + threadIdx.x / TPR;
+    float acc = 0.0f, sq = 0.0f, vq = 0.0f, unused = 0.0f;
+    if (i < a.Sq) {
+      const int64_t off = ((int64_t)h * a.Sq + i) * D + sub * EPC;
+      chunk_dot(reinterpret_cast<const T*>(a.o) + off, reinterpret_cast<const T*>(a.d_o) + off, acc, sq);
+    }
+    if (i < a.Sk) {
+      const int64_t off = ((int64_t)h * a.Sk + i) * D + sub * EPC;
+      const T* v = reinterpret_cast<const T*>(a.v) + off;
+      chunk_dot(v, v, unused, vq);
+    }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float x = bf2f(dp[e]);
-          acc = fmaf(bf2f(op[e]), x, acc);
-          nd = fmaf(x, x, nd);
-        }
-      }
-    } else {
-      const float* o = reinterpret_cast<const float*>(a.o) + row * D;
-      const float* d = reinterpret_cast<const float*>(a.d_o) + row * D;
-#pragma unroll
-      for (int c = 0; c < D; ++c) {
-        acc = fmaf(o[c], d[c], acc);
-        nd = fmaf(d[c], d[c], nd);
+    for (int o = TPR / 2; o >= 1; o >>= 1) {
+      acc += __shfl_xor(acc, o);
+      sq += __shfl_xor(sq, o);
+      vq += __shfl_xor(vq, o);
+    }
+    if (i < a.Sq) {
+      const int64_t row = (int64_t)h * a.Sq + i;
+      nd = fmaxf(nd, sq);
+      nl = fmaxf(nl, fabsf(acc));
+      if (sub == 0) {
+        a.dlt[row] = acc;
+        const float L = a.lse[row];
+        a.lse2[row] = (L == -INFINITY) ? INFINITY : L * kLog2e;
       }
     }
-    a.dlt[row] = acc;
-    nl = fabsf(acc);
-    const float L = a.lse[row];
-    a.lse2[row] = (L == -INFINITY) ? INFINITY : L * kLog2e;
-  }
-  if (i < a.Sk) {
-    const int64_t row = (int64_t)h * a.Sk + i;
-    if constexpr (BF16) {
-      const uint16_t* v = reinterpret_cast<const uint16_t*>(a.v) + row * D;
-#pragma unroll
-      for (int c = 0; c < D; c += 8) {
-        const uint4 vv = *reinterpret_cast<const uint4*>(v + c);
-        const uint16_t* vp = reinterpret_cast<const uint16_t*>(&vv);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float y = bf2f(vp[e]);
-          nv = fmaf(y, y, nv);
-        }
-      }
-    } else {
-      const float* v = reinterpret_cast<const float*>(a.v) + row * D;
-#pragma unroll
-      for (int c = 0; c < D; ++c) nv = fmaf(v[c], v[c], nv);
-    }
+    if (i < a.Sk) nv = fmaxf(nv, vq);
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
