@@ -24,6 +24,7 @@ import json
 import math
 import os
 import platform
+import statistics
 import sys
 import time
 from pathlib import Path
@@ -44,7 +45,8 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=5)
     p.add_argument("--warmup", type=int, default=2)
-    p.add_argument("--workload", default="sbm128k")
+    p.add_argument("--workload", default="sbm128k", choices=("sbm128k", "ba16k"),
+                   help="single-layer bf16 workload (the headline is sbm128k)")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--cpu-rows", type=int, default=512,
                    help="query rows of the oracle CPU baseline sample")
@@ -231,6 +233,15 @@ def cpu_baseline(w, args):
                        f"host {platform.processor() or platform.machine()}, os.cpu_count()={os.cpu_count()}")}
 
 
+def graph_label(w) -> str:
+    kind = w.graph[0]
+    if kind == "sbm":
+        return f"clustered planted-partition graph, {w.graph[1]} communities"
+    if kind == "ba":
+        return f"Barabasi-Albert graph, m={w.graph[1]}"
+    return f"Erdos-Renyi graph, average degree {w.graph[1]}"
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -273,7 +284,7 @@ def main():
         cpu = cpu_baseline(w, args)
 
     out = {
-        "metric": "biased-attention fwd+bwd TFLOP/s and % bf16 MFMA peak at N=131072, H=8, d=64",
+        "metric": f"biased-attention fwd+bwd TFLOP/s and % bf16 MFMA peak at N={w.N}, H={w.H}, d={w.d}",
         "value": tflops,
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -286,11 +297,13 @@ def main():
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "pct_of_bf16_peak": 100.0 * tflops * 1e12 / PEAK_BF16,
-        "config": {"workload": f"{w.name}: clustered planted-partition graph, 64 communities, "
-                               f"N={w.N}, H={w.H}, d={w.d}, {w.n_buckets} spd buckets, bf16",
+        "config": {"workload": f"{w.name}: {graph_label(w)}, N={w.N}, H={w.H}, d={w.d}, "
+                               f"{w.n_buckets} spd buckets, bf16",
                    "N": w.N, "H": w.H, "d": w.d, "n_buckets": w.n_buckets,
                    "flop_per_step": flop, "parallelism": "single GPU"},
         "kernel_ms": mean,
+        "step_ms_stats": {"mean": ms, "median": statistics.median(per["step"]),
+                          "min": min(per["step"]), "max": max(per["step"])},
         "wall_ms_per_step": wall * 1e3 / K,
         "roofline": roofline,
         "cpu_baseline": cpu,

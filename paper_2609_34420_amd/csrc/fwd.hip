@@ -178,8 +178,9 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
 }
 
 // VEC: spd rows are 16-byte aligned. FULL: VEC and Sk a multiple of the key
-// tile, so every spd group is loaded whole and no tile needs masking.
-template <int D, bool OUT_F32, bool VEC, bool FULL>
+// tile, so every spd group is loaded whole and no tile needs masking. SKIP:
+// Sq is not a multiple of the workgroup's rows, so some waves may own no row.
+template <int D, bool OUT_F32, bool VEC, bool FULL, bool SKIP>
 __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
@@ -204,6 +205,10 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   const int h = (int)(lid % a.H);
   const int64_t qblk = lid / a.H;
   const int64_t qbase = qblk * BR + (int64_t)wave * 32 * kQB;
+  // A wave whose rows all lie past Sq (short sequences) still takes its
+  // share of the tile copies, spd loads, waits and barriers, but skips the
+  // products and the softmax, leaving its SIMD to the other wave.
+  const bool active = !SKIP || qbase < a.Sq;
 
   fill_lane_table(sTab, a.table + (int64_t)table_row(a, h) * a.n_buckets, a.n_buckets, a.scale, kThreads);
 
@@ -299,7 +304,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
       spd_of(1, wB);
       wait_vmcnt<0>();
       __syncthreads();     // table, and tiles 0..2
-      issue_scores<D>(sTab, wA[0][0], lane4, sK0, off.k, 0, qf[0], s0);
+      if (active) issue_scores<D>(sTab, wA[0][0], lane4, sK0, off.k, 0, qf[0], s0);
     }
     // Tile t from stage S = t % 3 and spd set P = t % 2; units u = (key
     // block, query block) in the order (0,0), (0,1), (1,0), (1,1). The score
@@ -317,6 +322,14 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
       GT_FWD_STAGE(SN, k_n, v_n)
       auto& w = P == 0 ? wA : wB;
       auto& w_n = P == 0 ? wB : wA;
+      if (!active) {
+        // same loads, waits and barrier as the working waves
+        spd_of(t + 2, w);
+        wait_vmcnt<SPD_LOADS + Dma::NLOADS>();
+        __builtin_amdgcn_s_barrier();
+        copy_tile(t + 3, stagec);
+        return;
+      }
       bf16x8 vop[2][NCB];
       f32x16 s1, s2, s3;
       issue_scores<D>(sTab, w[1][0], lane4, k_s, off.k, 0, qf[1], s1);
@@ -373,7 +386,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
       spd_of(t + 2, S == 0 ? w2 : (S == 1 ? w0 : w1));
       sched_fence();
       auto& w = S == 0 ? w0 : (S == 1 ? w1 : w2);
-      fwd_tile<D, MASK>(k_s, v_s, sTab, off, qf, w, lane4, a.Sk - t * kBC, sl2, sm, acc);
+      if (active) fwd_tile<D, MASK>(k_s, v_s, sTab, off, qf, w, lane4, a.Sk - t * kBC, sl2, sm, acc);
       wait_vmcnt<0>();
       __builtin_amdgcn_s_barrier();
     };
@@ -557,12 +570,23 @@ hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t s) {
   constexpr int BR = kWaves * 32 * kQB;
   const int64_t nqb = (a.Sq + BR - 1) / BR;
   const dim3 grid((unsigned)(nqb * a.H));
-  if (a.spd_vec && a.Sk % kBC == 0)
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, true>), grid, dim3(kThreads), 0, s, a);
-  else if (a.spd_vec)
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, false>), grid, dim3(kThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, false, false>), grid, dim3(kThreads), 0, s, a);
+  const bool skip = a.Sq % BR != 0;
+  if (a.spd_vec && a.Sk % kBC == 0) {
+    if (skip)
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, true, true>), grid, dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, true, false>), grid, dim3(kThreads), 0, s, a);
+  } else if (a.spd_vec) {
+    if (skip)
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, false, true>), grid, dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, false, false>), grid, dim3(kThreads), 0, s, a);
+  } else {
+    if (skip)
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, false, false, true>), grid, dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, false, false, false>), grid, dim3(kThreads), 0, s, a);
+  }
   return hipGetLastError();
 }
 
