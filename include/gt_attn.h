@@ -52,7 +52,7 @@ typedef enum { GT_F32 = 0, GT_BF16 = 1 } gt_dtype_t;
 typedef enum {
   GT_OK = 0,
   GT_ERR_INVALID = 1,     /* null pointer, bad size, bad offset, bad scale   */
-  GT_ERR_UNSUPPORTED = 2, /* head dim or dtype the library has no kernel for */
+  GT_ERR_UNSUPPORTED = 2, /* head dim, dtype or spd stride with no kernel    */
   GT_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required      */
   GT_ERR_LAUNCH = 4       /* the HIP runtime rejected a kernel launch        */
 } gt_status_t;
@@ -172,9 +172,10 @@ gt_status_t gt_attn_bwd_phase(int32_t phase,
  *            r = row_off + i, c = col_off + j (typically row_off = 0 and
  *            col_off = the KV block's first global node id)
  *   o_part   [H, Sq, d] fp32 (written)  lse_part [H, Sq] fp32 (written)
- * Sq >= 1, Sk >= 0, row_off >= 0, col_off >= 0, ld_spd >= col_off + Sk.
- * Sk = 0 gives o_part = 0 and lse_part = -inf (k_shard, v_shard, spd may
- * then be NULL). Deterministic. */
+ * Sq >= 1, Sk >= 0, row_off >= 0, col_off >= 0, ld_spd >= col_off + Sk;
+ * ld_spd <= 2^25 - 16 (GT_ERR_UNSUPPORTED otherwise: spd offsets are
+ * 32-bit). Sk = 0 gives o_part = 0 and lse_part = -inf (k_shard, v_shard,
+ * spd may then be NULL). Deterministic. */
 gt_status_t gt_attn_ring_step(const void* q_shard, int64_t Sq,
                               const void* k_shard, const void* v_shard, int64_t Sk,
                               const uint8_t* spd, int64_t ld_spd,
@@ -249,8 +250,8 @@ size_t gt_attn_bwd_ring_workspace_size(int32_t H, int64_t Sq, int64_t Sk, int32_
  *              before the first step of a ring)
  *   workspace  at least gt_attn_bwd_ring_workspace_size(H, Sq, Sk, d, dtype)
  *              bytes of device memory, 256-byte aligned, contents ignored.
- * Sq >= 1, Sk >= 0, row_off >= 0, col_off >= 0, ld_spd >= col_off + Sk; the
- * spd buffer must hold rows row_off .. row_off + Sq - 1. Sk = 0 touches
+ * Sq >= 1, Sk >= 0, row_off >= 0, col_off >= 0, col_off + Sk <= ld_spd <=
+ * 2^25 - 16; the spd buffer must hold rows row_off .. row_off + Sq - 1. Sk = 0 touches
  * nothing (k_blk, v_blk, spd, dk_acc, dv_acc may then be NULL). Steps on one
  * stream are ordered; steps that update the same accumulators must not run
  * concurrently. dtable_acc is updated with floating-point atomics. */

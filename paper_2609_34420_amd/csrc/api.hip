@@ -10,7 +10,10 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int64_t kMaxGrid = 0x7fffffffLL;
-constexpr int64_t kMaxLd = 1LL << 25;   // spd row stride: 32-bit buffer offsets
+// Largest spd row stride (and N): a forward wave reads 64 spd rows through
+// one buffer resource whose byte offsets stop at 2^31 - 1, so 64 ld must
+// stay below 2^31.
+constexpr int64_t kMaxLd = (1LL << 25) - 16;
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 

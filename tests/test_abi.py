@@ -117,6 +117,7 @@ def _ring(entry="gt_attn_ring_step", **kw):
 @pytest.mark.parametrize("kw,code", [
     (dict(Sq=0), INVALID), (dict(Sk=-1), INVALID), (dict(ro=-1), INVALID), (dict(co=-1), INVALID),
     (dict(ld=191), INVALID),                      # ld < col_off + Sk
+    (dict(ld=1 << 25), UNSUPPORTED),
     (dict(k=None), INVALID), (dict(v=None), INVALID), (dict(spd=None), INVALID),
     (dict(q=None), INVALID), (dict(o=None), INVALID), (dict(lse=None), INVALID),
     (dict(table=None), INVALID), (dict(nb=300), INVALID), (dict(d=24), UNSUPPORTED),
@@ -174,7 +175,7 @@ def _bwd_ring(**kw):
 @pytest.mark.parametrize("kw,code", [
     (dict(Sq=0), INVALID), (dict(Sk=-1), INVALID), (dict(ro=-1), INVALID), (dict(co=-1), INVALID),
     (dict(ld=191), INVALID),                      # ld < col_off + Sk
-    (dict(ld=(1 << 25) + 16), UNSUPPORTED),
+    (dict(ld=(1 << 25) + 16), UNSUPPORTED), (dict(ld=1 << 25), UNSUPPORTED),
     (dict(q=None), INVALID), (dict(o=None), INVALID), (dict(lse=None), INVALID),
     (dict(do=None), INVALID), (dict(table=None), INVALID), (dict(dq=None), INVALID),
     (dict(dt=None), INVALID), (dict(k=None), INVALID), (dict(v=None), INVALID),
