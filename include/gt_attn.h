@@ -24,7 +24,9 @@
  *     element is computed in fp32 on the vector ALUs from the bf16 inputs.
  *     GT_F32: all of those tensors are fp32 and computed in fp32. table,
  *     dtable, LSE, partial O and partial LSE are always fp32.
- *   - d (head dim) must be 8, 16, 32 or 64; 1 <= n_buckets <= 256.
+ *   - d (head dim) must be 8, 16, 32 or 64; 1 <= n_buckets <= 256;
+ *     N <= 2^25 - 16 (GT_ERR_UNSUPPORTED otherwise: spd offsets are
+ *     32-bit).
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
  *     stream) and stream-ordered; results are valid once the stream has
  *     synchronised. Calls on different streams do not interfere except
@@ -97,7 +99,7 @@ size_t gt_attn_bwd_workspace_size(int32_t H, int64_t N, int32_t d, gt_dtype_t dt
  *   dQ = scale dS K,  dK = scale dS^T Q,
  *   dtable[h, b] = sum of dS[h, i, j] over pairs with spd[i, j] == b.
  *   spd_t    OPTIONAL [N, N] uint8 transpose of spd (spd_t[j*N + i] ==
- *            spd[i*N + j]), host-owned device memory, read only. The
+ *            spd[i*N + j]), caller-owned device memory, read only. The
  *            key-stationary stage reads spd by columns; with spd_t it reads
  *            rows instead. The shortest-path matrix of an undirected graph is
  *            symmetric: pass spd itself. A directed graph's spd is fixed per
@@ -251,10 +253,11 @@ size_t gt_attn_bwd_ring_workspace_size(int32_t H, int64_t Sq, int64_t Sk, int32_
  *   workspace  at least gt_attn_bwd_ring_workspace_size(H, Sq, Sk, d, dtype)
  *              bytes of device memory, 256-byte aligned, contents ignored.
  * Sq >= 1, Sk >= 0, row_off >= 0, col_off >= 0, col_off + Sk <= ld_spd <=
- * 2^25 - 16; the spd buffer must hold rows row_off .. row_off + Sq - 1. Sk = 0 touches
- * nothing (k_blk, v_blk, spd, dk_acc, dv_acc may then be NULL). Steps on one
- * stream are ordered; steps that update the same accumulators must not run
- * concurrently. dtable_acc is updated with floating-point atomics. */
+ * 2^25 - 16; the spd buffer must hold rows row_off .. row_off + Sq - 1.
+ * Sk = 0 touches nothing (k_blk, v_blk, spd, dk_acc, dv_acc may then be
+ * NULL). Steps on one stream are ordered; steps that update the same
+ * accumulators must not run concurrently. dtable_acc is updated with
+ * floating-point atomics. */
 gt_status_t gt_attn_bwd_ring_step(const void* q_shard, const void* o_shard,
                                   const float* lse_shard, const void* d_o_shard, int64_t Sq,
                                   const void* k_blk, const void* v_blk, int64_t Sk,
