@@ -88,6 +88,68 @@ def test_ragged_sizes(N, d, dt):
             assert np.abs(got[name]).max() <= 1e-6, name
 
 
+@pytest.mark.parametrize("d", [8, 32, 64])
+def test_large_and_rising_scores(d):
+    """Score ranges far past the forward's block-sum limit, bf16 (the
+    matrix-core path at d = 32, 64, the vector-ALU path at d = 8). Head 0:
+    large Q, K and table entries (scores spread over tens of units, so the
+    softmax is nearly one-hot). Head 1: every query's scores rise along the
+    keys (q_i . k_j grows with j, up to about 170), so each new key block
+    moves the row max and the exact rescaling path runs on every block.
+    (The fp32 bars are absolute and sized for scores of order one.) The
+    backward is checked as a function of its inputs, to the relative bar
+    except head 1's dQ on the matrix cores (see below)."""
+    dt = "bf16"
+    H, N, nb = 2, 600, 12
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=40 + d, dt=dt, table_std=4.0, qkv_std=1.5)
+    g = np.random.default_rng(41 + d)
+    u = np.abs(g.standard_normal(d)) + 0.1
+    u /= np.linalg.norm(u)
+    span = 40.0 * math.sqrt(d)                     # scores up to span * scale * max|q|
+    q[1] = u[None, :] * (1.0 + np.abs(g.standard_normal((N, 1))))
+    k[1] = u[None, :] * (span * np.arange(N) / N)[:, None]
+    table[1] *= 0.05
+    v *= 0.25                                      # exact in bf16
+    q, k = synth.round_bf16(q.astype(np.float32)), synth.round_bf16(k.astype(np.float32))
+    scale = 1.0 / math.sqrt(d)
+    say(f"large scores {dt} d={d}")
+    td = tdtype(dt)
+    Q, K, V, dO = (to_dev(x, td) for x in (q, k, v, do))
+    T, S = to_dev(table), to_dev(spd, torch.uint8)
+    O, L = gt.gt_attn_fwd(Q, K, V, S, T, scale=scale)
+    torch.cuda.synchronize()
+    o_r, l_r = oracle.forward(q, k, v, spd, table, scale)
+    assert np.isfinite(to_np(O)).all() and np.isfinite(to_np(L)).all()
+    check_fwd(f"large d={d}", to_np(O), to_np(L), o_r, l_r, dt)
+    # Backward as a function of its inputs: with a nearly one-hot softmax
+    # dS = P (dP - Dlt) nearly cancels, so both sides take the oracle's O
+    # rounded to bf16 (Dlt comes from it) and its LSE.
+    o_in = synth.round_bf16(o_r.astype(np.float32))
+    l_in = l_r.astype(np.float32)
+    gq, gk, gv, gtab = oracle.ring_backward_step(q, o_in, l_in, do, k, v, spd, 0, 0, table, scale)
+    dq, dk, dv, dtab = gt.gt_attn_bwd(Q, K, V, S, T, to_dev(o_in, td), to_dev(l_in), dO, scale=scale)
+    torch.cuda.synchronize()
+    dq = to_np(dq)
+    check_grads(f"large d={d}", dict(dq=dq[:1], dk=to_np(dk), dv=to_np(dv), dtable=to_np(dtab)),
+                dict(dq=gq[:1], dk=gk, dv=gv, dtable=gtab), dt)
+    if d >= 32:
+        # Head 1's dQ_i = scale sum_j dS_ij k_j sums nearly cancelling terms
+        # (parallel keys with norms up to ~230, sum_j dS_ij ~ 0). On the
+        # matrix cores dS is rounded to bf16 (relative 2^-9) before that
+        # product, which moves dQ by up to scale 2^-9 sum_j |dS_ij| |k_jc|;
+        # check it against twice that bound instead of the relative bar.
+        q1, k1, v1, do1 = (x[1].astype(np.float64) for x in (q, k, v, do))
+        bias = np.where(spd < nb, table[1][np.minimum(spd, nb - 1)], 0.0)
+        p1 = np.exp(scale * q1 @ k1.T + bias - l_in[1][:, None].astype(np.float64))
+        ds1 = p1 * (do1 @ v1.T - (do1 * o_in[1]).sum(1)[:, None])
+        bound = 2.0 * scale * 2.0 ** -9 * (np.abs(ds1) @ np.abs(k1)) + 1e-4
+        err = np.abs(dq[1] - gq[1])
+        say(f"large d={d}: head-1 dq max err / bound {(err / bound).max():.3f}")
+        assert (err <= bound).all()
+    else:
+        check_grads(f"large d={d} head 1", dict(dq=dq[1:]), dict(dq=gq[1:]), dt)
+
+
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 def test_masked_rows_and_neg_inf_table(dt):
     """-inf table entries; rows 0..9 only see -inf buckets: O = 0, LSE = -inf,
