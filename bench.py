@@ -43,8 +43,8 @@ def log(msg: str) -> None:
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=5)
-    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="sbm128k", choices=("sbm128k", "ba16k"),
                    help="single-layer bf16 workload (the headline is sbm128k)")
     p.add_argument("--seed", type=int, default=0)
