@@ -302,7 +302,7 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
       hipLaunchKernelGGL((bwd_prep_kernel<D, false>), grid, dim3(256), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if (bf16 && D >= 32) {
+  if (bf16) {     // matrix cores at every head dim (8 and 16 on 32-wide tiles)
     if (phase < 0 || phase == 1) {
       if ((e = launch_dkdv_bf16(a, D, s)) != hipSuccess) return e;
     }

@@ -89,17 +89,18 @@ struct DkdvOffsets {
   }
 };
 
-// A query tile in flight: Q and dO rows (rows past N read as zero) and the
-// statistics of its 64 queries.
-template <int D>
+// A query tile in flight: Q and dO rows (rows past N read as zero; source
+// rows of DS < D features padded with zeros) and the statistics of its 64
+// queries.
+template <int D, int DS>
 struct QTileStage {
-  RowStage<D, kThreads> q, o;
+  RowStage<D, kThreads, DS> q, o;
   float stat;
 
   __device__ __forceinline__ void load(const uint16_t* qh, const uint16_t* oh, const float* lse2h,
                                        const float* dlth, int64_t i0, int64_t n) {
-    q.load(tile_rsrc<D>(qh, i0, n));
-    o.load(tile_rsrc<D>(oh, i0, n));
+    q.load(tile_rsrc<DS>(qh, i0, n));
+    o.load(tile_rsrc<DS>(oh, i0, n));
     // every thread loads (two copies of the 128 values), clamped to row N-1
     const int ts = (int)threadIdx.x & (2 * kBQ - 1);
     const int64_t i = i0 + (ts & (kBQ - 1));
@@ -195,7 +196,7 @@ __device__ __forceinline__ void clamp_buckets(uint8_t (&b)[16]) {
 
 // b: this lane's 16 bucket indices, as 16 bytes (gathered from spd columns)
 // or as 4 words (a 16-byte row segment of spd_t).
-template <int D, int NB, bool KTAIL, int BUF, int QS, typename BT>
+template <int D, int NKS, int NB, bool KTAIL, int BUF, int QS, typename BT>
 __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOffsets<D>& off,
                                               const bf16x8* kf, const bf16x8* vf,
                                               const BT* b, float sl2, bool jok,
@@ -218,7 +219,7 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOff
     }
   }
 #pragma unroll
-  for (int kc = 0; kc < NKC; ++kc) {
+  for (int kc = 0; kc < NKS; ++kc) {
     s = mfma32(lds_b128(sm.q[BUF] + QS * 32 * D + off.row[kc]), kf[kc], s);
     dp = mfma32(lds_b128(sm.o[BUF] + QS * 32 * D + off.row[kc]), vf[kc], dp);
   }
@@ -297,15 +298,15 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOff
   }
 }
 
-template <int D, int NB, bool KTAIL, bool QFULL, bool TR>
+template <int D, int DS, int NB, bool KTAIL, bool QFULL, bool TR>
 __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm, int h, int64_t key0,
                                           int64_t j, bool jok, int fexp) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 5;
-  const int64_t hq = (int64_t)h * a.Sq * D;   // query-side rows
-  const int64_t hk = (int64_t)h * a.Sk * D;   // key-side rows
+  const int64_t hq = (int64_t)h * a.Sq * DS;   // query-side rows
+  const int64_t hk = (int64_t)h * a.Sk * DS;   // key-side rows
   const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + hq;
   const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + hk;
   const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + hk;
@@ -322,8 +323,10 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   bf16x8 kf[NKC], vf[NKC];
 #pragma unroll
   for (int kc = 0; kc < NKC; ++kc) {
-    kf[kc] = jok ? *reinterpret_cast<const bf16x8*>(kh + j * D + kc * 16 + g * 8) : zero_bf16x8();
-    const bf16x8 v8 = jok ? *reinterpret_cast<const bf16x8*>(vh + j * D + kc * 16 + g * 8) : zero_bf16x8();
+    const int f0 = kc * 16 + g * 8;
+    const bool in = jok && f0 < DS;
+    kf[kc] = in ? *reinterpret_cast<const bf16x8*>(kh + j * DS + f0) : zero_bf16x8();
+    const bf16x8 v8 = in ? *reinterpret_cast<const bf16x8*>(vh + j * DS + f0) : zero_bf16x8();
 #pragma unroll
     for (int e = 0; e < 8; ++e) vf[kc][e] = (__bf16)((float)v8[e] * sF);
   }
@@ -357,7 +360,7 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
     }
   };
 
-  QTileStage<D> st;
+  QTileStage<D, DS> st;
   st.load(qh, oh, lse2h, dlth, 0, a.Sq);
   BT bA[NBT], bB[NBT];
   fetch(0, bA);
@@ -376,10 +379,10 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
     fetch(i0 + 32, bB);
     st.load(qh, oh, lse2h, dlth, inext, a.Sq);
     sched_fence();
-    dkdv_subblock<D, NB, KTAIL, BUF, 0>(sm, off, kf, vf, bA, sl2, jok, dk, dv);
+    dkdv_subblock<D, (DS + 15) / 16, NB, KTAIL, BUF, 0>(sm, off, kf, vf, bA, sl2, jok, dk, dv);
     fetch(inext, bA);
     sched_fence();
-    dkdv_subblock<D, NB, KTAIL, BUF, 1>(sm, off, kf, vf, bB, sl2, jok, dk, dv);
+    dkdv_subblock<D, (DS + 15) / 16, NB, KTAIL, BUF, 1>(sm, off, kf, vf, bB, sl2, jok, dk, dv);
     if (more) st.template store<BUF ^ 1>(sm, inext, a.Sq, inv_sl2, sF);
     __syncthreads();
   };
@@ -393,13 +396,14 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   const float dk_scale = a.scale * ldexpf(1.0f, -fexp);
   if (jok && a.accumulate) {
     // fp32 partials of the key block, accumulated across ring steps
-    float* dkp = reinterpret_cast<float*>(a.dk) + hk + j * D;
-    float* dvp = reinterpret_cast<float*>(a.dv) + hk + j * D;
+    float* dkp = reinterpret_cast<float*>(a.dk) + hk + j * DS;
+    float* dvp = reinterpret_cast<float*>(a.dv) + hk + j * DS;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int c = cb * 32 + 8 * u + 4 * g;
+        if (c >= DS) continue;               // zero padding of a narrow head dim
         float4 xk = *reinterpret_cast<const float4*>(dkp + c);
         float4 xv = *reinterpret_cast<const float4*>(dvp + c);
         xk.x += dk[cb][4 * u] * dk_scale; xk.y += dk[cb][4 * u + 1] * dk_scale;
@@ -411,13 +415,14 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
       }
     }
   } else if (jok) {
-    uint16_t* dkp = reinterpret_cast<uint16_t*>(a.dk) + hk + j * D;
-    uint16_t* dvp = reinterpret_cast<uint16_t*>(a.dv) + hk + j * D;
+    uint16_t* dkp = reinterpret_cast<uint16_t*>(a.dk) + hk + j * DS;
+    uint16_t* dvp = reinterpret_cast<uint16_t*>(a.dv) + hk + j * DS;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int c = cb * 32 + 8 * u + 4 * g;
+        if (c >= DS) continue;
         uint2 pk, pv;
         pk.x = (uint32_t)f2bf(dk[cb][4 * u] * dk_scale) | ((uint32_t)f2bf(dk[cb][4 * u + 1] * dk_scale) << 16);
         pk.y = (uint32_t)f2bf(dk[cb][4 * u + 2] * dk_scale) | ((uint32_t)f2bf(dk[cb][4 * u + 3] * dk_scale) << 16);
@@ -430,7 +435,9 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   }
 }
 
-template <int D, int NB, bool QFULL, bool TR>
+// D: the tile's head dim (32 or 64); DS <= D: the head dim of the tensors
+// (8 and 16 run on 32-wide tiles whose extra features are zero).
+template <int D, int DS, int NB, bool QFULL, bool TR>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   constexpr int CPY = copies<NB>();
   __shared__ __attribute__((aligned(16))) DkdvSmem<D, NB> sm;
@@ -494,9 +501,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   }
 
   if ((kblk + 1) * kBK <= a.Sk)
-    dkdv_main<D, NB, false, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
+    dkdv_main<D, DS, NB, false, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
   else
-    dkdv_main<D, NB, true, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
+    dkdv_main<D, DS, NB, true, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
 
   __syncthreads();
   const double unscale = ldexp(1.0, -fexp);
@@ -508,42 +515,45 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   }
 }
 
-}  // namespace
-
-hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s) {
+template <int D, int DS, int NB>
+void launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
   const int64_t nkb = (a.Sk + kBK - 1) / kBK;
   const dim3 grid((unsigned)(nkb * a.H));
   const bool qfull = a.Sq % kBQ == 0;
-#define GT_DKDV_LAUNCH(D_, NB_)                                                                     \
-  {                                                                                                 \
-    if (a.spd_t) {                                                                                  \
-      if (qfull)                                                                                    \
-        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D_, NB_, true, true>), grid, dim3(kThreads), 0, s, a);  \
-      else                                                                                          \
-        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D_, NB_, false, true>), grid, dim3(kThreads), 0, s, a); \
-    } else {                                                                                        \
-      if (qfull)                                                                                    \
-        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D_, NB_, true, false>), grid, dim3(kThreads), 0, s, a); \
-      else                                                                                          \
-        hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D_, NB_, false, false>), grid, dim3(kThreads), 0, s, a);\
-    }                                                                                               \
+  if (a.spd_t) {
+    if (qfull)
+      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, DS, NB, true, true>), grid, dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, DS, NB, false, true>), grid, dim3(kThreads), 0, s, a);
+  } else {
+    if (qfull)
+      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, DS, NB, true, false>), grid, dim3(kThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, DS, NB, false, false>), grid, dim3(kThreads), 0, s, a);
   }
+}
+
+template <int NB>
+void launch_dkdv_nb(const BwdArgs& a, int d, hipStream_t s) {
+  switch (d) {
+    case 8: launch_dkdv_t<32, 8, NB>(a, s); break;
+    case 16: launch_dkdv_t<32, 16, NB>(a, s); break;
+    case 32: launch_dkdv_t<32, 32, NB>(a, s); break;
+    default: launch_dkdv_t<64, 64, NB>(a, s); break;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s) {
   // Byte values at or past n_buckets read bias 0 and their gradient is
   // dropped. Up to 127 buckets the 128-bucket layout (one byte permute per
   // address) is used, with larger bytes mapped to its padding bucket 127;
   // otherwise the full 256-bucket layout.
-  if (a.n_buckets <= 127) {
-    if (d == 64)
-      GT_DKDV_LAUNCH(64, 128)
-    else
-      GT_DKDV_LAUNCH(32, 128)
-  } else {
-    if (d == 64)
-      GT_DKDV_LAUNCH(64, 256)
-    else
-      GT_DKDV_LAUNCH(32, 256)
-  }
-#undef GT_DKDV_LAUNCH
+  if (a.n_buckets <= 127)
+    launch_dkdv_nb<128>(a, d, s);
+  else
+    launch_dkdv_nb<256>(a, d, s);
   return hipGetLastError();
 }
 

@@ -60,8 +60,9 @@ struct DqLane {
   float mlse2;            // -LSE log2 e; -inf for padded or empty rows (P = 0)
 };
 
-// Score and dP products of one 32-key block (key block kb of a staged tile).
-template <int D>
+// Score and dP products of one 32-key block (key block kb of a staged tile)
+// over the NK 16-feature chunks that hold data.
+template <int D, int NK>
 __device__ __forceinline__ void issue_block(const float* tab, const uint32_t (&w)[4], uint32_t lane4,
                                             const uint16_t* sK, const uint16_t* sV,
                                             const DqOffsets<D>& off, int kb, const DqLane<D>& ln,
@@ -69,7 +70,7 @@ __device__ __forceinline__ void issue_block(const float* tab, const uint32_t (&w
   load_bias(tab, w, lane4, s);
   dp = mfma32(ln.ones, ln.dlt, zero_f32x16());
 #pragma unroll
-  for (int kc = 0; kc < D / 16; ++kc) {
+  for (int kc = 0; kc < NK; ++kc) {
     s = mfma32(lds_b128(sK + kb * 32 * D + off.row[kc]), ln.qf[kc], s);
     dp = mfma32(lds_b128(sV + kb * 32 * D + off.row[kc]), ln.df[kc], dp);
   }
@@ -106,14 +107,17 @@ __device__ __forceinline__ void block_dq(const f32x16& s, const f32x16& dp, cons
   }
 }
 
-// VEC: spd rows are 16-byte aligned. FULL: VEC and Sk a multiple of the key
-// tile, so every spd group is loaded whole and no tile needs masking.
-template <int D, bool VEC, bool FULL>
+// D: the tile's head dim (32 or 64); DS <= D: the head dim of the tensors
+// (8 and 16 run on 32-wide tiles whose extra features are zero). VEC: spd
+// rows are 16-byte aligned. FULL: VEC and Sk a multiple of the key tile, so
+// every spd group is loaded whole and no tile needs masking.
+template <int D, int DS, bool VEC, bool FULL>
 __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
   constexpr int NKC = D / 16;
+  constexpr int NKS = (DS + 15) / 16;   // feature chunks that hold data
   constexpr int NCB = D / 32;
   constexpr int BR = kWaves * 32;
-  using Dma = TileDma<D, kWaves>;     // K and V
+  using Dma = TileDma<D, kWaves, DS>;     // K and V
   static_assert(kBC == kTileRows, "key tile is one staged tile");
 
   __shared__ __attribute__((aligned(16))) uint16_t sK0[kBC * D], sK1[kBC * D], sK2[kBC * D];
@@ -133,8 +137,8 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
 
   fill_lane_table(sTab, a.table + (int64_t)table_row(a, h) * a.n_buckets, a.n_buckets, a.scale, kThreads);
 
-  const int64_t hq = (int64_t)h * a.Sq * D;   // query-side rows
-  const int64_t hk = (int64_t)h * a.Sk * D;   // key-side rows
+  const int64_t hq = (int64_t)h * a.Sq * DS;   // query-side rows
+  const int64_t hk = (int64_t)h * a.Sk * DS;   // key-side rows
   const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + hq;
   const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + hk;
   const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + hk;
@@ -148,8 +152,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
   const int64_t qrow = i < a.Sq ? i : a.Sq - 1;
 #pragma unroll
   for (int kc = 0; kc < NKC; ++kc) {
-    ln.qf[kc] = *reinterpret_cast<const bf16x8*>(qh + qrow * D + kc * 16 + g * 8);
-    ln.df[kc] = *reinterpret_cast<const bf16x8*>(oh + qrow * D + kc * 16 + g * 8);
+    const int f0 = kc * 16 + g * 8;
+    ln.qf[kc] = f0 < DS ? *reinterpret_cast<const bf16x8*>(qh + qrow * DS + f0) : zero_bf16x8();
+    ln.df[kc] = f0 < DS ? *reinterpret_cast<const bf16x8*>(oh + qrow * DS + f0) : zero_bf16x8();
   }
   {
     const float l2 = a.lse2[(int64_t)h * a.Sq + qrow];
@@ -202,7 +207,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
     constexpr int S = decltype(stagec)::value;
     GT_DQ_STAGE(S, k_s, v_s)
     const int64_t j_ = (tt < ntiles ? tt : ntiles - 1) * kBC;
-    dma.load(tile_rsrc<D>(kh, j_, a.Sk), tile_rsrc<D>(vh, j_, a.Sk), k_s, v_s);
+    dma.load(tile_rsrc<DS>(kh, j_, a.Sk), tile_rsrc<DS>(vh, j_, a.Sk), k_s, v_s);
   };
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
@@ -223,7 +228,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
       fetch_spd(1, wB);
       wait_vmcnt<0>();
       __syncthreads();     // table, tiles 0..2
-      issue_block<D>(sTab, wA[0], lane4, sK0, sV0, off, 0, ln, s0, dp0);
+      issue_block<D, NKS>(sTab, wA[0], lane4, sK0, sV0, off, 0, ln, s0, dp0);
     }
     // Tile t: products of key block 1 issued, then block 0's element work
     // and dQ product; block 1's K^T operands read; spd words of tile t + 2
@@ -240,7 +245,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
       auto& w_n = P == 0 ? wB : wA;
       f32x16 s1, dp1;
       bf16x8 kt[2][NCB];
-      issue_block<D>(sTab, w[1], lane4, k_s, v_s, off, 1, ln, s1, dp1);
+      issue_block<D, NKS>(sTab, w[1], lane4, k_s, v_s, off, 1, ln, s1, dp1);
       read_kt<D>(k_s, off, 0, kt);
       block_dq<D, false>(s0, dp0, kt, kBC, sl2, ln.mlse2, acc);
       read_kt<D>(k_s, off, 1, kt);
@@ -251,7 +256,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
       __builtin_amdgcn_s_barrier();
       copy_tile(t + 3, stagec);
       sched_fence();
-      issue_block<D>(sTab, w_n[0], lane4, k_n, v_n, off, 0, ln, s0, dp0);
+      issue_block<D, NKS>(sTab, w_n[0], lane4, k_n, v_n, off, 0, ln, s0, dp0);
       block_dq<D, false>(s1, dp1, kt, kBC, sl2, ln.mlse2, acc);
     };
     int64_t t = 0;
@@ -293,7 +298,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
       for (int kb = 0; kb < kKB; ++kb) {
         f32x16 s, dp;
         bf16x8 kt[2][NCB];
-        issue_block<D>(sTab, w[kb], lane4, k_s, v_s, off, kb, ln, s, dp);
+        issue_block<D, NKS>(sTab, w[kb], lane4, k_s, v_s, off, kb, ln, s, dp);
         read_kt<D>(k_s, off, kb, kt);
         block_dq<D, MASK>(s, dp, kt, jrem - kb * 32, sl2, ln.mlse2, acc);
       }
@@ -318,12 +323,13 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
 
   if (i >= a.Sq) return;
   if (a.accumulate) {   // fp32 partial of the query shard, accumulated across ring steps
-    float* dqa = reinterpret_cast<float*>(a.dq) + hq + i * D;
+    float* dqa = reinterpret_cast<float*>(a.dq) + hq + i * DS;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int c = cb * 32 + 8 * u + 4 * g;
+        if (c >= DS) continue;               // zero padding of a narrow head dim
         float4 x = *reinterpret_cast<const float4*>(dqa + c);
         x.x += acc[cb][4 * u] * a.scale; x.y += acc[cb][4 * u + 1] * a.scale;
         x.z += acc[cb][4 * u + 2] * a.scale; x.w += acc[cb][4 * u + 3] * a.scale;
@@ -332,12 +338,13 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
     }
     return;
   }
-  uint16_t* dqp = reinterpret_cast<uint16_t*>(a.dq) + hq + i * D;
+  uint16_t* dqp = reinterpret_cast<uint16_t*>(a.dq) + hq + i * DS;
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int c = cb * 32 + 8 * u + 4 * g;
+      if (c >= DS) continue;
       uint2 pk;
       pk.x = (uint32_t)f2bf(acc[cb][4 * u] * a.scale) | ((uint32_t)f2bf(acc[cb][4 * u + 1] * a.scale) << 16);
       pk.y = (uint32_t)f2bf(acc[cb][4 * u + 2] * a.scale) | ((uint32_t)f2bf(acc[cb][4 * u + 3] * a.scale) << 16);
@@ -346,27 +353,27 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
   }
 }
 
-}  // namespace
-
-hipError_t launch_dq_bf16(const BwdArgs& a, int d, hipStream_t s) {
+template <int D, int DS>
+void launch_dq_t(const BwdArgs& a, hipStream_t s) {
   constexpr int BR = kWaves * 32;
   const int64_t nqb = (a.Sq + BR - 1) / BR;
   const dim3 grid((unsigned)(nqb * a.H));
-  const bool full = a.spd_vec && a.Sk % kBC == 0;
-  if (d == 64) {
-    if (full)
-      hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, true, true>), grid, dim3(kThreads), 0, s, a);
-    else if (a.spd_vec)
-      hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, true, false>), grid, dim3(kThreads), 0, s, a);
-    else
-      hipLaunchKernelGGL((bwd_dq_bf16_kernel<64, false, false>), grid, dim3(kThreads), 0, s, a);
-  } else {
-    if (full)
-      hipLaunchKernelGGL((bwd_dq_bf16_kernel<32, true, true>), grid, dim3(kThreads), 0, s, a);
-    else if (a.spd_vec)
-      hipLaunchKernelGGL((bwd_dq_bf16_kernel<32, true, false>), grid, dim3(kThreads), 0, s, a);
-    else
-      hipLaunchKernelGGL((bwd_dq_bf16_kernel<32, false, false>), grid, dim3(kThreads), 0, s, a);
+  if (a.spd_vec && a.Sk % kBC == 0)
+    hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, DS, true, true>), grid, dim3(kThreads), 0, s, a);
+  else if (a.spd_vec)
+    hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, DS, true, false>), grid, dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((bwd_dq_bf16_kernel<D, DS, false, false>), grid, dim3(kThreads), 0, s, a);
+}
+
+}  // namespace
+
+hipError_t launch_dq_bf16(const BwdArgs& a, int d, hipStream_t s) {
+  switch (d) {
+    case 8: launch_dq_t<32, 8>(a, s); break;
+    case 16: launch_dq_t<32, 16>(a, s); break;
+    case 32: launch_dq_t<32, 32>(a, s); break;
+    default: launch_dq_t<64, 64>(a, s); break;
   }
   return hipGetLastError();
 }

@@ -135,13 +135,15 @@ __device__ __forceinline__ void softmax_pv(const f32x16& s, const bf16x8 (&vop)[
 // Score product of one 32x32 unit: bias entries into the accumulator, then
 // the K operands of key block kb (read from the staged tile) times the
 // unit's Q^T.
-template <int D>
+// NK: the 16-feature chunks that hold data (all D / 16, or fewer when the
+// source rows are narrower than the tile and the rest is zero).
+template <int D, int NK>
 __device__ __forceinline__ void issue_scores(const float* tab, const uint32_t (&w)[4], uint32_t lane4,
                                              const uint16_t* sK, const int (&koff)[D / 16], int kb,
                                              const bf16x8 (&q)[D / 16], f32x16& s) {
   load_bias(tab, w, lane4, s);
 #pragma unroll
-  for (int kc = 0; kc < D / 16; ++kc) s = mfma32(lds_b128(sK + kb * 32 * D + koff[kc]), q[kc], s);
+  for (int kc = 0; kc < NK; ++kc) s = mfma32(lds_b128(sK + kb * 32 * D + koff[kc]), q[kc], s);
 }
 
 template <int D>
@@ -156,7 +158,7 @@ __device__ __forceinline__ void read_v(const uint16_t* sV, const FwdOffsets<D>& 
 
 // Unpipelined tile (ragged or unaligned shapes): for each 32-key block the
 // score products of both query blocks, then their softmax and P V.
-template <int D, bool MASK>
+template <int D, int NK, bool MASK>
 __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV, const float* tab,
                                          const FwdOffsets<D>& off,
                                          const bf16x8 (&qf)[kQB][D / 16],
@@ -168,7 +170,7 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
   for (int kb = 0; kb < kKB; ++kb) {
     f32x16 s[kQB];
 #pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) issue_scores<D>(tab, w[qb][kb], lane4, sK, off.k, kb, qf[qb], s[qb]);
+    for (int qb = 0; qb < kQB; ++qb) issue_scores<D, NK>(tab, w[qb][kb], lane4, sK, off.k, kb, qf[qb], s[qb]);
     bf16x8 vop[2][NCB];
     read_v<D>(sV, off, kb, vop);
 #pragma unroll
@@ -177,15 +179,18 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
   }
 }
 
-// VEC: spd rows are 16-byte aligned. FULL: VEC and Sk a multiple of the key
-// tile, so every spd group is loaded whole and no tile needs masking. SKIP:
-// Sq is not a multiple of the workgroup's rows, so some waves may own no row.
-template <int D, bool OUT_F32, bool VEC, bool FULL, bool SKIP>
+// D: the tile's head dim (32 or 64); DS <= D: the head dim of the tensors
+// (8 and 16 run on 32-wide tiles whose extra features are zero). VEC: spd
+// rows are 16-byte aligned. FULL: VEC and Sk a multiple of the key tile, so
+// every spd group is loaded whole and no tile needs masking. SKIP: Sq is not
+// a multiple of the workgroup's rows, so some waves may own no row.
+template <int D, int DS, bool OUT_F32, bool VEC, bool FULL, bool SKIP>
 __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   constexpr int NKC = D / 16;
+  constexpr int NKS = (DS + 15) / 16;   // feature chunks that hold data
   constexpr int NCB = D / 32;
   constexpr int BR = kWaves * 32 * kQB;
-  using Dma = TileDma<D, kWaves>;     // K and V
+  using Dma = TileDma<D, kWaves, DS>;     // K and V
   static_assert(kBC == kTileRows, "key tile is one staged tile");
 
   // Three-stage ring of K / V tiles, one array per stage so that no read of
@@ -212,9 +217,9 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
 
   fill_lane_table(sTab, a.table + (int64_t)table_row(a, h) * a.n_buckets, a.n_buckets, a.scale, kThreads);
 
-  const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)h * a.Sq * D;
-  const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + (int64_t)h * a.Sk * D;
-  const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + (int64_t)h * a.Sk * D;
+  const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)h * a.Sq * DS;
+  const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + (int64_t)h * a.Sk * DS;
+  const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + (int64_t)h * a.Sk * DS;
   const float sl2 = a.scale * kLog2e;
 
   // Q^T operands; rows past Sq load the clamped row Sq-1 (their output is
@@ -226,8 +231,10 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
     const int64_t i = qbase + qb * 32 + col;
     qrow[qb] = i < a.Sq ? i : a.Sq - 1;
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc)
-      qf[qb][kc] = *reinterpret_cast<const bf16x8*>(qh + qrow[qb] * D + kc * 16 + g * 8);
+    for (int kc = 0; kc < NKC; ++kc) {
+      const int f0 = kc * 16 + g * 8;
+      qf[qb][kc] = f0 < DS ? *reinterpret_cast<const bf16x8*>(qh + qrow[qb] * DS + f0) : zero_bf16x8();
+    }
   }
 
   // spd bytes of key group j..j+15 of the lane's query row: one 16-byte raw
@@ -280,7 +287,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
     constexpr int S = decltype(stagec)::value;
     GT_FWD_STAGE(S, k_s, v_s)
     const int64_t j_ = (tt < ntiles ? tt : ntiles - 1) * kBC;
-    dma.load(tile_rsrc<D>(kh, j_, a.Sk), tile_rsrc<D>(vh, j_, a.Sk), k_s, v_s);
+    dma.load(tile_rsrc<DS>(kh, j_, a.Sk), tile_rsrc<DS>(vh, j_, a.Sk), k_s, v_s);
   };
   auto spd_of = [&](int64_t tt, uint32_t (&w)[kQB][kKB][4]) {
     fetch_spd((tt < ntiles ? tt : ntiles - 1) * kBC, w);
@@ -304,7 +311,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
       spd_of(1, wB);
       wait_vmcnt<0>();
       __syncthreads();     // table, and tiles 0..2
-      if (active) issue_scores<D>(sTab, wA[0][0], lane4, sK0, off.k, 0, qf[0], s0);
+      if (active) issue_scores<D, NKS>(sTab, wA[0][0], lane4, sK0, off.k, 0, qf[0], s0);
     }
     // Tile t from stage S = t % 3 and spd set P = t % 2; units u = (key
     // block, query block) in the order (0,0), (0,1), (1,0), (1,1). The score
@@ -332,12 +339,12 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
       }
       bf16x8 vop[2][NCB];
       f32x16 s1, s2, s3;
-      issue_scores<D>(sTab, w[1][0], lane4, k_s, off.k, 0, qf[1], s1);
+      issue_scores<D, NKS>(sTab, w[1][0], lane4, k_s, off.k, 0, qf[1], s1);
       read_v<D>(v_s, off, 0, vop);
       softmax_pv<D, false>(s0, vop, kBC, sl2, sm[0], acc[0]);
-      issue_scores<D>(sTab, w[0][1], lane4, k_s, off.k, 1, qf[0], s2);
+      issue_scores<D, NKS>(sTab, w[0][1], lane4, k_s, off.k, 1, qf[0], s2);
       softmax_pv<D, false>(s1, vop, kBC, sl2, sm[1], acc[1]);
-      issue_scores<D>(sTab, w[1][1], lane4, k_s, off.k, 1, qf[1], s3);
+      issue_scores<D, NKS>(sTab, w[1][1], lane4, k_s, off.k, 1, qf[1], s3);
       read_v<D>(v_s, off, 1, vop);
       spd_of(t + 2, w);      // set P is free: tile t + 2's words
       sched_fence();
@@ -349,7 +356,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
       __builtin_amdgcn_s_barrier();
       copy_tile(t + 3, stagec);
       sched_fence();
-      issue_scores<D>(sTab, w_n[0][0], lane4, k_n, off.k, 0, qf[0], s0);
+      issue_scores<D, NKS>(sTab, w_n[0][0], lane4, k_n, off.k, 0, qf[0], s0);
       softmax_pv<D, false>(s3, vop, kBC, sl2, sm[1], acc[1]);
     };
     int64_t t = 0;
@@ -386,7 +393,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
       spd_of(t + 2, S == 0 ? w2 : (S == 1 ? w0 : w1));
       sched_fence();
       auto& w = S == 0 ? w0 : (S == 1 ? w1 : w2);
-      if (active) fwd_tile<D, MASK>(k_s, v_s, sTab, off, qf, w, lane4, a.Sk - t * kBC, sl2, sm, acc);
+      if (active) fwd_tile<D, NKS, MASK>(k_s, v_s, sTab, off, qf, w, lane4, a.Sk - t * kBC, sl2, sm, acc);
       wait_vmcnt<0>();
       __builtin_amdgcn_s_barrier();
     };
@@ -427,10 +434,11 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int c = cb * 32 + 8 * u + 4 * g;
+        if (c >= DS) continue;                 // zero padding of a narrow head dim
         float o0 = acc[qb][cb][4 * u + 0] * inv, o1 = acc[qb][cb][4 * u + 1] * inv;
         float o2 = acc[qb][cb][4 * u + 2] * inv, o3 = acc[qb][cb][4 * u + 3] * inv;
         if constexpr (OUT_F32) {
-          float* op = reinterpret_cast<float*>(a.o) + ((int64_t)h * a.Sq + i) * D + c;
+          float* op = reinterpret_cast<float*>(a.o) + ((int64_t)h * a.Sq + i) * DS + c;
           if (wo != 0.0f) {
             const float4 old = *reinterpret_cast<const float4*>(op);
             o0 = fmaf(old.x, wo, o0);
@@ -440,7 +448,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
           }
           *reinterpret_cast<float4*>(op) = make_float4(o0, o1, o2, o3);
         } else {
-          uint16_t* op = reinterpret_cast<uint16_t*>(a.o) + ((int64_t)h * a.Sq + i) * D + c;
+          uint16_t* op = reinterpret_cast<uint16_t*>(a.o) + ((int64_t)h * a.Sq + i) * DS + c;
           uint2 pk;
           pk.x = (uint32_t)f2bf(o0) | ((uint32_t)f2bf(o1) << 16);
           pk.y = (uint32_t)f2bf(o2) | ((uint32_t)f2bf(o3) << 16);
@@ -565,7 +573,7 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   a.lse[(int64_t)h * a.Sq + i] = lse_out;
 }
 
-template <int D, bool OUT_F32>
+template <int D, int DS, bool OUT_F32>
 hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t s) {
   constexpr int BR = kWaves * 32 * kQB;
   const int64_t nqb = (a.Sq + BR - 1) / BR;
@@ -573,23 +581,22 @@ hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t s) {
   const bool skip = a.Sq % BR != 0;
   if (a.spd_vec && a.Sk % kBC == 0) {
     if (skip)
-      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, true, true>), grid, dim3(kThreads), 0, s, a);
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, DS, OUT_F32, true, true, true>), grid, dim3(kThreads), 0, s, a);
     else
-      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, true, false>), grid, dim3(kThreads), 0, s, a);
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, DS, OUT_F32, true, true, false>), grid, dim3(kThreads), 0, s, a);
   } else if (a.spd_vec) {
     if (skip)
-      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, false, true>), grid, dim3(kThreads), 0, s, a);
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, DS, OUT_F32, true, false, true>), grid, dim3(kThreads), 0, s, a);
     else
-      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, true, false, false>), grid, dim3(kThreads), 0, s, a);
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, DS, OUT_F32, true, false, false>), grid, dim3(kThreads), 0, s, a);
   } else {
     if (skip)
-      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, false, false, true>), grid, dim3(kThreads), 0, s, a);
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, DS, OUT_F32, false, false, true>), grid, dim3(kThreads), 0, s, a);
     else
-      hipLaunchKernelGGL((fwd_bf16_kernel<D, OUT_F32, false, false, false>), grid, dim3(kThreads), 0, s, a);
+      hipLaunchKernelGGL((fwd_bf16_kernel<D, DS, OUT_F32, false, false, false>), grid, dim3(kThreads), 0, s, a);
   }
   return hipGetLastError();
 }
-
 template <int D>
 hipError_t launch_fwd_valu(const FwdArgs& a, bool bf16, bool out_f32, hipStream_t s) {
   const dim3 grid((unsigned)((a.Sq + 127) / 128 * a.H));
@@ -605,8 +612,16 @@ hipError_t launch_fwd_valu(const FwdArgs& a, bool bf16, bool out_f32, hipStream_
 }  // namespace
 
 hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStream_t s) {
-  if (bf16 && d == 64) return out_f32 ? launch_fwd_bf16<64, true>(a, s) : launch_fwd_bf16<64, false>(a, s);
-  if (bf16 && d == 32) return out_f32 ? launch_fwd_bf16<32, true>(a, s) : launch_fwd_bf16<32, false>(a, s);
+  // bf16 runs on the matrix cores at every head dim: 8 and 16 on 32-wide
+  // tiles whose extra features are zero. fp32 runs on the vector ALUs.
+  if (bf16) {
+    switch (d) {
+      case 8: return out_f32 ? launch_fwd_bf16<32, 8, true>(a, s) : launch_fwd_bf16<32, 8, false>(a, s);
+      case 16: return out_f32 ? launch_fwd_bf16<32, 16, true>(a, s) : launch_fwd_bf16<32, 16, false>(a, s);
+      case 32: return out_f32 ? launch_fwd_bf16<32, 32, true>(a, s) : launch_fwd_bf16<32, 32, false>(a, s);
+      default: return out_f32 ? launch_fwd_bf16<64, 64, true>(a, s) : launch_fwd_bf16<64, 64, false>(a, s);
+    }
+  }
   switch (d) {
     case 8: return launch_fwd_valu<8>(a, bf16, out_f32, s);
     case 16: return launch_fwd_valu<16>(a, bf16, out_f32, s);

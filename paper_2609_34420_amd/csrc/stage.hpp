@@ -54,12 +54,24 @@ __device__ __forceinline__ uint4 buf_b128(__amdgpu_buffer_rsrc_t r, uint32_t vof
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
+// Source rows narrower than the tile (DS < D features, for head dims 8 and
+// 16 on the 32-wide tiles): a chunk at or past DS / 8 is loaded from this
+// offset, past the end of every tile resource, so the load returns zeros.
+constexpr uint32_t kZeroChunk = 0x40000000u;
+
+// Byte offset, in a tile of DS-feature source rows, of 16-byte chunk `chunk`
+// of row `row` (zero-filled past DS).
+template <int DS>
+__device__ __forceinline__ uint32_t src_chunk_off(int row, int chunk) {
+  return chunk < DS / 8 ? (uint32_t)(row * DS * 2 + chunk * 16) : kZeroChunk;
+}
+
 // One tensor's tile in flight: NT threads, 16 bytes per item, item u =
-// row u / (D/8), chunk u % (D/8). A tile is contiguous in global memory, so
-// item u sits at byte 16 u of it. With fewer items than threads, the extra
-// threads load a duplicate (so every wave issues the same loads) and store
-// nothing.
-template <int D, int NT>
+// row u / (D/8), chunk u % (D/8); the source rows hold DS <= D features (a
+// tile of them is contiguous in global memory) and the chunks past DS read
+// as zero. With fewer items than threads, the extra threads load a
+// duplicate (so every wave issues the same loads) and store nothing.
+template <int D, int NT, int DS = D>
 struct RowStage {
   static constexpr int CPR = D / 8;
   static constexpr int ITEMS = kTileRows * CPR;
@@ -72,7 +84,7 @@ struct RowStage {
   }
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs) {
 #pragma unroll
-    for (int s = 0; s < IPT; ++s) r[s] = buf_b128(rs, (uint32_t)item(s) * 16u);
+    for (int s = 0; s < IPT; ++s) r[s] = buf_b128(rs, src_chunk_off<DS>(item(s) / CPR, item(s) % CPR));
   }
   // LDS element offset of this thread's item s.
   __device__ __forceinline__ static int lds_off(int s) {
@@ -98,8 +110,9 @@ struct RowStage {
 // one descriptor per tensor) is split into 1 KiB blocks handed to the NW
 // waves in order; within a block, lane l fills LDS chunk l % (D/8) of tile
 // row (block row 0) + l / (D/8), so it reads the logical chunk that the
-// swizzle stores there.
-template <int D, int NW>
+// swizzle stores there. Source rows of DS < D features leave the chunks
+// past DS zero.
+template <int D, int NW, int DS = D>
 struct TileDma {
   static constexpr int ROWB = D * 2;
   static constexpr int RPB = 1024 / ROWB;              // rows per block
@@ -120,7 +133,7 @@ struct TileDma {
       lds_byte[i] = lb * 1024;
       const int row = lb * RPB + lane / (D / 8);
       const int chunk = swz_tile<D>(row, lane % (D / 8));   // involution: logical chunk here
-      voff[i] = (uint32_t)(row * ROWB + chunk * 16);
+      voff[i] = src_chunk_off<DS>(row, chunk);
     }
   }
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs0, __amdgpu_buffer_rsrc_t rs1,
