@@ -17,11 +17,11 @@
  * added unscaled. LSE is the natural-log log-sum-exp of each score row.
  *
  * Conventions shared by every entry point
- *   - dtype GT_BF16: Q, K, V, O, dO, dQ, dK, dV are bfloat16. With d = 32 or
- *     64 the products run on bf16 matrix cores with fp32 accumulation and P
- *     and dS are rounded to bf16 before their products; with d = 8 or 16 (the
- *     8 heads over a 64-wide model of Section IV-A give d = 8) every score
- *     element is computed in fp32 on the vector ALUs from the bf16 inputs.
+ *   - dtype GT_BF16: Q, K, V, O, dO, dQ, dK, dV are bfloat16; the products
+ *     run on bf16 matrix cores with fp32 accumulation, and P and dS are
+ *     rounded to bf16 before their products. d = 8 and 16 (the 8 heads over
+ *     a 64-wide model of Section IV-A give d = 8) run on the same kernels
+ *     with 32-wide tiles whose extra features are zero.
  *     GT_F32: all of those tensors are fp32 and computed in fp32. table,
  *     dtable, LSE, partial O and partial LSE are always fp32.
  *   - d (head dim) must be 8, 16, 32 or 64; 1 <= n_buckets <= 256;
@@ -143,9 +143,8 @@ gt_status_t gt_attn_bwd_batch(const void* q, const void* k, const void* v,
  * (e.g. the two independent stages on two streams) or time them:
  *   phase 0  prepare: rowsum(dO * O) and LSE * log2(e) into the workspace;
  *            dtable = 0
- *   phase 1  dK and dV, and dtable on the matrix-core path (bf16, d >= 32)
- *            (needs phase 0)
- *   phase 2  dQ, and dtable on the vector-ALU path (fp32, or d < 32)
+ *   phase 1  dK and dV, and dtable for bf16 (needs phase 0)
+ *   phase 2  dQ, and dtable for fp32
  *            (needs phase 0; independent of phase 1)
  * Arguments and results are exactly those of gt_attn_bwd; running phases
  * 0, 1, 2 on one stream is gt_attn_bwd. Outputs a phase does not produce

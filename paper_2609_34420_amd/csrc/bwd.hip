@@ -8,13 +8,12 @@
 //
 // Launch order: prepare (lse2 = LSE log2 e, +inf for an empty row so that
 // P = 0; Dlt; dtable = 0), then the key-stationary dK/dV/dtable kernel and
-// the query-stationary dQ kernel (bwd_dkdv.hip, bwd_dq.hip for bf16 with
-// d >= 32; the vector-ALU kernels below for fp32 and for d < 32). Splitting dQ
-// from dK/dV recomputes two products but needs no atomics on dQ.
+// the query-stationary dQ kernel (bwd_dkdv.hip, bwd_dq.hip for bf16 at
+// every head dim; the vector-ALU kernels below for fp32). Splitting dQ from
+// dK/dV recomputes two products but needs no atomics on dQ.
 #include <type_traits>
 
 #include "common.hpp"
-#include "dtable.hpp"
 #include "kernels.hpp"
 
 namespace gt {
@@ -119,50 +118,45 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Vector-ALU path: one thread per query row / key column, fp32 math. Serves
-// fp32 inputs and bf16 inputs with head dims below 32 (IN_BF16: q, k, v, dO
-// are bf16, and so are dq, dk, dv unless the call accumulates into fp32).
+// Vector-ALU path (fp32 inputs): one thread per query row / key column, fp32
+// math; dq, dk, dv are fp32 (stored, or added into the caller's
+// accumulators).
 // ---------------------------------------------------------------------------
-template <int D, bool IN_BF16>
-__device__ __forceinline__ void store_grad(void* base, int64_t idx, float x, bool accumulate) {
-  if (accumulate) {
-    float* p = reinterpret_cast<float*>(base) + idx;
-    *p += x;
-  } else if constexpr (IN_BF16) {
-    reinterpret_cast<uint16_t*>(base)[idx] = f2bf(x);
-  } else {
-    reinterpret_cast<float*>(base)[idx] = x;
-  }
+__device__ __forceinline__ void store_grad(float* base, int64_t idx, float x, bool accumulate) {
+  if (accumulate)
+    base[idx] += x;
+  else
+    base[idx] = x;
 }
 
-template <int D, bool IN_BF16>
+template <int D>
 __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
   constexpr int TK = 64;             // keys per LDS tile, in blocks of 16
   __shared__ __attribute__((aligned(16))) float sK[TK][D];
   __shared__ __attribute__((aligned(16))) float sV[TK][D];
   __shared__ float sT[256];
-  // dtable histogram: bf16 inputs add in fixed point (dtable.hpp), fp32
-  // inputs in fp32 (slow LDS float atomics, but no quantisation of dS)
-  using HistT = std::conditional_t<IN_BF16, unsigned long long, float>;
-  __shared__ HistT sH[256];
-  __shared__ float sRed[3][2];
+  // dtable histogram in fp32: LDS float atomics are slow, but fp32 inputs
+  // need the unquantised dS
+  __shared__ float sH[256];
   const int tid = threadIdx.x;
   const int64_t nqb = (a.Sq + 127) / 128;
   const int h = (int)(blockIdx.x / nqb);
   const int64_t i = (blockIdx.x % nqb) * 128 + tid;
   for (int t = tid; t < 256; t += 128) {
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
-    sH[t] = HistT(0);
+    sH[t] = 0.0f;
   }
-  const int fexp = IN_BF16 ? hist_exponent<2>(a, h, sRed) : 0;
-  const float sF = ldexpf(1.0f, fexp);
+  const float* qg = reinterpret_cast<const float*>(a.q);
+  const float* kg = reinterpret_cast<const float*>(a.k);
+  const float* vg = reinterpret_cast<const float*>(a.v);
+  const float* dog = reinterpret_cast<const float*>(a.d_o);
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
   const bool ok = i < a.Sq;
   float qv[D], dov[D], acc[D];
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    qv[c] = ok ? load_elem<IN_BF16>(a.q, hq + i * D + c) * a.scale : 0.0f;
-    dov[c] = ok ? load_elem<IN_BF16>(a.d_o, hq + i * D + c) : 0.0f;
+    qv[c] = ok ? qg[hq + i * D + c] * a.scale : 0.0f;
+    dov[c] = ok ? dog[hq + i * D + c] : 0.0f;
     acc[c] = 0.0f;
   }
   const float L = ok ? a.lse[(int64_t)h * a.Sq + i] : -INFINITY;
@@ -173,8 +167,8 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
     for (int t = tid; t < TK * D; t += 128) {
       const int r = t / D, c = t % D;
       const bool in = j0 + r < a.Sk;
-      sK[r][c] = in ? load_elem<IN_BF16>(a.k, hk + (j0 + r) * D + c) : 0.0f;
-      sV[r][c] = in ? load_elem<IN_BF16>(a.v, hk + (j0 + r) * D + c) : 0.0f;
+      sK[r][c] = in ? kg[hk + (j0 + r) * D + c] : 0.0f;
+      sV[r][c] = in ? vg[hk + (j0 + r) * D + c] : 0.0f;
     }
     __syncthreads();
     if (!ok || L == -INFINITY) continue;
@@ -202,30 +196,21 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
         const float ds = p * (dp - dlt);
 #pragma unroll
         for (int c = 0; c < D; ++c) acc[c] = fmaf(ds, sK[key][c], acc[c]);
-        if (b < (uint32_t)a.n_buckets) {
-          if constexpr (IN_BF16)
-            atomicAdd(&sH[b], (unsigned long long)(long long)round_to_int(ds * sF));
-          else
-            atomicAdd(&sH[b], ds);
-        }
+        if (b < (uint32_t)a.n_buckets) atomicAdd(&sH[b], ds);
       }
     }
   }
   if (ok) {
 #pragma unroll
-    for (int c = 0; c < D; ++c) store_grad<D, IN_BF16>(a.dq, hq + i * D + c, acc[c] * a.scale, a.accumulate);
+    for (int c = 0; c < D; ++c) store_grad(reinterpret_cast<float*>(a.dq), hq + i * D + c, acc[c] * a.scale, a.accumulate);
   }
   __syncthreads();
   float* dth = a.dtable + (int64_t)table_row(a, h) * a.n_buckets;
-  if constexpr (IN_BF16) {
-    flush_hist<1>(sH, a.n_buckets, fexp, dth, 128);
-  } else {
-    for (int t = tid; t < a.n_buckets; t += 128)
-      if (sH[t] != 0.0f) atomicAdd(&dth[t], sH[t]);
-  }
+  for (int t = tid; t < a.n_buckets; t += 128)
+    if (sH[t] != 0.0f) atomicAdd(&dth[t], sH[t]);
 }
 
-template <int D, bool IN_BF16>
+template <int D>
 __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
   constexpr int TQ = 32;
   __shared__ float sQ[TQ][D];
@@ -244,8 +229,8 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
   float kv[D], vv[D], dk[D], dv[D];
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    kv[c] = ok ? load_elem<IN_BF16>(a.k, hk + j * D + c) * a.scale : 0.0f;
-    vv[c] = ok ? load_elem<IN_BF16>(a.v, hk + j * D + c) : 0.0f;
+    kv[c] = ok ? reinterpret_cast<const float*>(a.k)[hk + j * D + c] * a.scale : 0.0f;
+    vv[c] = ok ? reinterpret_cast<const float*>(a.v)[hk + j * D + c] : 0.0f;
     dk[c] = 0.0f;
     dv[c] = 0.0f;
   }
@@ -254,8 +239,8 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
     for (int t = tid; t < TQ * D; t += 128) {
       const int r = t / D, c = t % D;
       const bool in = i0 + r < a.Sq;
-      sQ[r][c] = in ? load_elem<IN_BF16>(a.q, hq + (i0 + r) * D + c) : 0.0f;
-      sO[r][c] = in ? load_elem<IN_BF16>(a.d_o, hq + (i0 + r) * D + c) : 0.0f;
+      sQ[r][c] = in ? reinterpret_cast<const float*>(a.q)[hq + (i0 + r) * D + c] : 0.0f;
+      sO[r][c] = in ? reinterpret_cast<const float*>(a.d_o)[hq + (i0 + r) * D + c] : 0.0f;
     }
     for (int t = tid; t < TQ; t += 128) {
       const bool in = i0 + t < a.Sq;
@@ -285,8 +270,8 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
   if (!ok) return;
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    store_grad<D, IN_BF16>(a.dk, hk + j * D + c, dk[c] * a.scale, a.accumulate);
-    store_grad<D, IN_BF16>(a.dv, hk + j * D + c, dv[c], a.accumulate);
+    store_grad(reinterpret_cast<float*>(a.dk), hk + j * D + c, dk[c] * a.scale, a.accumulate);
+    store_grad(reinterpret_cast<float*>(a.dv), hk + j * D + c, dv[c], a.accumulate);
   }
 }
 
@@ -311,20 +296,14 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
     }
     return e;
   }
-  // vector-ALU path: dK/dV in phase 1, dQ and dtable in phase 2
+  // vector-ALU path (fp32): dK/dV in phase 1, dQ and dtable in phase 2
   const int64_t nkb = (a.Sk + 127) / 128, nqb = (a.Sq + 127) / 128;
   if (phase < 0 || phase == 1) {
-    if (bf16)
-      hipLaunchKernelGGL((bwd_dkdv_valu_kernel<D, true>), dim3((unsigned)(nkb * a.H)), dim3(128), 0, s, a);
-    else
-      hipLaunchKernelGGL((bwd_dkdv_valu_kernel<D, false>), dim3((unsigned)(nkb * a.H)), dim3(128), 0, s, a);
+    hipLaunchKernelGGL((bwd_dkdv_valu_kernel<D>), dim3((unsigned)(nkb * a.H)), dim3(128), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (phase < 0 || phase == 2) {
-    if (bf16)
-      hipLaunchKernelGGL((bwd_dq_valu_kernel<D, true>), dim3((unsigned)(nqb * a.H)), dim3(128), 0, s, a);
-    else
-      hipLaunchKernelGGL((bwd_dq_valu_kernel<D, false>), dim3((unsigned)(nqb * a.H)), dim3(128), 0, s, a);
+    hipLaunchKernelGGL((bwd_dq_valu_kernel<D>), dim3((unsigned)(nqb * a.H)), dim3(128), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return e;

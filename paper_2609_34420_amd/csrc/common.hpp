@@ -125,26 +125,6 @@ __device__ __forceinline__ float bf2f(uint16_t x) {
   return __uint_as_float(((uint32_t)x) << 16);
 }
 
-// c + a . b over NP packed bf16 pairs (v_dot2: the bf16 products are exact in
-// fp32).
-template <int NP>
-__device__ __forceinline__ float dot_bf16(const uint32_t* a, const uint32_t* b, float c) {
-#pragma unroll
-  for (int i = 0; i < NP; ++i)
-    c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a[i]), __builtin_bit_cast(bf16x2, b[i]), c,
-                                        false);
-  return c;
-}
-
-// Element idx of a tensor of bf16 (BF) or fp32 values, as fp32.
-template <bool BF>
-__device__ __forceinline__ float load_elem(const void* p, int64_t idx) {
-  if constexpr (BF)
-    return bf2f(reinterpret_cast<const uint16_t*>(p)[idx]);
-  else
-    return reinterpret_cast<const float*>(p)[idx];
-}
-
 // Workgroup id -> logical id so that consecutive logical ids (the H heads of
 // one row block, which share their spd tiles) land on the same XCD at about
 // the same time. Workgroups are handed to the 8 XCDs round robin.

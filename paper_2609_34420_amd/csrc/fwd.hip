@@ -460,19 +460,13 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   }
 }
 
-// Vector-ALU path: one thread per query row, keys staged through LDS as fp32,
-// fp32 math with expf/logf. Serves fp32 inputs (any head dim) and bf16
-// inputs with head dims below the 32 the matrix-core kernels tile by, where
-// the work per score element is the bias gather and the softmax, not the
-// products. IN_BF16: q, k, v are bf16; OUT_F32: o is fp32 (else the input
-// type).
-template <int D, bool IN_BF16, bool OUT_F32>
+// Vector-ALU path (fp32 inputs, any head dim): one thread per query row,
+// keys staged through LDS, fp32 math with the hardware exp2 and logf; o is
+// fp32.
+template <int D>
 __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   constexpr int TK = 64;             // keys per LDS tile, in blocks of 16
-  constexpr int DP = D / 2;          // bf16 pairs per row
-  // K as fp32 (fp32 inputs) or as packed bf16 pairs for v_dot2 (bf16 inputs)
-  __shared__ __attribute__((aligned(16))) float sK[IN_BF16 ? 1 : TK][D];
-  __shared__ __attribute__((aligned(16))) uint32_t sKp[IN_BF16 ? TK : 1][DP];
+  __shared__ __attribute__((aligned(16))) float sK[TK][D];
   __shared__ __attribute__((aligned(16))) float sV[TK][D];
   __shared__ float sT[256];
   const int tid = threadIdx.x;
@@ -481,18 +475,17 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   const int64_t i = (blockIdx.x % nqb) * 128 + tid;
   for (int t = tid; t < 256; t += 128)
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
+  const float* qg = reinterpret_cast<const float*>(a.q);
+  const float* kg = reinterpret_cast<const float*>(a.k);
+  const float* vg = reinterpret_cast<const float*>(a.v);
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
   const bool ok = i < a.Sq;
   float qv[D], acc[D];
-  uint32_t qp[DP];                   // bf16 inputs: the query row as packed pairs
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    qv[c] = ok ? load_elem<IN_BF16>(a.q, hq + i * D + c) * a.scale : 0.0f;
+    qv[c] = ok ? qg[hq + i * D + c] * a.scale : 0.0f;
     acc[c] = 0.0f;
   }
-#pragma unroll
-  for (int c = 0; c < DP; ++c)
-    qp[c] = (IN_BF16 && ok) ? reinterpret_cast<const uint32_t*>(a.q)[(hq + i * D) / 2 + c] : 0u;
   const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
   float m = -INFINITY, l = 0.0f;     // running max (natural units) and sum relative to it
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
@@ -500,14 +493,8 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
     for (int t = tid; t < TK * D; t += 128) {
       const int r = t / D, c = t % D;
       const bool in = j0 + r < a.Sk;
-      if constexpr (!IN_BF16) sK[r][c] = in ? load_elem<false>(a.k, hk + (j0 + r) * D + c) : 0.0f;
-      sV[r][c] = in ? load_elem<IN_BF16>(a.v, hk + (j0 + r) * D + c) : 0.0f;
-    }
-    if constexpr (IN_BF16) {
-      for (int t = tid; t < TK * DP; t += 128) {
-        const int r = t / DP, c = t % DP;
-        sKp[r][c] = (j0 + r < a.Sk) ? reinterpret_cast<const uint32_t*>(a.k)[(hk + (j0 + r) * D) / 2 + c] : 0u;
-      }
+      sK[r][c] = in ? kg[hk + (j0 + r) * D + c] : 0.0f;
+      sV[r][c] = in ? vg[hk + (j0 + r) * D + c] : 0.0f;
     }
     __syncthreads();
     if (!ok) continue;
@@ -526,12 +513,8 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float x = sT[(w[r >> 2] >> (8 * (r & 3))) & 0xffu];
-        if constexpr (IN_BF16) {
-          x = fmaf(dot_bf16<DP>(qp, sKp[r0 + r], 0.0f), a.scale, x);
-        } else {
 #pragma unroll
-          for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[r0 + r][c], x);
-        }
+        for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[r0 + r][c], x);
         sc[r] = (r0 + r < nk) ? x : -INFINITY;
         bm = fmaxf(bm, sc[r]);
       }
@@ -561,15 +544,9 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
     lse_merge_weights(a.lse[(int64_t)h * a.Sq + i], lse_out, wo, wb, lse_out);
     inv *= wb;
   }
-  if constexpr (IN_BF16 && !OUT_F32) {
-    uint16_t* op = reinterpret_cast<uint16_t*>(a.o) + hq + i * D;
+  float* op = reinterpret_cast<float*>(a.o) + hq + i * D;
 #pragma unroll
-    for (int c = 0; c < D; ++c) op[c] = f2bf(acc[c] * inv);
-  } else {
-    float* op = reinterpret_cast<float*>(a.o) + hq + i * D;
-#pragma unroll
-    for (int c = 0; c < D; ++c) op[c] = wo != 0.0f ? fmaf(op[c], wo, acc[c] * inv) : acc[c] * inv;
-  }
+  for (int c = 0; c < D; ++c) op[c] = wo != 0.0f ? fmaf(op[c], wo, acc[c] * inv) : acc[c] * inv;
   a.lse[(int64_t)h * a.Sq + i] = lse_out;
 }
 
@@ -597,18 +574,6 @@ hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t s) {
   }
   return hipGetLastError();
 }
-template <int D>
-hipError_t launch_fwd_valu(const FwdArgs& a, bool bf16, bool out_f32, hipStream_t s) {
-  const dim3 grid((unsigned)((a.Sq + 127) / 128 * a.H));
-  if (!bf16)
-    hipLaunchKernelGGL((fwd_valu_kernel<D, false, true>), grid, dim3(128), 0, s, a);
-  else if (out_f32)
-    hipLaunchKernelGGL((fwd_valu_kernel<D, true, true>), grid, dim3(128), 0, s, a);
-  else
-    hipLaunchKernelGGL((fwd_valu_kernel<D, true, false>), grid, dim3(128), 0, s, a);
-  return hipGetLastError();
-}
-
 }  // namespace
 
 hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStream_t s) {
@@ -622,12 +587,14 @@ hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStrea
       default: return out_f32 ? launch_fwd_bf16<64, 64, true>(a, s) : launch_fwd_bf16<64, 64, false>(a, s);
     }
   }
+  const dim3 grid((unsigned)((a.Sq + 127) / 128 * a.H));
   switch (d) {
-    case 8: return launch_fwd_valu<8>(a, bf16, out_f32, s);
-    case 16: return launch_fwd_valu<16>(a, bf16, out_f32, s);
-    case 32: return launch_fwd_valu<32>(a, bf16, out_f32, s);
-    default: return launch_fwd_valu<64>(a, bf16, out_f32, s);
+    case 8: hipLaunchKernelGGL((fwd_valu_kernel<8>), grid, dim3(128), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((fwd_valu_kernel<16>), grid, dim3(128), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((fwd_valu_kernel<32>), grid, dim3(128), 0, s, a); break;
+    default: hipLaunchKernelGGL((fwd_valu_kernel<64>), grid, dim3(128), 0, s, a); break;
   }
+  return hipGetLastError();
 }
 
 }  // namespace gt

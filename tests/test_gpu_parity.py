@@ -168,7 +168,7 @@ def test_masked_rows_and_neg_inf_table(dt):
     (256, 320, 64, 128, 512, 64),     # 16-byte aligned slice: vector loads
     (129, 1, 3, 500, 512, 64),        # single key
     (64, 77, 0, 0, 77, 64),           # ld not a multiple of 16
-    (100, 150, 5, 40, 256, 8),        # small head dims (vector-ALU path)
+    (100, 150, 5, 40, 256, 8),        # small head dim (zero-padded 32-wide tiles for bf16)
     (70, 64, 0, 64, 128, 16),
 ])
 def test_ring_step_offsets(Sq, Sk, row_off, col_off, ld, d, dt):
