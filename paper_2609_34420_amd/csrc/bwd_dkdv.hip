@@ -323,10 +323,9 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   bf16x8 kf[NKC], vf[NKC];
 #pragma unroll
   for (int kc = 0; kc < NKC; ++kc) {
-    const int f0 = kc * 16 + g * 8;
-    const bool in = jok && f0 < DS;
-    kf[kc] = in ? *reinterpret_cast<const bf16x8*>(kh + j * DS + f0) : zero_bf16x8();
-    const bf16x8 v8 = in ? *reinterpret_cast<const bf16x8*>(vh + j * DS + f0) : zero_bf16x8();
+    const bool in = jok && kc * 16 + g * 8 < DS;
+    kf[kc] = in ? *reinterpret_cast<const bf16x8*>(kh + j * DS + kc * 16 + g * 8) : zero_bf16x8();
+    const bf16x8 v8 = in ? *reinterpret_cast<const bf16x8*>(vh + j * DS + kc * 16 + g * 8) : zero_bf16x8();
 #pragma unroll
     for (int e = 0; e < 8; ++e) vf[kc][e] = (__bf16)((float)v8[e] * sF);
   }

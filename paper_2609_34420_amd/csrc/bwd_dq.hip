@@ -152,9 +152,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_bf16_kernel(BwdArgs a) {
   const int64_t qrow = i < a.Sq ? i : a.Sq - 1;
 #pragma unroll
   for (int kc = 0; kc < NKC; ++kc) {
-    const int f0 = kc * 16 + g * 8;
-    ln.qf[kc] = f0 < DS ? *reinterpret_cast<const bf16x8*>(qh + qrow * DS + f0) : zero_bf16x8();
-    ln.df[kc] = f0 < DS ? *reinterpret_cast<const bf16x8*>(oh + qrow * DS + f0) : zero_bf16x8();
+    const bool in = DS == D || kc * 16 + g * 8 < DS;
+    ln.qf[kc] = in ? *reinterpret_cast<const bf16x8*>(qh + qrow * DS + kc * 16 + g * 8) : zero_bf16x8();
+    ln.df[kc] = in ? *reinterpret_cast<const bf16x8*>(oh + qrow * DS + kc * 16 + g * 8) : zero_bf16x8();
   }
   {
     const float l2 = a.lse2[(int64_t)h * a.Sq + qrow];

@@ -232,8 +232,10 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
     qrow[qb] = i < a.Sq ? i : a.Sq - 1;
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
-      const int f0 = kc * 16 + g * 8;
-      qf[qb][kc] = f0 < DS ? *reinterpret_cast<const bf16x8*>(qh + qrow[qb] * DS + f0) : zero_bf16x8();
+      if (DS == D || kc * 16 + g * 8 < DS)
+        qf[qb][kc] = *reinterpret_cast<const bf16x8*>(qh + qrow[qb] * DS + kc * 16 + g * 8);
+      else
+        qf[qb][kc] = zero_bf16x8();
     }
   }
 

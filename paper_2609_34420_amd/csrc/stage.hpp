@@ -84,7 +84,12 @@ struct RowStage {
   }
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs) {
 #pragma unroll
-    for (int s = 0; s < IPT; ++s) r[s] = buf_b128(rs, src_chunk_off<DS>(item(s) / CPR, item(s) % CPR));
+    for (int s = 0; s < IPT; ++s) {
+      if constexpr (DS == D)
+        r[s] = buf_b128(rs, (uint32_t)item(s) * 16u);
+      else
+        r[s] = buf_b128(rs, src_chunk_off<DS>(item(s) / CPR, item(s) % CPR));
+    }
   }
   // LDS element offset of this thread's item s.
   __device__ __forceinline__ static int lds_off(int s) {
@@ -133,7 +138,10 @@ struct TileDma {
       lds_byte[i] = lb * 1024;
       const int row = lb * RPB + lane / (D / 8);
       const int chunk = swz_tile<D>(row, lane % (D / 8));   // involution: logical chunk here
-      voff[i] = src_chunk_off<DS>(row, chunk);
+      if constexpr (DS == D)
+        voff[i] = (uint32_t)(row * ROWB + chunk * 16);
+      else
+        voff[i] = src_chunk_off<DS>(row, chunk);
     }
   }
   __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs0, __amdgpu_buffer_rsrc_t rs1,
