@@ -55,6 +55,10 @@ def parse():
                    help="also time one read-only pass over the resident spd matrix (a torch "
                         "reduction over it as int64 words: the achievable rate for the spd "
                         "stream) and add it to the line")
+    p.add_argument("--batch", default=None, metavar="B,N,d",
+                   help="instead of the headline, time a batch of B graphs of N nodes (H = 8, "
+                        "head dim d, bf16, 64 spd buckets, i.i.d. uniform spd per graph) through "
+                        "the batched entry points and print one JSON line for it")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run one plain 1 GiB device copy before the timed region (its "
                         "FETCH_SIZE / WRITE_SIZE counters calibrate the kernels')")
@@ -240,6 +244,65 @@ def cpu_baseline(w, args):
                        f"host {platform.processor() or platform.machine()}, os.cpu_count()={os.cpu_count()}")}
 
 
+def run_batch(args):
+    """Batches of short graphs (the paper's training batches of sampled
+    sequences) through gt_attn_fwd_batch / gt_attn_bwd_batch."""
+    import torch
+
+    import paper_2609_34420_amd as gt
+
+    B, N, d = (int(x) for x in args.batch.split(","))
+    H, nb = 8, 64
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed)
+    shape = (B, H, N, d)
+    q, k, v = ((torch.randn(shape, device=dev, generator=g) / math.sqrt(d)).bfloat16() for _ in range(3))
+    do = torch.randn(shape, device=dev, generator=g).bfloat16()
+    spd = torch.randint(0, nb, (B, N, N), dtype=torch.uint8, device=dev, generator=g)
+    table = torch.randn(H, nb, device=dev, generator=g) * 0.02
+    scale = 1.0 / math.sqrt(d)
+    O = torch.empty_like(q)
+    L = torch.empty((B, H, N), dtype=torch.float32, device=dev)
+    grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v), torch.empty_like(table))
+    ws = torch.empty(gt.gt_attn_bwd_workspace_size(B * H, N, d, torch.bfloat16), dtype=torch.uint8,
+                     device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        gt.gt_attn_fwd_batch(q, k, v, spd, table, scale=scale, out=O, lse=L)
+        if ev is not None:
+            ev[1].record(stream)
+        gt.gt_attn_bwd_batch(q, k, v, spd, table, O, L, do, scale=scale, workspace=ws, grads=grads)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    fwd = [e[0].elapsed_time(e[1]) for e in evs]
+    bwd = [e[1].elapsed_time(e[2]) for e in evs]
+    ms = sum(f + b for f, b in zip(fwd, bwd)) / args.steps
+    elems = float(B) * H * N * N
+    flop = 14.0 * elems * d
+    print(json.dumps({
+        "metric": f"batched biased-attention fwd+bwd at B={B}, N={N}, H={H}, d={d}",
+        "value": flop / (ms * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "dtype": "bf16",
+        "data": "synthetic", "score_elements_per_ns": elems / (ms * 1e6),
+        "kernel_ms": {"fwd": sum(fwd) / len(fwd), "bwd": sum(bwd) / len(bwd)},
+        "config": {"workload": f"batch of {B} graphs of {N} nodes, i.i.d. uniform spd over {nb} "
+                               f"buckets, H={H}, d={d}, bf16", "parallelism": "single GPU"},
+    }), flush=True)
+
+
 def graph_label(w) -> str:
     kind = w.graph[0]
     if kind == "sbm":
@@ -257,6 +320,9 @@ def main():
                           "ring across GPUs is not built (see the single-GPU ring step), "
                           f"asked for --gpus {args.gpus} / WORLD_SIZE {world}"}))
         sys.exit(2)
+    if args.batch:
+        run_batch(args)
+        return
     import torch
 
     import synth
