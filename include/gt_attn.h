@@ -159,6 +159,34 @@ gt_status_t gt_attn_bwd_phase(int32_t phase,
                               int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
                               float scale, void* stream);
 
+/* Calling convention of a rank's whole ring (Section III-A-1 parts 1-3), for
+ * the entry points below. P ranks split the N' regular nodes into P
+ * contiguous blocks [b_r, b_{r+1}); the batch may also hold N_s super nodes
+ * (global nodes, ids N' .. N' + N_s - 1) that every rank replicates.
+ *   - Rank r's query shard is its regular rows [b_r, b_{r+1}) followed by
+ *     every super-node row, and it holds only those rows of spd (its bias
+ *     shard, [b_{r+1} - b_r + N_s, N' + N_s]); row_off indexes that shard.
+ *   - At step t = 0 .. P-1 the rank holds regular KV block (r - t) mod P and
+ *     calls a ring step with col_off = that block's first node id. With
+ *     N_s > 0 it then makes ONE more step over the super-node KV block,
+ *     col_off = N'. The paper places the super nodes in every KV block; read
+ *     literally, every super-node key would then enter each row's softmax P
+ *     times, so the super block is visited once instead and every key counts
+ *     exactly once (the merged result equals the unsharded attention over
+ *     all N' + N_s nodes).
+ *   - The forward merges the P (+1) partials: gt_attn_ring_step for the
+ *     first step, gt_attn_ring_step_acc for the others (or partials and
+ *     gt_attn_merge). Every rank computes the same super-node rows.
+ *   - The backward visits the same blocks in the same order with
+ *     gt_attn_bwd_ring_step, using the merged O and LSE. The replicated
+ *     super-node rows' loss must count once: rank 0 passes their dO and
+ *     every other rank passes zeros for those rows. dK/dV of a block
+ *     accumulate over every rank's step on it (the accumulators travel with
+ *     the block); dQ of a super-node row is the sum of its rows' dq_acc over
+ *     the ranks (only rank 0's is nonzero); dtable is summed over the ranks.
+ * The Python binding's paper_2609_34420_amd.ring module returns these
+ * shards and step lists. */
+
 /* One step of graph-aware context parallelism (Section III-A-1: ring-based
  * KV rotation, query-dimension bias sharding, Eq. (2)). A rank holding the
  * query shard q_shard and, at this step, one KV block computes the block's

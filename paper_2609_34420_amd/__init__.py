@@ -131,21 +131,81 @@ def _need(cond: bool, msg: str):
         raise ValueError(msg)
 
 
-def _dev_contig(*ts):
+# Argument checks. Every entry point checks each tensor's shape and dtype
+# against q (and table) first, then that all tensors are contiguous tensors
+# on q's device, all before anything is launched: a wrong shape raises
+# ValueError instead of becoming an out-of-bounds device access.
+
+_HEAD_DIMS = (8, 16, 32, 64)
+
+
+def _shape(t, name: str, shape, dtype=None):
+    _need(isinstance(t, torch.Tensor), f"{name} must be a tensor")
+    _need(tuple(t.shape) == tuple(shape), f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if dtype is not None:
+        _need(t.dtype == dtype, f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _qdims(q, name: str, ndim: int):
+    _need(isinstance(q, torch.Tensor) and q.dim() == ndim, f"{name} must be a {ndim}-D tensor")
+    _need(q.dtype in (torch.bfloat16, torch.float32), f"{name} must be bfloat16 or float32, got {q.dtype}")
+    _need(q.shape[-1] in _HEAD_DIMS, f"head dim must be one of {_HEAD_DIMS}, got {q.shape[-1]}")
+    _need(all(n >= 1 for n in q.shape), f"{name} must not be empty")
+    return q.dtype
+
+
+def _table(table, H: int):
+    _need(isinstance(table, torch.Tensor) and table.dim() == 2 and table.shape[0] == H
+          and table.dtype == torch.float32, f"table must be fp32 [H={H}, n_buckets]")
+    _need(1 <= table.shape[1] <= 256, f"table must have 1..256 buckets, got {table.shape[1]}")
+
+
+def _devices(ref, *ts, contiguous=True):
+    """Every tensor is a device tensor on ref's device (and contiguous)."""
+    _need(ref.is_cuda, "tensors must be device tensors")
     for t in ts:
-        if t is not None:
-            _need(t.is_cuda and t.is_contiguous(), "tensors must be contiguous device tensors")
+        if t is None:
+            continue
+        _need(t.is_cuda and t.device == ref.device, "tensors must be device tensors on one device")
+        if contiguous:
+            _need(t.is_contiguous(), "tensors must be contiguous")
+
+
+def _spd_view(spd, rows_needed: int, cols_needed: int, name: str = "spd"):
+    """A 2-D uint8 spd shard with unit column stride that holds rows
+    [0, rows_needed) and columns [0, cols_needed) of what the step reads
+    (the row stride is passed on as ld_spd, so a column-sliced view must
+    not let the step read past its last column)."""
+    _need(isinstance(spd, torch.Tensor) and spd.dtype == torch.uint8 and spd.dim() == 2
+          and spd.stride(1) == 1, f"{name} must be a uint8 2-D tensor with unit column stride")
+    _need(rows_needed <= spd.shape[0], f"{name} has {spd.shape[0]} rows; the step reads rows up to {rows_needed}")
+    _need(cols_needed <= spd.shape[1],
+          f"{name} has {spd.shape[1]} columns; the step reads columns up to {cols_needed}")
+
+
+def _workspace(ws, need: int, ref):
+    _need(isinstance(ws, torch.Tensor) and ws.dtype == torch.uint8 and ws.dim() == 1
+          and ws.is_contiguous(), "workspace must be a contiguous uint8 1-D tensor")
+    _need(ws.numel() >= need, f"workspace holds {ws.numel()} bytes; {need} are needed")
+    _need(ws.is_cuda and ws.device == ref.device, "workspace must be on the tensors' device")
+    _need(ws.data_ptr() % 256 == 0, "workspace must be 256-byte aligned")
 
 
 def gt_attn_fwd(q, k, v, spd, table, scale: float | None = None, out=None, lse=None,
                 stream=None):
     """O, LSE of biased attention over all N nodes (C ABI gt_attn_fwd).
     q, k, v [H, N, d] bf16|fp32; spd [N, N] uint8; table [H, n_buckets] fp32."""
+    dt = _qdims(q, "q", 3)
     H, N, d = q.shape
-    _dev_contig(q, k, v, spd, table, out, lse)
-    _need(spd.dtype == torch.uint8 and tuple(spd.shape) == (N, N), "spd must be uint8 [N, N]")
-    _need(table.dtype == torch.float32 and table.dim() == 2 and table.shape[0] == H,
-          "table must be fp32 [H, n_buckets]")
+    _shape(k, "k", q.shape, dt)
+    _shape(v, "v", q.shape, dt)
+    _shape(spd, "spd", (N, N), torch.uint8)
+    _table(table, H)
+    if out is not None:
+        _shape(out, "out", q.shape, dt)
+    if lse is not None:
+        _shape(lse, "lse", (H, N), torch.float32)
+    _devices(q, k, v, spd, table, out, lse)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     if out is None:
         out = torch.empty_like(q)
@@ -171,23 +231,46 @@ def gt_attn_bwd(q, k, v, spd, table, o, lse, d_o, scale: float | None = None,
                              spd_t)
 
 
+def _check_bwd(q, k, v, spd, table, o, lse, d_o, grads, spd_t, lead):
+    """Shapes of a (batched) backward: q [*lead, N, d]; spd [N, N] (or
+    [B, N, N] / [N, N] for a batch, checked by the caller)."""
+    dt = q.dtype
+    N = q.shape[-2]
+    for name, t in (("k", k), ("v", v), ("o", o), ("d_o", d_o)):
+        _shape(t, name, q.shape, dt)
+    _shape(lse, "lse", tuple(q.shape[:-1]), torch.float32)
+    H = q.shape[-3]
+    _table(table, H)
+    if spd_t is not None:
+        _need(isinstance(spd_t, torch.Tensor) and tuple(spd_t.shape) == tuple(spd.shape)
+              and spd_t.dtype == spd.dtype and spd_t.stride() == spd.stride(),
+              "spd_t must have the shape and layout of spd")
+    if grads is not None:
+        _need(len(grads) == 4, "grads must be (dq, dk, dv, dtable)")
+        for name, t in zip(("dq", "dk", "dv"), grads[:3]):
+            _shape(t, name, q.shape, dt)
+        _shape(grads[3], "dtable", table.shape, torch.float32)
+    return N
+
+
 def gt_attn_bwd_phase(phase: int, q, k, v, spd, table, o, lse, d_o, scale: float | None = None,
                       workspace=None, grads=None, stream=None, spd_t=None):
     """One stage of the backward (C ABI gt_attn_bwd_phase): 0 prepare,
     1 dK/dV/dtable, 2 dQ; phase -1 runs gt_attn_bwd (all three)."""
+    _need(phase in (-1, 0, 1, 2), f"phase must be -1, 0, 1 or 2, got {phase}")
+    _qdims(q, "q", 3)
     H, N, d = q.shape
-    _dev_contig(q, k, v, spd, table, o, lse, d_o)
-    if spd_t is not None:
-        _dev_contig(spd_t)
-        if tuple(spd_t.shape) != tuple(spd.shape) or spd_t.dtype != spd.dtype:
-            raise ValueError("spd_t must have the shape and dtype of spd")
+    _shape(spd, "spd", (N, N), torch.uint8)
+    _check_bwd(q, k, v, spd, table, o, lse, d_o, grads, spd_t, (H,))
+    need = gt_attn_bwd_workspace_size(H, N, d, q.dtype)
+    _devices(q, k, v, spd, table, o, lse, d_o, spd_t, *(grads or ()))
+    if workspace is not None:
+        _workspace(workspace, need, q)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     if grads is None:
         grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
                  torch.empty_like(table))
     dq, dk, dv, dtable = grads
-    _dev_contig(dq, dk, dv, dtable)
-    need = gt_attn_bwd_workspace_size(H, N, d, q.dtype)
     if workspace is None:
         workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
     args = (_ptr(q), _ptr(k), _ptr(v), _ptr(spd), None if spd_t is None else _ptr(spd_t),
@@ -203,8 +286,8 @@ def gt_attn_bwd_phase(phase: int, q, k, v, spd, table, o, lse, d_o, scale: float
 
 
 def _batch_spd(spd, B, N):
-    _need(spd.dtype == torch.uint8 and spd.dim() in (2, 3) and tuple(spd.shape[-2:]) == (N, N),
-          "spd must be uint8 [B, N, N] or [N, N] (shared by the batch)")
+    _need(isinstance(spd, torch.Tensor) and spd.dtype == torch.uint8 and spd.dim() in (2, 3)
+          and tuple(spd.shape[-2:]) == (N, N), "spd must be uint8 [B, N, N] or [N, N] (shared by the batch)")
     if spd.dim() == 2:
         return 0
     _need(spd.shape[0] == B, "spd must hold one [N, N] matrix per graph")
@@ -215,11 +298,17 @@ def gt_attn_fwd_batch(q, k, v, spd, table, scale: float | None = None, out=None,
                       stream=None):
     """O, LSE of a batch of graphs (C ABI gt_attn_fwd_batch). q, k, v
     [B, H, N, d]; spd [B, N, N] uint8 (or [N, N] shared); table [H, nb]."""
+    dt = _qdims(q, "q", 4)
     B, H, N, d = q.shape
-    _dev_contig(q, k, v, spd, table, out, lse)
+    _shape(k, "k", q.shape, dt)
+    _shape(v, "v", q.shape, dt)
     stride = _batch_spd(spd, B, N)
-    _need(table.dtype == torch.float32 and table.dim() == 2 and table.shape[0] == H,
-          "table must be fp32 [H, n_buckets]")
+    _table(table, H)
+    if out is not None:
+        _shape(out, "out", q.shape, dt)
+    if lse is not None:
+        _shape(lse, "lse", (B, H, N), torch.float32)
+    _devices(q, k, v, spd, table, out, lse)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     if out is None:
         out = torch.empty_like(q)
@@ -236,20 +325,19 @@ def gt_attn_bwd_batch(q, k, v, spd, table, o, lse, d_o, scale: float | None = No
                       workspace=None, grads=None, stream=None, spd_t=None):
     """dQ, dK, dV [B, H, N, d] and dTable [H, nb] summed over the batch (C ABI
     gt_attn_bwd_batch); spd_t, if given, has spd's shape."""
+    _qdims(q, "q", 4)
     B, H, N, d = q.shape
-    _dev_contig(q, k, v, spd, table, o, lse, d_o)
     stride = _batch_spd(spd, B, N)
-    if spd_t is not None:
-        _dev_contig(spd_t)
-        _need(tuple(spd_t.shape) == tuple(spd.shape) and spd_t.dtype == spd.dtype and
-              spd_t.stride() == spd.stride(), "spd_t must have the shape and layout of spd")
+    _check_bwd(q, k, v, spd, table, o, lse, d_o, grads, spd_t, (B, H))
+    need = gt_attn_bwd_workspace_size(B * H, N, d, q.dtype)
+    _devices(q, k, v, spd, table, o, lse, d_o, spd_t, *(grads or ()))
+    if workspace is not None:
+        _workspace(workspace, need, q)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     if grads is None:
         grads = (torch.empty_like(q), torch.empty_like(k), torch.empty_like(v),
                  torch.empty_like(table))
     dq, dk, dv, dtable = grads
-    _dev_contig(dq, dk, dv, dtable)
-    need = gt_attn_bwd_workspace_size(B * H, N, d, q.dtype)
     if workspace is None:
         workspace = torch.empty(need, device=q.device, dtype=torch.uint8)
     st = lib().gt_attn_bwd_batch(_ptr(q), _ptr(k), _ptr(v), _ptr(spd),
@@ -262,26 +350,49 @@ def gt_attn_bwd_batch(q, k, v, spd, table, o, lse, d_o, scale: float | None = No
     return dq, dk, dv, dtable
 
 
+def _check_kv_block(q_shard, k_shard, v_shard):
+    """KV block [H, Sk, d] of q_shard's dtype, or None for an empty block;
+    returns Sk."""
+    if k_shard is None and v_shard is None:
+        return 0
+    H, _, d = q_shard.shape
+    _need(isinstance(k_shard, torch.Tensor) and k_shard.dim() == 3, "k_shard must be [H, Sk, d]")
+    Sk = k_shard.shape[1]
+    _shape(k_shard, "k_shard", (H, Sk, d), q_shard.dtype)
+    _shape(v_shard, "v_shard", (H, Sk, d), q_shard.dtype)
+    return Sk
+
+
 def gt_attn_ring_step(q_shard, k_shard, v_shard, spd, row_off: int, col_off: int, table,
                       scale: float | None = None, out=None, lse=None, stream=None):
     """Partial (O_p fp32, LSE_p) of one context-parallel step (C ABI
     gt_attn_ring_step). spd: uint8 2-D tensor, element (r, c) = spd[r, c];
-    its row stride is ld_spd."""
+    its row stride is ld_spd, and it must hold rows row_off .. row_off + Sq - 1
+    and columns col_off .. col_off + Sk - 1."""
+    _qdims(q_shard, "q_shard", 3)
     H, Sq, d = q_shard.shape
-    Sk = k_shard.shape[1] if k_shard is not None else 0
-    _dev_contig(q_shard, k_shard, v_shard, table, out, lse)
-    _need(spd is None or (spd.dtype == torch.uint8 and spd.dim() == 2 and spd.stride(1) == 1),
-          "spd must be a uint8 2-D tensor with unit column stride")
+    Sk = _check_kv_block(q_shard, k_shard, v_shard)
+    _need(int(row_off) >= 0 and int(col_off) >= 0, "row_off and col_off must be >= 0")
+    if Sk > 0:
+        _spd_view(spd, int(row_off) + Sq, int(col_off) + Sk)
+    _table(table, H)
+    if out is not None:
+        _shape(out, "out", (H, Sq, d), torch.float32)
+    if lse is not None:
+        _shape(lse, "lse", (H, Sq), torch.float32)
+    _devices(q_shard, k_shard, v_shard, table, out, lse)
+    if Sk > 0:
+        _devices(q_shard, spd, contiguous=False)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     if out is None:
         out = torch.empty((H, Sq, d), device=q_shard.device, dtype=torch.float32)
     if lse is None:
         lse = torch.empty((H, Sq), device=q_shard.device, dtype=torch.float32)
-    ld = spd.stride(0) if spd is not None else 0
+    ld = spd.stride(0) if (spd is not None and Sk > 0) else 0
     st = lib().gt_attn_ring_step(_ptr(q_shard), Sq, _ptr(k_shard), _ptr(v_shard), Sk,
-                                 _ptr(spd), ld, int(row_off), int(col_off), _ptr(table),
-                                 table.shape[1], _ptr(out), _ptr(lse), H, d, _dt(q_shard),
-                                 scale, _stream(stream))
+                                 _ptr(spd) if Sk > 0 else None, ld, int(row_off), int(col_off),
+                                 _ptr(table), table.shape[1], _ptr(out), _ptr(lse), H, d,
+                                 _dt(q_shard), scale, _stream(stream))
     _check(st, "gt_attn_ring_step")
     return out, lse
 
@@ -292,21 +403,25 @@ def gt_attn_ring_step_acc(q_shard, k_shard, v_shard, spd, row_off: int, col_off:
     (o_acc fp32 [H, Sq, d], lse_acc fp32 [H, Sq]) (C ABI
     gt_attn_ring_step_acc); returns the state. The first step's
     gt_attn_ring_step output is a valid starting state."""
+    _qdims(q_shard, "q_shard", 3)
     H, Sq, d = q_shard.shape
-    Sk = k_shard.shape[1] if k_shard is not None else 0
+    Sk = _check_kv_block(q_shard, k_shard, v_shard)
+    _need(int(row_off) >= 0 and int(col_off) >= 0, "row_off and col_off must be >= 0")
+    if Sk > 0:
+        _spd_view(spd, int(row_off) + Sq, int(col_off) + Sk)
+    _table(table, H)
+    _need(len(state) == 2, "state must be (o_acc, lse_acc)")
     o_acc, lse_acc = state
-    _dev_contig(q_shard, k_shard, v_shard, table, o_acc, lse_acc)
-    _need(spd is None or (spd.dtype == torch.uint8 and spd.dim() == 2 and spd.stride(1) == 1),
-          "spd must be a uint8 2-D tensor with unit column stride")
-    _need(o_acc.dtype == torch.float32 and tuple(o_acc.shape) == (H, Sq, d),
-          "o_acc must be fp32 [H, Sq, d]")
-    _need(lse_acc.dtype == torch.float32 and tuple(lse_acc.shape) == (H, Sq),
-          "lse_acc must be fp32 [H, Sq]")
+    _shape(o_acc, "o_acc", (H, Sq, d), torch.float32)
+    _shape(lse_acc, "lse_acc", (H, Sq), torch.float32)
+    _devices(q_shard, k_shard, v_shard, table, o_acc, lse_acc)
+    if Sk > 0:
+        _devices(q_shard, spd, contiguous=False)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
-    ld = spd.stride(0) if spd is not None else 0
+    ld = spd.stride(0) if (spd is not None and Sk > 0) else 0
     st = lib().gt_attn_ring_step_acc(_ptr(q_shard), Sq, _ptr(k_shard), _ptr(v_shard), Sk,
-                                     _ptr(spd), ld, int(row_off), int(col_off), _ptr(table),
-                                     table.shape[1], _ptr(o_acc), _ptr(lse_acc), H, d,
+                                     _ptr(spd) if Sk > 0 else None, ld, int(row_off), int(col_off),
+                                     _ptr(table), table.shape[1], _ptr(o_acc), _ptr(lse_acc), H, d,
                                      _dt(q_shard), scale, _stream(stream))
     _check(st, "gt_attn_ring_step_acc")
     return o_acc, lse_acc
@@ -324,11 +439,28 @@ def gt_attn_bwd_ring_step(q_shard, o_shard, lse_shard, d_o_shard, k_blk, v_blk, 
     fp32 accumulators acc = (dq [H,Sq,d], dk [H,Sk,d], dv [H,Sk,d],
     dtable [H,n_buckets]); acc=None starts them at zero. o_shard / lse_shard
     are the merged forward results of the shard's rows."""
+    dt = _qdims(q_shard, "q_shard", 3)
     H, Sq, d = q_shard.shape
-    Sk = k_blk.shape[1] if k_blk is not None else 0
-    _dev_contig(q_shard, o_shard, lse_shard, d_o_shard, k_blk, v_blk, table)
-    _need(spd is None or (spd.dtype == torch.uint8 and spd.dim() == 2 and spd.stride(1) == 1),
-          "spd must be a uint8 2-D tensor with unit column stride")
+    _shape(o_shard, "o_shard", q_shard.shape, dt)
+    _shape(d_o_shard, "d_o_shard", q_shard.shape, dt)
+    _shape(lse_shard, "lse_shard", (H, Sq), torch.float32)
+    Sk = _check_kv_block(q_shard, k_blk, v_blk)
+    _need(int(row_off) >= 0 and int(col_off) >= 0, "row_off and col_off must be >= 0")
+    if Sk > 0:
+        _spd_view(spd, int(row_off) + Sq, int(col_off) + Sk)
+    _table(table, H)
+    if acc is not None:
+        _need(len(acc) == 4, "acc must be (dq, dk, dv, dtable)")
+        _shape(acc[0], "dq accumulator", (H, Sq, d), torch.float32)
+        _shape(acc[1], "dk accumulator", (H, Sk, d), torch.float32)
+        _shape(acc[2], "dv accumulator", (H, Sk, d), torch.float32)
+        _shape(acc[3], "dtable accumulator", table.shape, torch.float32)
+    need = gt_attn_bwd_ring_workspace_size(H, Sq, Sk, d, q_shard.dtype)
+    _devices(q_shard, o_shard, lse_shard, d_o_shard, k_blk, v_blk, table, *(acc or ()))
+    if Sk > 0:
+        _devices(q_shard, spd, contiguous=False)
+    if workspace is not None:
+        _workspace(workspace, need, q_shard)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     dev = q_shard.device
     if acc is None:
@@ -337,16 +469,12 @@ def gt_attn_bwd_ring_step(q_shard, o_shard, lse_shard, d_o_shard, k_blk, v_blk, 
                torch.zeros((H, Sk, d), device=dev, dtype=torch.float32),
                torch.zeros_like(table))
     dq, dk, dv, dtable = acc
-    _dev_contig(dq, dk, dv, dtable)
-    for t in acc:
-        _need(t.dtype == torch.float32, "accumulators must be fp32")
-    need = gt_attn_bwd_ring_workspace_size(H, Sq, Sk, d, q_shard.dtype)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=dev, dtype=torch.uint8)
-    ld = spd.stride(0) if spd is not None else 0
+    ld = spd.stride(0) if (spd is not None and Sk > 0) else 0
     st = lib().gt_attn_bwd_ring_step(
         _ptr(q_shard), _ptr(o_shard), _ptr(lse_shard), _ptr(d_o_shard), Sq,
-        _ptr(k_blk), _ptr(v_blk), Sk, _ptr(spd), ld, int(row_off), int(col_off),
+        _ptr(k_blk), _ptr(v_blk), Sk, _ptr(spd) if Sk > 0 else None, ld, int(row_off), int(col_off),
         _ptr(table), table.shape[1], _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dtable),
         _ptr(workspace), workspace.numel() * workspace.element_size(), H, d, _dt(q_shard),
         scale, _stream(stream))
@@ -356,8 +484,20 @@ def gt_attn_bwd_ring_step(q_shard, o_shard, lse_shard, d_o_shard, k_blk, v_blk, 
 
 def gt_attn_merge(o_parts, lse_parts, dtype=torch.bfloat16, out=None, lse=None, stream=None):
     """Combine partials [P, H, S, d] / [P, H, S] (C ABI gt_attn_merge)."""
+    _need(isinstance(o_parts, torch.Tensor) and o_parts.dim() == 4 and o_parts.dtype == torch.float32,
+          "o_parts must be fp32 [P, H, S, d]")
     P, H, S, d = o_parts.shape
-    _dev_contig(o_parts, lse_parts, out, lse)
+    _need(d in _HEAD_DIMS, f"head dim must be one of {_HEAD_DIMS}, got {d}")
+    _need(P >= 1 and H >= 1 and S >= 1, "o_parts must not be empty")
+    _shape(lse_parts, "lse_parts", (P, H, S), torch.float32)
+    if out is not None:
+        _need(out.dtype in (torch.bfloat16, torch.float32), "out must be bfloat16 or float32")
+        _shape(out, "out", (H, S, d))
+    else:
+        _need(dtype in (torch.bfloat16, torch.float32), "dtype must be bfloat16 or float32")
+    if lse is not None:
+        _shape(lse, "lse", (H, S), torch.float32)
+    _devices(o_parts, lse_parts, out, lse)
     if out is None:
         out = torch.empty((H, S, d), device=o_parts.device, dtype=dtype)
     if lse is None:

@@ -13,6 +13,7 @@ import torch
 import oracle
 import paper_2609_34420_amd as gt
 import synth
+from paper_2609_34420_amd import ring
 from gpu_common import DEV, TOL, check_fwd, check_grads, rel_l2, say, tdtype, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
@@ -228,12 +229,15 @@ def test_context_parallel_super_nodes(n_reg, n_super, bounds, d, dt):
     acc_v = {c: torch.zeros(H, e - c, d, device=DEV) for c, e in blocks + [(n_reg, N)]}
     o_sup = []
     for r in range(P):
-        rows = oracle.super_shard_rows(bounds, N, n_super, r)
+        # the schedule of the documented calling convention
+        rows = np.array(ring.shard_rows(bounds, r, n_super))
+        assert np.array_equal(rows, oracle.super_shard_rows(bounds, N, n_super, r))
         nr = bounds[r + 1] - bounds[r]
         idx = torch.from_numpy(rows).to(DEV)
         shard = to_dev(spd[rows], torch.uint8)
         q_r = Q[:, idx].contiguous()
-        steps = [blocks[(r - t) % P] for t in range(P)] + [(n_reg, N)]
+        steps = ring.ring_steps(bounds, r, n_super)
+        assert steps == [blocks[(r - t) % P] for t in range(P)] + [(n_reg, N)]
         state = None
         for c0, c1 in steps:
             Kb, Vb = K[:, c0:c1].contiguous(), V[:, c0:c1].contiguous()
@@ -247,7 +251,7 @@ def test_context_parallel_super_nodes(n_reg, n_super, bounds, d, dt):
         check_fwd(f"super rank {r}", to_np(state[0]), to_np(state[1]), O_ref[:, rows], L_ref[:, rows], dt)
         o_sup.append(to_np(state[0])[:, nr:])
         do_r = dO[:, idx].contiguous()
-        if r != 0:
+        if not ring.carries_super_rows(r):
             do_r[:, nr:] = 0
         dq_r = torch.zeros(H, len(rows), d, device=DEV)
         for c0, c1 in steps:
