@@ -164,6 +164,23 @@ class Workload:
         r = np.unique(np.concatenate([r, [lo, hi - 1]]))
         return r.astype(np.int64)
 
+    def stratified_rows(self, count: int, block: int = 256, seed: int = 0, lo: int = 0,
+                        hi: int | None = None):
+        """Sorted seeded row sample in [lo, hi): the range is cut into blocks
+        of `block` rows and each block contributes the same number of rows
+        (at least one, at most the block's size), drawn without replacement,
+        plus both ends of the range. Every block of the kernels' row tiles
+        (any multiple of `block`) then holds a sampled row."""
+        hi = self.N if hi is None else hi
+        g = rng(seed, "rows")
+        nblk = (hi - lo + block - 1) // block
+        per = max(1, -(-count // nblk))
+        picks = [np.array([lo, hi - 1])]
+        for b in range(nblk):
+            a, e = lo + b * block, min(hi, lo + (b + 1) * block)
+            picks.append(g.choice(np.arange(a, e), size=min(per, e - a), replace=False))
+        return np.unique(np.concatenate(picks)).astype(np.int64)
+
 
 def _spd_seed(seed: int) -> int:
     return int(np.random.SeedSequence(entropy=int(seed),

@@ -72,3 +72,29 @@ def check_grads(tag, got: dict, ref: dict, dt):
         say(f"{tag}: {name} rel-L2 {e:.3e}")
         assert np.isfinite(got[name]).all(), (tag, name, "non-finite")
         assert e <= TOL[dt]["grad"], (tag, name, e)
+
+
+def _oracle_head_job(args):
+    """One head of the oracle on query rows R against all keys: O, LSE and
+    the backward of rows R (runs in a worker process; two BLAS threads)."""
+    q, k, v, do, spd_R, table, scale, R = args
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    with threadpool_limits(2):
+        o, l = oracle.block_attention(q[:, R], k, v, spd_R, table, scale)
+        dq, dk, dv, dt = oracle.block_backward(q[:, R], k, v, spd_R, table, scale, do[:, R])
+    return o, l, dq, dk, dv, dt
+
+
+def oracle_by_head(q, k, v, do, spd_R, table, scale, R, workers=8):
+    """The oracle on rows R, each head in its own worker process (spawned,
+    numpy only: the workers never touch the GPU). Returns, per head,
+    (O, LSE, dQ of rows R, dK, dV, dtable of a dO zero outside R)."""
+    import multiprocessing
+
+    H = q.shape[0]
+    jobs = [(q[h:h + 1], k[h:h + 1], v[h:h + 1], do[h:h + 1], spd_R, table[h:h + 1], scale, R)
+            for h in range(H)]
+    with multiprocessing.get_context("spawn").Pool(min(workers, H)) as pool:
+        return pool.map(_oracle_head_job, jobs)
