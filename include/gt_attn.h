@@ -124,6 +124,31 @@ gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v,
                         int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
                         float scale, void* stream);
 
+/* gt_attn_bwd without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). The scratch that gt_attn_bwd takes as
+ * its workspace is a fixed device array inside the library instead, of
+ * gt_attn_bwd_noalloc_max_bytes() = 16 MiB on each GPU the library runs on,
+ * held until the process ends. The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); the array's device address is
+ * looked up once per device, on the first call with that device current.
+ *   Arguments, results and validation as gt_attn_bwd. Sizes whose
+ *   gt_attn_bwd_workspace_size(H, N, d, dtype) exceeds the array (H * N
+ *   above about 2.09 million rows) give GT_ERR_WORKSPACE and touch nothing;
+ *   a failed address lookup gives GT_ERR_LAUNCH.
+ *   Every call on one GPU shares that GPU's array: calls that overlap in time
+ *   on one GPU (different streams, or host threads without ordering) race
+ *   and give wrong results. Calls ordered on one stream are safe; each call
+ *   rewrites every part of the array it reads, so nothing needs clearing. */
+size_t gt_attn_bwd_noalloc_max_bytes(void);
+gt_status_t gt_attn_bwd_noalloc(const void* q, const void* k, const void* v,
+                                const uint8_t* spd, const uint8_t* spd_t,
+                                const float* table, int32_t n_buckets,
+                                const void* o, const float* lse, const void* d_o,
+                                void* dq, void* dk, void* dv, float* dtable,
+                                int32_t H, int64_t N, int32_t d, gt_dtype_t dtype,
+                                float scale, void* stream);
+
 /* Backward of gt_attn_fwd_batch: dq, dk, dv [B, H, N, d] dtype (overwritten);
  * dtable [H, n_buckets] fp32 (overwritten) sums the gradient over every graph
  * of the batch, since they share the table. spd_t (optional) holds graph b's

@@ -24,7 +24,8 @@ from pathlib import Path
 
 import torch
 
-__all__ = ["gt_attn_fwd", "gt_attn_bwd", "gt_attn_bwd_phase", "gt_attn_ring_step",
+__all__ = ["gt_attn_fwd", "gt_attn_bwd", "gt_attn_bwd_phase", "gt_attn_bwd_noalloc",
+           "gt_attn_bwd_noalloc_max_bytes", "gt_attn_ring_step",
            "gt_attn_ring_step_acc", "gt_attn_merge",
            "gt_attn_bwd_ring_step", "gt_attn_bwd_workspace_size", "gt_attn_bwd_ring_workspace_size",
            "gt_status_string", "gt_attn_version",
@@ -65,6 +66,11 @@ def lib() -> ctypes.CDLL:
         L.gt_attn_bwd.restype = _I32
         L.gt_attn_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _P, _P, _P, _P,
                                   ctypes.c_size_t, _I32, _I64, _I32, _I32, _F, _P]
+        L.gt_attn_bwd_noalloc.restype = _I32
+        L.gt_attn_bwd_noalloc.argtypes = [_P, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _P, _P, _P,
+                                          _I32, _I64, _I32, _I32, _F, _P]
+        L.gt_attn_bwd_noalloc_max_bytes.restype = ctypes.c_size_t
+        L.gt_attn_bwd_noalloc_max_bytes.argtypes = []
         L.gt_attn_bwd_phase.restype = _I32
         L.gt_attn_bwd_phase.argtypes = [_I32] + L.gt_attn_bwd.argtypes
         L.gt_attn_ring_step.restype = _I32
@@ -282,6 +288,32 @@ def gt_attn_bwd_phase(phase: int, q, k, v, spd, table, o, lse, d_o, scale: float
         _check(lib().gt_attn_bwd(*args), "gt_attn_bwd")
     else:
         _check(lib().gt_attn_bwd_phase(int(phase), *args), "gt_attn_bwd_phase")
+    return dq, dk, dv, dtable
+
+
+def gt_attn_bwd_noalloc_max_bytes() -> int:
+    return int(lib().gt_attn_bwd_noalloc_max_bytes())
+
+
+def gt_attn_bwd_noalloc(q, k, v, spd, table, o, lse, d_o, grads, scale: float | None = None,
+                        stream=None, spd_t=None):
+    """gt_attn_bwd with the library's fixed device scratch instead of a
+    workspace (C ABI gt_attn_bwd_noalloc): the call allocates nothing, so the
+    outputs `grads` = (dq, dk, dv, dtable) must be given. Calls that overlap
+    on one GPU share the scratch and race."""
+    _qdims(q, "q", 3)
+    H, N, d = q.shape
+    _shape(spd, "spd", (N, N), torch.uint8)
+    _need(grads is not None, "grads (dq, dk, dv, dtable) must be given: the call allocates nothing")
+    _check_bwd(q, k, v, spd, table, o, lse, d_o, grads, spd_t, (H,))
+    _devices(q, k, v, spd, table, o, lse, d_o, spd_t, *grads)
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dq, dk, dv, dtable = grads
+    st = lib().gt_attn_bwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(spd),
+                                   None if spd_t is None else _ptr(spd_t), _ptr(table),
+                                   table.shape[1], _ptr(o), _ptr(lse), _ptr(d_o), _ptr(dq), _ptr(dk),
+                                   _ptr(dv), _ptr(dtable), H, N, d, _dt(q), scale, _stream(stream))
+    _check(st, "gt_attn_bwd_noalloc")
     return dq, dk, dv, dtable
 
 

@@ -2,6 +2,7 @@
 // Nothing is launched and no output is touched unless every check passes.
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "../../include/gt_attn.h"
 #include "kernels.hpp"
@@ -201,6 +202,55 @@ gt_status_t gt_attn_bwd(const void* q, const void* k, const void* v, const uint8
                         int64_t N, int32_t d, gt_dtype_t dtype, float scale, void* stream) {
   return bwd_impl(-1, q, k, v, spd, spd_t, 0, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
                   workspace, workspace_bytes, 1, H, N, d, dtype, scale, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Device scratch of the allocation-free backward: a file-scope array that
+// every GPU the library runs on holds until the process ends. In host code
+// the name `scratch` is only a host-side stand-in, never a device address:
+// the device address is taken once per device with hipGetSymbolAddress and
+// kept in scratch_dev[], and only that pointer is handed to kernels.
+constexpr size_t kScratchBytes = size_t(16) << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+void* scratch_dev[kMaxDevices];
+std::mutex scratch_mu;
+
+// The current device's scratch address (set up on the first call on that
+// device, with it current); nullptr if the address cannot be obtained.
+void* device_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_dev[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    scratch_dev[dev] = p;
+  }
+  return scratch_dev[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t gt_attn_bwd_noalloc_max_bytes(void) { return kScratchBytes; }
+
+gt_status_t gt_attn_bwd_noalloc(const void* q, const void* k, const void* v, const uint8_t* spd,
+                                const uint8_t* spd_t, const float* table, int32_t n_buckets,
+                                const void* o, const float* lse, const void* d_o, void* dq,
+                                void* dk, void* dv, float* dtable, int32_t H, int64_t N, int32_t d,
+                                gt_dtype_t dtype, float scale, void* stream) {
+  // the size limit first: nothing below may allocate
+  if (H >= 1 && N >= 1 && gt_attn_bwd_workspace_size(H, N, d, dtype) > kScratchBytes)
+    return GT_ERR_WORKSPACE;
+  void* ws = device_scratch();
+  if (!ws) return GT_ERR_LAUNCH;
+  return bwd_impl(-1, q, k, v, spd, spd_t, 0, table, n_buckets, o, lse, d_o, dq, dk, dv, dtable,
+                  ws, kScratchBytes, 1, H, N, d, dtype, scale, stream);
 }
 
 gt_status_t gt_attn_bwd_batch(const void* q, const void* k, const void* v, const uint8_t* spd,
