@@ -183,37 +183,59 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* sK, const uint16_t* sV,
 // (8 and 16 run on 32-wide tiles whose extra features are zero). VEC: spd
 // rows are 16-byte aligned. FULL: VEC and Sk a multiple of the key tile, so
 // every spd group is loaded whole and no tile needs masking. SKIP: Sq is not
-// a multiple of the workgroup's rows, so some waves may own no row.
-template <int D, int DS, bool OUT_F32, bool VEC, bool FULL, bool SKIP>
+// a multiple of the workgroup's rows, so some waves may own no row. PAIR
+// (batches of sequences of at most 256 nodes): the two halves of the
+// workgroup (waves 0-3 and 4-7) take the same head of two consecutive
+// sequences, which share the bias table; each half stages its own K/V.
+template <int D, int DS, bool OUT_F32, bool VEC, bool FULL, bool SKIP, bool PAIR = false>
 __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   constexpr int NKC = D / 16;
   constexpr int NKS = (DS + 15) / 16;   // feature chunks that hold data
   constexpr int NCB = D / 32;
-  constexpr int BR = kWaves * 32 * kQB;
-  using Dma = TileDma<D, kWaves, DS>;     // K and V
+  constexpr int NWI = PAIR ? kWaves / 2 : kWaves;   // waves per sequence
+  constexpr int BR = NWI * 32 * kQB;
+  using Dma = TileDma<D, NWI, DS>;        // K and V
   static_assert(kBC == kTileRows, "key tile is one staged tile");
 
   // Three-stage ring of K / V tiles, one array per stage so that no read of
   // one stage can be taken to alias the copy into another; the bias table,
   // one copy per lane: entry (b, lane) at float index 64 b + lane.
-  __shared__ __attribute__((aligned(16))) uint16_t sK0[kBC * D], sK1[kBC * D], sK2[kBC * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sV0[kBC * D], sV1[kBC * D], sV2[kBC * D];
+  constexpr int NI = PAIR ? 2 : 1;
+  __shared__ __attribute__((aligned(16))) uint16_t sK0[NI * kBC * D], sK1[NI * kBC * D], sK2[NI * kBC * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sV0[NI * kBC * D], sV1[NI * kBC * D], sV2[NI * kBC * D];
   __shared__ __attribute__((aligned(16))) float sTab[kLaneTableFloats];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = wave_id();
+  const int lane = tid & 63, wave_all = wave_id();
+  const int item = PAIR ? wave_all / NWI : 0;        // the workgroup half (sequence) of the wave
+  const int wave = PAIR ? wave_all % NWI : wave_all;
   const int col = lane & 31, g = lane >> 5;
   const uint32_t lane4 = (uint32_t)lane * 4u;
 
   const int64_t nqb = (a.Sq + BR - 1) / BR;
-  const int64_t lid = xcd_remap(blockIdx.x, nqb * a.H);
-  const int h = (int)(lid % a.H);
-  const int64_t qblk = lid / a.H;
+  int h;
+  int64_t qblk;
+  bool item_ok = true;
+  if constexpr (PAIR) {
+    // workgroup = (sequence pair, head); Sq <= BR, so one row block
+    const int nseq = a.H / a.hpb;
+    const int64_t lid = xcd_remap(blockIdx.x, (int64_t)((nseq + 1) / 2) * a.hpb);
+    const int hh = (int)(lid % a.hpb);
+    const int seq = (int)(lid / a.hpb) * 2 + item;
+    item_ok = seq < nseq;
+    h = (item_ok ? seq : seq - 1) * a.hpb + hh;
+    qblk = 0;
+  } else {
+    const int64_t lid = xcd_remap(blockIdx.x, nqb * a.H);
+    h = (int)(lid % a.H);
+    qblk = lid / a.H;
+  }
   const int64_t qbase = qblk * BR + (int64_t)wave * 32 * kQB;
   // A wave whose rows all lie past Sq (short sequences) still takes its
   // share of the tile copies, spd loads, waits and barriers, but skips the
   // products and the softmax, leaving its SIMD to the other wave.
-  const bool active = !SKIP || qbase < a.Sq;
+  const bool active = (!SKIP || qbase < a.Sq) && item_ok;
+  const int item_off = item * kBC * D;               // this half's K/V staging
 
   fill_lane_table(sTab, a.table + (int64_t)table_row(a, h) * a.n_buckets, a.n_buckets, a.scale, kThreads);
 
@@ -280,8 +302,8 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   const Dma dma(wave);
   constexpr int SPD_LOADS = kQB * kKB;
 #define GT_FWD_STAGE(S_, K_, V_)                                                                \
-  uint16_t* K_ = (S_) == 0 ? sK0 : ((S_) == 1 ? sK1 : sK2);                                   \
-  uint16_t* V_ = (S_) == 0 ? sV0 : ((S_) == 1 ? sV1 : sV2);
+  uint16_t* K_ = ((S_) == 0 ? sK0 : ((S_) == 1 ? sK1 : sK2)) + item_off;                      \
+  uint16_t* V_ = ((S_) == 0 ? sV0 : ((S_) == 1 ? sV1 : sV2)) + item_off;
   // K/V tiles: a three-stage LDS ring, tile t in stage t % 3, copied two
   // tiles ahead (Dma::NLOADS vector-memory ops per wave); tiles past the
   // end are clamped to the last one.
@@ -313,7 +335,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
       spd_of(1, wB);
       wait_vmcnt<0>();
       __syncthreads();     // table, and tiles 0..2
-      if (active) issue_scores<D, NKS>(sTab, wA[0][0], lane4, sK0, off.k, 0, qf[0], s0);
+      if (active) issue_scores<D, NKS>(sTab, wA[0][0], lane4, sK0 + item_off, off.k, 0, qf[0], s0);
     }
     // Tile t from stage S = t % 3 and spd set P = t % 2; units u = (key
     // block, query block) in the order (0,0), (0,1), (1,0), (1,1). The score
@@ -420,7 +442,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   for (int qb = 0; qb < kQB; ++qb) {
     const float lt = sm[qb].l + __shfl_xor(sm[qb].l, 32);
     const int64_t i = qbase + qb * 32 + col;
-    if (i >= a.Sq) continue;
+    if (i >= a.Sq || !item_ok) continue;
     float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
     float lse_out = lt > 0.0f ? (sm[qb].m + __log2f(lt)) * kLn2 : -INFINITY;
     float wo = 0.0f;     // weight of the running state (accumulate mode)
@@ -558,6 +580,19 @@ hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t s) {
   const int64_t nqb = (a.Sq + BR - 1) / BR;
   const dim3 grid((unsigned)(nqb * a.H));
   const bool skip = a.Sq % BR != 0;
+  const int nseq = a.H / a.hpb;
+  if constexpr (D == 32) {
+    // batches of short sequences: two sequences per workgroup
+    constexpr int BRP = kWaves / 2 * 32 * kQB;
+    if (a.spd_vec && a.Sk % kBC == 0 && a.Sq <= BRP && a.hpb < a.H && nseq >= 2 && !a.accumulate) {
+      const dim3 gridp((unsigned)((nseq + 1) / 2 * a.hpb));
+      if (a.Sq % BRP != 0)
+        hipLaunchKernelGGL((fwd_bf16_kernel<D, DS, OUT_F32, true, true, true, true>), gridp, dim3(kThreads), 0, s, a);
+      else
+        hipLaunchKernelGGL((fwd_bf16_kernel<D, DS, OUT_F32, true, true, false, true>), gridp, dim3(kThreads), 0, s, a);
+      return hipGetLastError();
+    }
+  }
   if (a.spd_vec && a.Sk % kBC == 0) {
     if (skip)
       hipLaunchKernelGGL((fwd_bf16_kernel<D, DS, OUT_F32, true, true, true>), grid, dim3(kThreads), 0, s, a);

@@ -330,6 +330,7 @@ def test_ring_step_acc_from_empty_state_and_empty_block(dt):
     (5, 96, 64, "shared"),          # one spd for every graph (stride 0)
     (16, 65, 8, "per_graph"),       # the paper's head dim: 8 heads over 64 features
     (6, 128, 16, "per_graph_t"),
+    (8, 192, 8, "shared"),          # two graphs per forward workgroup, 192 of its 256 rows used
 ])
 def test_batch_of_graphs(B, N, d, spd_kind, dt):
     """A batch of graphs, each with its own spd, sharing the table: every
