@@ -117,6 +117,90 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdArgs a) {
   }
 }
 
+// Preprocess for sequences of at most 256 rows (one row block per head):
+// one wave per head, so the head's maxima are reduced within the wave (no
+// LDS, no barrier) and a workgroup of 4 waves covers 4 heads. The outputs
+// are those of bwd_prep_kernel with one 256-row block.
+template <int D, bool BF16>
+__global__ __launch_bounds__(256) void bwd_prep_short_kernel(BwdArgs a) {
+  constexpr int EPC = BF16 ? 8 : 4;
+  constexpr int TPR = D / EPC;               // lanes per row
+  constexpr int RPW = 64 / TPR;              // rows per wave pass
+  constexpr int NPASS = 256 / RPW;
+  const int lane = threadIdx.x & 63;
+  const int h = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (blockIdx.x == 0 && !a.accumulate) {
+    for (int t = threadIdx.x; t < a.hpb * a.n_buckets; t += 256) a.dtable[t] = 0.0f;
+  }
+  if (h >= a.H) return;
+  const int sub = lane % TPR;
+  using T = std::conditional_t<BF16, uint16_t, float>;
+  auto chunk_dot = [](const T* x, const T* y, float& xy, float& yy) {
+    if constexpr (BF16) {
+      const uint4 xv = *reinterpret_cast<const uint4*>(x);
+      const uint4 yv = *reinterpret_cast<const uint4*>(y);
+      const uint16_t* xp = reinterpret_cast<const uint16_t*>(&xv);
+      const uint16_t* yp = reinterpret_cast<const uint16_t*>(&yv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float yf = bf2f(yp[e]);
+        xy = fmaf(bf2f(xp[e]), yf, xy);
+        yy = fmaf(yf, yf, yy);
+      }
+    } else {
+      const float4 xv = *reinterpret_cast<const float4*>(x);
+      const float4 yv = *reinterpret_cast<const float4*>(y);
+      xy = fmaf(xv.x, yv.x, fmaf(xv.y, yv.y, fmaf(xv.z, yv.z, fmaf(xv.w, yv.w, xy))));
+      yy = fmaf(yv.x, yv.x, fmaf(yv.y, yv.y, fmaf(yv.z, yv.z, fmaf(yv.w, yv.w, yy))));
+    }
+  };
+  float nd = 0.0f, nv = 0.0f, nl = 0.0f;
+#pragma unroll 4
+  for (int pass = 0; pass < NPASS; ++pass) {
+    const int64_t i = pass * RPW + lane / TPR;
+    float acc = 0.0f, sq = 0.0f, vq = 0.0f, unused = 0.0f;
+    if (i < a.Sq) {
+      const int64_t off = ((int64_t)h * a.Sq + i) * D + sub * EPC;
+      chunk_dot(reinterpret_cast<const T*>(a.o) + off, reinterpret_cast<const T*>(a.d_o) + off, acc, sq);
+    }
+    if (i < a.Sk) {
+      const int64_t off = ((int64_t)h * a.Sk + i) * D + sub * EPC;
+      const T* v = reinterpret_cast<const T*>(a.v) + off;
+      chunk_dot(v, v, unused, vq);
+    }
+#pragma unroll
+    for (int o = TPR / 2; o >= 1; o >>= 1) {
+      acc += __shfl_xor(acc, o);
+      sq += __shfl_xor(sq, o);
+      vq += __shfl_xor(vq, o);
+    }
+    if (i < a.Sq) {
+      const int64_t row = (int64_t)h * a.Sq + i;
+      nd = fmaxf(nd, sq);
+      nl = fmaxf(nl, fabsf(acc));
+      if (sub == 0) {
+        a.dlt[row] = acc;
+        const float L = a.lse[row];
+        a.lse2[row] = (L == -INFINITY) ? INFINITY : L * kLog2e;
+      }
+    }
+    if (i < a.Sk) nv = fmaxf(nv, vq);
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    nd = fmaxf(nd, __shfl_xor(nd, off));
+    nv = fmaxf(nv, __shfl_xor(nv, off));
+    nl = fmaxf(nl, __shfl_xor(nl, off));
+  }
+  if (lane == 0) {
+    float* out = a.nmax + (int64_t)h * 4;
+    out[0] = nd;
+    out[1] = nv;
+    out[2] = nl;
+    out[3] = 0.0f;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Vector-ALU path (fp32 inputs): one thread per query row / key column, fp32
 // math; dq, dk, dv are fp32 (stored, or added into the caller's
@@ -280,11 +364,19 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
   hipError_t e = hipSuccess;
   if (phase < 0 || phase == 0) {
     const int64_t rows = a.Sq > a.Sk ? a.Sq : a.Sk;
-    const dim3 grid((unsigned)((rows + 255) / 256), (unsigned)a.H);
-    if (bf16)
-      hipLaunchKernelGGL((bwd_prep_kernel<D, true>), grid, dim3(256), 0, s, a);
-    else
-      hipLaunchKernelGGL((bwd_prep_kernel<D, false>), grid, dim3(256), 0, s, a);
+    if (rows <= 256) {
+      const dim3 grid((unsigned)((a.H + 3) / 4));
+      if (bf16)
+        hipLaunchKernelGGL((bwd_prep_short_kernel<D, true>), grid, dim3(256), 0, s, a);
+      else
+        hipLaunchKernelGGL((bwd_prep_short_kernel<D, false>), grid, dim3(256), 0, s, a);
+    } else {
+      const dim3 grid((unsigned)((rows + 255) / 256), (unsigned)a.H);
+      if (bf16)
+        hipLaunchKernelGGL((bwd_prep_kernel<D, true>), grid, dim3(256), 0, s, a);
+      else
+        hipLaunchKernelGGL((bwd_prep_kernel<D, false>), grid, dim3(256), 0, s, a);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (bf16) {     // matrix cores at every head dim (8 and 16 on 32-wide tiles)
