@@ -10,7 +10,10 @@
 // P = 0; Dlt; dtable = 0), then the key-stationary dK/dV/dtable kernel and
 // the query-stationary dQ kernel (bwd_dkdv.hip, bwd_dq.hip for bf16 at
 // every head dim; the vector-ALU kernels below for fp32). Splitting dQ from
-// dK/dV recomputes two products but needs no atomics on dQ.
+// dK/dV recomputes two products but needs no atomics on dQ. Sequences of at
+// most 256 rows at head dims up to 32 take one fused kernel instead
+// (bwd_short.hip): there a workgroup holds every key, so dQ is reduced inside
+// it.
 #include <type_traits>
 
 #include "common.hpp"
@@ -380,6 +383,7 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (bf16) {     // matrix cores at every head dim (8 and 16 on 32-wide tiles)
+    if (phase < 0 && bwd_short_applies(a, D)) return launch_bwd_short_bf16(a, D, s);
     if (phase < 0 || phase == 1) {
       if ((e = launch_dkdv_bf16(a, D, s)) != hipSuccess) return e;
     }

@@ -1,0 +1,484 @@
+// Backward for sequences of at most 256 rows (bf16, head dims 8, 16, 32):
+// dK, dV, dQ and the bias-table gradient in one kernel.
+//
+// One workgroup of 8 waves covers every key of a sequence (wave w owns keys
+// 32 w .. 32 w + 31, lane & 31 = key), so each 32 x 32 block of scores is
+// formed once. P and dS feed dV^T += dO^T P and dK^T += Q^T dS straight from
+// registers, as in the key-stationary kernel, and dQ = scale dS K is reduced
+// inside the workgroup instead of by a second pass that recomputes S and dP.
+// The 8 x 8 blocks are visited on diagonals: at step t wave w forms block
+// (query block (w + t) mod 8, key block w) and stores its dS (bf16) in an LDS
+// slot; after the step's barrier wave w adds to dQ of its own query block w
+// the block (w, (w - t) mod 8), stored by wave (w - t) mod 8 at that step,
+// as dQ^T += K^T dS^T with both operands read by transposing LDS reads. So
+// every wave accumulates dK and dV of its key block and dQ of its query block
+// in registers across the 8 steps, and every stored block is read by one
+// wave. The slots are double buffered by step parity.
+//
+// The workgroups are persistent: there are at most 256 of them (one per
+// compute unit, the kernel holds 160 KiB of LDS) and workgroup w takes head
+// (w mod hpb) of every (G / hpb)-th sequence, G the grid size. Its bias table
+// and gradient histogram (the key-stationary kernel's layout and fixed-point
+// scheme) stay in LDS across its sequences: the table is filled and the
+// histogram flushed once, and the histogram's power-of-two scale is set from
+// the norm maxima of all its sequences. The hpb heads of a sequence run on
+// one XCD at about the same time, so they share its spd bytes in L2.
+//
+// The prepare stage (LSE log2 e, Dlt, norm maxima, dtable = 0) runs before.
+#include <type_traits>
+
+#include "common.hpp"
+#include "kernels.hpp"
+#include "stage.hpp"
+
+namespace gt {
+
+namespace {
+
+constexpr int kNW = 8;               // waves per workgroup
+constexpr int kThreads = kNW * 64;
+constexpr int kRows = 256;           // longest sequence: 8 blocks of 32 rows
+constexpr int D = 32;                // tile width; head dims below it are zero-padded
+constexpr uint32_t kTabBase = 65536;
+constexpr int kMaxGridShort = 256;
+
+template <int NB>
+constexpr int copies() { return NB <= 128 ? 32 : 16; }
+
+// LDS below 64 KiB: the sequence's Q, dO and K rows (row-major, the tile
+// swizzle of 64-row tiles, rows past N and features past the head dim zero),
+// the accumulator starts of S and dP per query, and -inf starts for the
+// lanes of keys past N.
+struct ShortTiles {
+  uint16_t q[kRows * D];
+  uint16_t o[kRows * D];
+  uint16_t k[kRows * D];
+  float init_s[kRows];                // -LSE log2 e / (scale log2 e); -inf past N
+  float init_p[kRows];                // -Dlt 2^F
+  float ninf[kRows];                  // -inf: S start of the keys past N, so P = 0
+  float red[3][kNW];
+};
+// From 64 KiB: table copies, histogram copies (as in the key-stationary
+// kernel: the histogram entry at a fixed offset from the table entry), then
+// the dS slots: [step parity][writer wave], 32 keys (rows) x 32 queries in
+// the 32-wide tile layout.
+template <int NB>
+struct ShortSmem : ShortTiles {
+  static constexpr int ENT = NB * copies<NB>();
+  uint8_t pad[kTabBase - sizeof(ShortTiles)];
+  uint2 tabw[ENT];
+  unsigned long long hist[ENT];
+  uint16_t xs[2][kNW][32 * D];
+};
+static_assert(sizeof(ShortSmem<128>) <= 160 * 1024 && sizeof(ShortSmem<256>) <= 160 * 1024,
+              "LDS budget");
+
+__device__ __forceinline__ int round_to_int(float x) {
+  int r;
+  asm("v_cvt_rpi_i32_f32 %0, %1" : "=v"(r) : "v"(x));   // floor(x + 0.5)
+  return r;
+}
+
+// Byte values of 128 and more have no entry in the 128-bucket layout, which
+// is used only when n_buckets <= 127: they are mapped to its padding bucket
+// 127 (bias 0, gradient discarded). Valid input never takes the branch.
+template <int NB>
+__device__ __forceinline__ void clamp_buckets(uint32_t (&w)[4]) {
+  if constexpr (NB <= 128) {
+    if (__any(((w[0] | w[1] | w[2] | w[3]) & 0x80808080u) != 0)) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        uint32_t x = w[u];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if ((x >> (8 * k + 7)) & 1u) x = (x & ~(0xffu << (8 * k))) | (0x7fu << (8 * k));
+        w[u] = x;
+      }
+    }
+  }
+}
+template <int NB>
+__device__ __forceinline__ void clamp_buckets(uint8_t (&b)[16]) {
+  if constexpr (NB <= 128) {
+    uint32_t any = 0;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) any |= b[r];
+    if (__any((any & 0x80u) != 0)) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) b[r] = (b[r] & 0x80u) ? (uint8_t)0x7f : b[r];
+    }
+  }
+}
+
+// Per-lane LDS element offsets of the operand reads.
+struct ShortOffsets {
+  int row[D / 16];     // rows perm32(lane) of a 32-row block, feature chunk 2 kc + g
+  int tr[2];           // transposing reads h = 0, 1 (tile columns 0..31)
+  __device__ __forceinline__ ShortOffsets() {
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) row[kc] = row_operand_off<D>(kc);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) tr[h] = tr_operand_off<D>(h, 0);
+  }
+};
+
+// Block (query block qb, this wave's keys): S and dP, P and dS, the bias
+// reads and gradient adds, dV and dK, and dS (bf16) into slot xs.
+// b: the lane's 16 bucket indices (4 words of spd_t, or 16 gathered bytes).
+template <int NKS, int NB, typename BT>
+__device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets& off,
+                                           const bf16x8* kf, const bf16x8* vf, const BT* b,
+                                           const float* is_lane, float sl2, int qb, uint16_t* xs,
+                                           f32x16& dk, f32x16& dv) {
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 5;
+  const int ib = qb * 32 + 16 * g;    // this lane half's first query
+
+  f32x16 s, dp;
+  {
+    const float4* is4 = reinterpret_cast<const float4*>(is_lane + qb * 32);
+    const float4* ip4 = reinterpret_cast<const float4*>(&sm.init_p[ib]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float4 x = is4[u], y = ip4[u];
+      s[4 * u] = x.x; s[4 * u + 1] = x.y; s[4 * u + 2] = x.z; s[4 * u + 3] = x.w;
+      dp[4 * u] = y.x; dp[4 * u + 1] = y.y; dp[4 * u + 2] = y.z; dp[4 * u + 3] = y.w;
+    }
+  }
+#pragma unroll
+  for (int kc = 0; kc < NKS; ++kc) {
+    s = mfma32(lds_b128(sm.q + qb * 32 * D + off.row[kc]), kf[kc], s);
+    dp = mfma32(lds_b128(sm.o + qb * 32 * D + off.row[kc]), vf[kc], dp);
+  }
+  float p[16], ds[16];
+  uint32_t addr[16];   // LDS byte offset of table entry (bucket, copy) from sm
+  float tb[16];
+  constexpr int CPY = copies<NB>();
+  const uint32_t cpyb = (uint32_t)(lane & (CPY - 1)) * 8u | kTabBase;
+  if constexpr (sizeof(BT) == 4) {
+    uint32_t w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      w[u] = b[u];
+      opaque(w[u]);
+    }
+    clamp_buckets<NB>(w);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      if constexpr (CPY == 32)
+        addr[r] = __builtin_amdgcn_perm(w[r >> 2], cpyb, 0x0c020000u | ((4u + (r & 3)) << 8));
+      else
+        addr[r] = (((w[r >> 2] >> (8 * (r & 3))) & 0xffu) << 7) | cpyb;
+    }
+  } else {
+    uint8_t bb[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      uint32_t bk = b[r];
+      opaque(bk);
+      bb[r] = (uint8_t)bk;
+    }
+    clamp_buckets<NB>(bb);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const uint32_t bk = bb[r];
+      if constexpr (CPY == 32)
+        addr[r] = __builtin_amdgcn_perm(bk, cpyb, 0x0c020400u);
+      else
+        addr[r] = (bk << 7) | cpyb;
+    }
+  }
+  const uint8_t* lds0 = reinterpret_cast<const uint8_t*>(&sm);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) tb[r] = *reinterpret_cast<const float*>(lds0 + addr[r]);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const float pv = exp2_fast(fmaf(s[r], sl2, tb[r]));
+    p[r] = pv;
+    ds[r] = pv * dp[r];
+  }
+  constexpr uint32_t kHistOff = ShortSmem<NB>::ENT * 8;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    unsigned long long* hp =
+        reinterpret_cast<unsigned long long*>(const_cast<uint8_t*>(lds0) + addr[r] + kHistOff);
+    atomicAdd(hp, (unsigned long long)(long long)round_to_int(ds[r]));
+  }
+  const int key = lane & 31;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const bf16x8 pb = cvt_bf16x8(p + 8 * q);
+    const bf16x8 db = cvt_bf16x8(ds + 8 * q);
+    const int base = (qb * 32 + 8 * q) * D;
+    dv = mfma32(lds_tr_operand(sm.o + base, off.tr[0], off.tr[1]), pb, dv);
+    dk = mfma32(lds_tr_operand(sm.q + base, off.tr[0], off.tr[1]), db, dk);
+    // queries 16 g + 8 q .. + 7 of this key: chunk 2 g + q of slot row `key`
+    *reinterpret_cast<bf16x8*>(xs + key * D + swz_tile<D>(key, 2 * g + q) * 8) = db;
+  }
+}
+
+template <int DS, int NB, bool TR>
+__global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) {
+  constexpr int NKS = (DS + 15) / 16;   // 16-feature chunks of S and dP that hold data
+  constexpr int CPS = DS / 8;           // 16-byte chunks per source row
+  constexpr int CPY = copies<NB>();
+  __shared__ __attribute__((aligned(16))) ShortSmem<NB> sm;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int g = lane >> 5;
+  const int w = wave_id();
+  const int N = (int)a.Sq;
+  const int nb = (N + 31) / 32;
+
+  const int G = (int)gridDim.x;
+  const int lw = (int)xcd_remap(blockIdx.x, G);
+  const int head = lw % a.hpb;
+  const int slot = lw / a.hpb;
+  const int nslots = G / a.hpb;
+  const int nseq = a.H / a.hpb;
+
+  // Table (times log2 e) and histogram of this workgroup's head; zero tiles
+  // (features past the head dim and rows past N stay zero); -inf starts.
+  for (int t = tid; t < ShortSmem<NB>::ENT; t += kThreads) {
+    const int bkt = t / CPY;
+    const float tv = (bkt < a.n_buckets) ? a.table[(int64_t)head * a.n_buckets + bkt] * kLog2e : 0.0f;
+    sm.tabw[t] = make_uint2(__float_as_uint(tv), 0u);
+    sm.hist[t] = 0ull;
+  }
+  for (int t = tid; t < 3 * kRows * D / 8; t += kThreads)
+    reinterpret_cast<uint4*>(sm.q)[t] = make_uint4(0u, 0u, 0u, 0u);
+  for (int t = tid; t < kRows; t += kThreads) sm.ninf[t] = -INFINITY;
+
+  // Fixed-point exponent F: (max|dO| max|V| + max|Dlt|) 2^F <= 2^30 over all
+  // of this workgroup's sequences (one 256-row block of maxima each).
+  {
+    float md = 0.0f, mv = 0.0f, ml = 0.0f;
+    for (int s = slot + tid * nslots; s < nseq; s += kThreads * nslots) {
+      const float* nm = a.nmax + ((int64_t)s * a.hpb + head) * 4;
+      md = fmaxf(md, nm[0]);
+      mv = fmaxf(mv, nm[1]);
+      ml = fmaxf(ml, nm[2]);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      md = fmaxf(md, __shfl_xor(md, o));
+      mv = fmaxf(mv, __shfl_xor(mv, o));
+      ml = fmaxf(ml, __shfl_xor(ml, o));
+    }
+    if (lane == 0) {
+      sm.red[0][w] = md;
+      sm.red[1][w] = mv;
+      sm.red[2][w] = ml;
+    }
+  }
+  __syncthreads();
+  float md = sm.red[0][0], mv = sm.red[1][0], ml = sm.red[2][0];
+#pragma unroll
+  for (int i = 1; i < kNW; ++i) {
+    md = fmaxf(md, sm.red[0][i]);
+    mv = fmaxf(mv, sm.red[1][i]);
+    ml = fmaxf(ml, sm.red[2][i]);
+  }
+  const float bound = 1.015f * (sqrtf(md) * sqrtf(mv) + ml);
+  int fexp = 40;
+  if (bound > 0.0f && bound < INFINITY) {
+    int e;
+    frexpf(bound, &e);
+    fexp = 30 - e;
+    fexp = fexp > 40 ? 40 : (fexp < -100 ? -100 : fexp);
+  }
+  const float sF = ldexpf(1.0f, fexp);
+  const float sl2 = a.scale * kLog2e;
+  const float inv_sl2 = 1.0f / sl2;
+  const float gscale = a.scale * ldexpf(1.0f, -fexp);   // dK and dQ: scale 2^-F
+
+  const int key = lane & 31;
+  const int j = w * 32 + key;           // this lane's key
+  const bool jok = j < N;
+  const int jc = jok ? j : N - 1;
+  const float* is_lane = (jok ? sm.init_s : sm.ninf) + 16 * g;
+  const ShortOffsets off;
+  const int ld = (int)a.ld_spd;
+  using BT = std::conditional_t<TR, uint32_t, uint8_t>;
+  constexpr int NBT = TR ? 4 : 16;
+
+  for (int seq = slot; seq < nseq; seq += nslots) {
+    const int h = seq * a.hpb + head;
+    const int64_t rowbase = (int64_t)h * N * DS;
+    const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + rowbase;
+    const uint16_t* oh = reinterpret_cast<const uint16_t*>(a.d_o) + rowbase;
+    const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + rowbase;
+    const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + rowbase;
+
+    // the previous sequence's readers are done with the tiles and slots
+    __syncthreads();
+    {
+      // Q, dO, K rows: item u = (tensor, row, chunk < DS/8); rows past N
+      // read zero (the resource ends at row N).
+      constexpr int PER = kRows * CPS;             // items per tensor (multiple of 64)
+      constexpr int NIT = 3 * PER;
+      constexpr int IPT = (NIT + kThreads - 1) / kThreads;
+      const __amdgpu_buffer_rsrc_t rq = make_rsrc_n(qh, (int64_t)N * DS * 2);
+      const __amdgpu_buffer_rsrc_t ro = make_rsrc_n(oh, (int64_t)N * DS * 2);
+      const __amdgpu_buffer_rsrc_t rk = make_rsrc_n(kh, (int64_t)N * DS * 2);
+      uint4 r[IPT];
+#pragma unroll
+      for (int s = 0; s < IPT; ++s) {
+        const int u = tid + s * kThreads;
+        if (u < NIT) {            // wave-uniform: NIT is a multiple of 64
+          const int tn = u / PER, rem = u % PER;
+          const int row = rem / CPS, chunk = rem % CPS;
+          const uint32_t voff = (uint32_t)(row * DS * 2 + chunk * 16);
+          r[s] = buf_b128(tn == 0 ? rq : (tn == 1 ? ro : rk), voff);
+        }
+      }
+      float st = 0.0f;
+      if (tid < N) st = a.lse2[(int64_t)h * N + tid];
+      else if (tid >= kRows && tid - kRows < N) st = a.dlt[(int64_t)h * N + tid - kRows];
+#pragma unroll
+      for (int s = 0; s < IPT; ++s) {
+        const int u = tid + s * kThreads;
+        if (u < NIT) {
+          const int tn = u / PER, rem = u % PER;
+          const int row = rem / CPS, chunk = rem % CPS;
+          uint16_t* tile = tn == 0 ? sm.q : (tn == 1 ? sm.o : sm.k);
+          *reinterpret_cast<uint4*>(tile + row * D + swz_tile<D>(row, chunk) * 8) = r[s];
+        }
+      }
+      if (tid < kRows)
+        sm.init_s[tid] = tid < N ? -st * inv_sl2 : -INFINITY;
+      else
+        sm.init_p[tid - kRows] = tid - kRows < N ? -st * sF : 0.0f;
+    }
+    // K and 2^F V of this lane's key as B operands (keys past N: zero)
+    bf16x8 kf[D / 16], vf[D / 16];
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) {
+      const bool in = jok && kc * 16 + g * 8 < DS;
+      kf[kc] = in ? *reinterpret_cast<const bf16x8*>(kh + (int64_t)j * DS + kc * 16 + g * 8) : zero_bf16x8();
+      const bf16x8 v8 = in ? *reinterpret_cast<const bf16x8*>(vh + (int64_t)j * DS + kc * 16 + g * 8) : zero_bf16x8();
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vf[kc][e] = (__bf16)((float)v8[e] * sF);
+    }
+
+    // spd bytes of block (qb, this wave's keys): rows 32 qb + 16 g + r, column j.
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc_n(TR ? seq_spd_t(a, h) : seq_spd(a, h), (int64_t)N * ld);
+    auto fetch = [&](int qb, BT* dst) {
+      if constexpr (TR) {
+        buf_u128(rs, (uint32_t)(jc * ld + 16 * g), (uint32_t)(qb * 32), reinterpret_cast<uint32_t*>(dst));
+      } else {
+        const uint32_t voff = (uint32_t)((qb * 32 + 16 * g) * ld + jc);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dst[r] = (uint8_t)buf_u8(rs, voff, (uint32_t)(r * ld));
+      }
+    };
+
+    f32x16 dk = zero_f32x16(), dv = zero_f32x16(), dq = zero_f32x16();
+    const bool wact = w < nb;
+    auto step_a = [&](int t, uint16_t* xs, const BT* b) {
+      const int qb = (w + t) & 7;
+      if (wact && qb < nb) block_dkdv<NKS, NB>(sm, off, kf, vf, b, is_lane, sl2, qb, xs, dk, dv);
+    };
+    auto step_b = [&](int t, int par) {
+      const int src = (w - t) & 7;      // key block whose dS for query block w was stored at step t
+      if (wact && src < nb) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const bf16x8 kt = lds_tr_operand(sm.k + (src * 32 + 8 * q) * D, off.tr[0], off.tr[1]);
+          const bf16x8 st = lds_tr_operand(&sm.xs[par][src][8 * q * D], off.tr[0], off.tr[1]);
+          dq = mfma32(kt, st, dq);
+        }
+      }
+    };
+
+    BT bA[NBT], bB[NBT];
+    fetch(w & 7, bA);
+    wait_loads();
+    __syncthreads();
+#pragma unroll 1
+    for (int t = 0; t < kNW; t += 2) {
+      fetch((w + t + 1) & 7, bB);
+      sched_fence();
+      if (t > 0) step_b(t - 1, 1);
+      step_a(t, sm.xs[0][w], bA);
+      __syncthreads();
+      fetch((w + t + 2) & 7, bA);
+      sched_fence();
+      step_b(t, 0);
+      step_a(t + 1, sm.xs[1][w], bB);
+      __syncthreads();
+    }
+    step_b(kNW - 1, 1);
+
+    // dK, dV of key j; dQ of query w * 32 + key (features 8 u + 4 g .. + 3)
+    if (jok) {
+      uint16_t* dkp = reinterpret_cast<uint16_t*>(a.dk) + rowbase + (int64_t)j * DS;
+      uint16_t* dvp = reinterpret_cast<uint16_t*>(a.dv) + rowbase + (int64_t)j * DS;
+      uint16_t* dqp = reinterpret_cast<uint16_t*>(a.dq) + rowbase + (int64_t)j * DS;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = 8 * u + 4 * g;
+        if (c >= DS) continue;
+        uint2 pk, pv, pq;
+        pk.x = (uint32_t)f2bf(dk[4 * u] * gscale) | ((uint32_t)f2bf(dk[4 * u + 1] * gscale) << 16);
+        pk.y = (uint32_t)f2bf(dk[4 * u + 2] * gscale) | ((uint32_t)f2bf(dk[4 * u + 3] * gscale) << 16);
+        pv.x = (uint32_t)f2bf(dv[4 * u]) | ((uint32_t)f2bf(dv[4 * u + 1]) << 16);
+        pv.y = (uint32_t)f2bf(dv[4 * u + 2]) | ((uint32_t)f2bf(dv[4 * u + 3]) << 16);
+        pq.x = (uint32_t)f2bf(dq[4 * u] * gscale) | ((uint32_t)f2bf(dq[4 * u + 1] * gscale) << 16);
+        pq.y = (uint32_t)f2bf(dq[4 * u + 2] * gscale) | ((uint32_t)f2bf(dq[4 * u + 3] * gscale) << 16);
+        *reinterpret_cast<uint2*>(dkp + c) = pk;
+        *reinterpret_cast<uint2*>(dvp + c) = pv;
+        *reinterpret_cast<uint2*>(dqp + c) = pq;
+      }
+    }
+  }
+
+  __syncthreads();
+  const double unscale = ldexp(1.0, -fexp);
+  for (int bkt = tid; bkt < a.n_buckets; bkt += kThreads) {
+    long long t = 0;
+#pragma unroll
+    for (int c = 0; c < CPY; ++c) t += (long long)sm.hist[bkt * CPY + ((c + bkt) & (CPY - 1))];
+    if (t != 0) atomicAdd(&a.dtable[(int64_t)head * a.n_buckets + bkt], (float)((double)t * unscale));
+  }
+}
+
+template <int DS, int NB>
+void launch_short_t(const BwdArgs& a, hipStream_t s) {
+  const int nseq = a.H / a.hpb;
+  int slots = kMaxGridShort / a.hpb;
+  if (slots < 1) slots = 1;
+  if (slots > nseq) slots = nseq;
+  const dim3 grid((unsigned)(slots * a.hpb));
+  if (a.spd_t)
+    hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, true>), grid, dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, false>), grid, dim3(kThreads), 0, s, a);
+}
+
+template <int NB>
+void launch_short_nb(const BwdArgs& a, int d, hipStream_t s) {
+  switch (d) {
+    case 8: launch_short_t<8, NB>(a, s); break;
+    case 16: launch_short_t<16, NB>(a, s); break;
+    default: launch_short_t<32, NB>(a, s); break;
+  }
+}
+
+}  // namespace
+
+bool bwd_short_applies(const BwdArgs& a, int d) {
+  return d <= 32 && !a.accumulate && a.row_off == 0 && a.col_off == 0 && a.Sq == a.Sk &&
+         a.Sq >= 1 && a.Sq <= kRows && a.hpb >= 1 && a.H % a.hpb == 0;
+}
+
+hipError_t launch_bwd_short_bf16(const BwdArgs& a, int d, hipStream_t s) {
+  if (a.n_buckets <= 127)
+    launch_short_nb<128>(a, d, s);
+  else
+    launch_short_nb<256>(a, d, s);
+  return hipGetLastError();
+}
+
+}  // namespace gt

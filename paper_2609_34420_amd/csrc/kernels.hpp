@@ -96,6 +96,10 @@ hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStrea
 hipError_t launch_bwd(const BwdArgs& a, int d, bool bf16, int phase, hipStream_t s);
 hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s);
 hipError_t launch_dq_bf16(const BwdArgs& a, int d, hipStream_t s);
+// Sequences of at most 256 rows (bf16, d <= 32, not a ring step): dK, dV,
+// dQ and dtable in one persistent kernel, after the prepare stage.
+bool bwd_short_applies(const BwdArgs& a, int d);
+hipError_t launch_bwd_short_bf16(const BwdArgs& a, int d, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, bool out_bf16, hipStream_t s);
 
 }  // namespace gt
