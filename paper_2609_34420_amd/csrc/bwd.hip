@@ -11,9 +11,9 @@
 // the query-stationary dQ kernel (bwd_dkdv.hip, bwd_dq.hip for bf16 at
 // every head dim; the vector-ALU kernels below for fp32). Splitting dQ from
 // dK/dV recomputes two products but needs no atomics on dQ. Sequences of at
-// most 256 rows at head dims up to 32 take one fused kernel instead
-// (bwd_short.hip): there a workgroup holds every key, so dQ is reduced inside
-// it.
+// most 256 rows at head dims up to 32 take one fused kernel instead, which
+// also does the prepare stage's work (bwd_short.hip): there a workgroup holds
+// every key, so dQ is reduced inside it.
 #include <type_traits>
 
 #include "common.hpp"
@@ -365,6 +365,8 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
 template <int D>
 hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
   hipError_t e = hipSuccess;
+  // sequences of at most 256 rows: one fused kernel, prepare stage included
+  if (bf16 && phase < 0 && bwd_short_applies(a, D)) return launch_bwd_short_bf16(a, D, s);
   if (phase < 0 || phase == 0) {
     const int64_t rows = a.Sq > a.Sk ? a.Sq : a.Sk;
     if (rows <= 256) {
@@ -383,7 +385,6 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (bf16) {     // matrix cores at every head dim (8 and 16 on 32-wide tiles)
-    if (phase < 0 && bwd_short_applies(a, D)) return launch_bwd_short_bf16(a, D, s);
     if (phase < 0 || phase == 1) {
       if ((e = launch_dkdv_bf16(a, D, s)) != hipSuccess) return e;
     }

@@ -20,11 +20,14 @@
 // (w mod hpb) of every (G / hpb)-th sequence, G the grid size. Its bias table
 // and gradient histogram (the key-stationary kernel's layout and fixed-point
 // scheme) stay in LDS across its sequences: the table is filled and the
-// histogram flushed once, and the histogram's power-of-two scale is set from
-// the norm maxima of all its sequences. The hpb heads of a sequence run on
-// one XCD at about the same time, so they share its spd bytes in L2.
+// histogram flushed once. The histogram's power-of-two scale follows the
+// largest norm bound seen so far (it only decreases; the accumulated sums are
+// shifted when it does). A sequence's loads are issued during the last step
+// of the one before. The hpb heads of a sequence run on one XCD at about the
+// same time, so they share its spd bytes in L2.
 //
-// The prepare stage (LSE log2 e, Dlt, norm maxima, dtable = 0) runs before.
+// The prepare stage's work is done here too: each sequence's Dlt = rowsum(dO * O),
+// LSE log2 e and norm maxima come from its rows as they are loaded.
 #include <type_traits>
 
 #include "common.hpp"
@@ -97,19 +100,6 @@ __device__ __forceinline__ void clamp_buckets(uint32_t (&w)[4]) {
     }
   }
 }
-template <int NB>
-__device__ __forceinline__ void clamp_buckets(uint8_t (&b)[16]) {
-  if constexpr (NB <= 128) {
-    uint32_t any = 0;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) any |= b[r];
-    if (__any((any & 0x80u) != 0)) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) b[r] = (b[r] & 0x80u) ? (uint8_t)0x7f : b[r];
-    }
-  }
-}
-
 // Per-lane LDS element offsets of the operand reads.
 struct ShortOffsets {
   int row[D / 16];     // rows perm32(lane) of a 32-row block, feature chunk 2 kc + g
@@ -155,38 +145,36 @@ __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets
   float tb[16];
   constexpr int CPY = copies<NB>();
   const uint32_t cpyb = (uint32_t)(lane & (CPY - 1)) * 8u | kTabBase;
+  uint32_t w[4];
   if constexpr (sizeof(BT) == 4) {
-    uint32_t w[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       w[u] = b[u];
       opaque(w[u]);
     }
-    clamp_buckets<NB>(w);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      if constexpr (CPY == 32)
-        addr[r] = __builtin_amdgcn_perm(w[r >> 2], cpyb, 0x0c020000u | ((4u + (r & 3)) << 8));
-      else
-        addr[r] = (((w[r >> 2] >> (8 * (r & 3))) & 0xffu) << 7) | cpyb;
-    }
   } else {
-    uint8_t bb[16];
+    // 16 gathered bytes (one per register, upper bits unknown to the
+    // compiler) packed into 4 words by byte permutes
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      uint32_t bk = b[r];
-      opaque(bk);
-      bb[r] = (uint8_t)bk;
-    }
-    clamp_buckets<NB>(bb);
+    for (int u = 0; u < 4; ++u) {
+      uint32_t x[4];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const uint32_t bk = bb[r];
-      if constexpr (CPY == 32)
-        addr[r] = __builtin_amdgcn_perm(bk, cpyb, 0x0c020400u);
-      else
-        addr[r] = (bk << 7) | cpyb;
+      for (int e = 0; e < 4; ++e) {
+        x[e] = b[4 * u + e];
+        opaque(x[e]);
+      }
+      const uint32_t lo = __builtin_amdgcn_perm(x[1], x[0], 0x0c0c0400u);
+      const uint32_t hi = __builtin_amdgcn_perm(x[3], x[2], 0x0c0c0400u);
+      w[u] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);
     }
+  }
+  clamp_buckets<NB>(w);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    if constexpr (CPY == 32)
+      addr[r] = __builtin_amdgcn_perm(w[r >> 2], cpyb, 0x0c020000u | ((4u + (r & 3)) << 8));
+    else
+      addr[r] = (((w[r >> 2] >> (8 * (r & 3))) & 0xffu) << 7) | cpyb;
   }
   const uint8_t* lds0 = reinterpret_cast<const uint8_t*>(&sm);
 #pragma unroll
@@ -222,6 +210,8 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   constexpr int NKS = (DS + 15) / 16;   // 16-feature chunks of S and dP that hold data
   constexpr int CPS = DS / 8;           // 16-byte chunks per source row
   constexpr int CPY = copies<NB>();
+  constexpr int PER = kRows * CPS;      // 16-byte items per tensor (a multiple of 64)
+  constexpr int IPT = (PER + kThreads - 1) / kThreads;
   __shared__ __attribute__((aligned(16))) ShortSmem<NB> sm;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -249,16 +239,96 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     reinterpret_cast<uint4*>(sm.q)[t] = make_uint4(0u, 0u, 0u, 0u);
   for (int t = tid; t < kRows; t += kThreads) sm.ninf[t] = -INFINITY;
 
-  // Fixed-point exponent F: (max|dO| max|V| + max|Dlt|) 2^F <= 2^30 over all
-  // of this workgroup's sequences (one 256-row block of maxima each).
-  {
-    float md = 0.0f, mv = 0.0f, ml = 0.0f;
-    for (int s = slot + tid * nslots; s < nseq; s += kThreads * nslots) {
-      const float* nm = a.nmax + ((int64_t)s * a.hpb + head) * 4;
-      md = fmaxf(md, nm[0]);
-      mv = fmaxf(mv, nm[1]);
-      ml = fmaxf(ml, nm[2]);
+  const float sl2 = a.scale * kLog2e;
+  const float inv_sl2 = 1.0f / sl2;
+  const int key = lane & 31;
+  const int j = w * 32 + key;           // this lane's key
+  const bool jok = j < N;
+  const int jc = jok ? j : N - 1;
+  const float* is_lane = (jok ? sm.init_s : sm.ninf) + 16 * g;
+  const ShortOffsets off;
+  const int ld = (int)a.ld_spd;
+  using BT = std::conditional_t<TR, uint32_t, uint8_t>;
+  constexpr int NBT = TR ? 4 : 16;
+
+  // The loads of a sequence, issued one sequence ahead (during the last step
+  // of the previous one) into registers: its Q, dO, K and O rows, item u =
+  // row * DS/8 + chunk held by thread u mod 512 (rows past N read zero: each
+  // resource ends at row N), the LSE of the rows whose chunk 0 the thread
+  // holds, and this lane's K and V row.
+  uint4 rq[IPT], rd[IPT], rk[IPT], ro[IPT];
+  float lsev[IPT], dltv[IPT];
+  bf16x8 kraw[D / 16], vraw[D / 16];
+  auto issue = [&](int s) {
+    const int h = s * a.hpb + head;
+    const int64_t rowbase = (int64_t)h * N * DS;
+    const int64_t nbytes = (int64_t)N * DS * 2;
+    const __amdgpu_buffer_rsrc_t sq = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.q) + rowbase, nbytes);
+    const __amdgpu_buffer_rsrc_t sd = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.d_o) + rowbase, nbytes);
+    const __amdgpu_buffer_rsrc_t sk = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.k) + rowbase, nbytes);
+    const __amdgpu_buffer_rsrc_t so = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.o) + rowbase, nbytes);
+#pragma unroll
+    for (int i = 0; i < IPT; ++i) {
+      const int u = tid + i * kThreads;
+      if (u < PER) {            // wave-uniform
+        const uint32_t voff = (uint32_t)((u / CPS) * DS * 2 + (u % CPS) * 16);
+        rq[i] = buf_b128(sq, voff);
+        rd[i] = buf_b128(sd, voff);
+        rk[i] = buf_b128(sk, voff);
+        ro[i] = buf_b128(so, voff);
+        const int row = u / CPS;
+        lsev[i] = (u % CPS == 0 && row < N) ? a.lse[(int64_t)h * N + row] : -INFINITY;
+      }
     }
+    const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + rowbase;
+    const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + rowbase;
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) {
+      const bool in = jok && kc * 16 + g * 8 < DS;
+      kraw[kc] = in ? *reinterpret_cast<const bf16x8*>(kh + (int64_t)j * DS + kc * 16 + g * 8) : zero_bf16x8();
+      vraw[kc] = in ? *reinterpret_cast<const bf16x8*>(vh + (int64_t)j * DS + kc * 16 + g * 8) : zero_bf16x8();
+    }
+  };
+  // Statistics of the loaded sequence (the prepare stage's definitions and
+  // order of operations): Dlt = dO . O and |dO|^2 per row, reduced over the
+  // DS/8 lanes of the row; |V|^2 per key; their maxima per wave into red.
+  auto stats = [&]() {
+    float md = 0.0f, mv = 0.0f, ml = 0.0f;
+#pragma unroll
+    for (int i = 0; i < IPT; ++i) {
+      const int u = tid + i * kThreads;
+      if (u < PER) {
+        const uint16_t* xp = reinterpret_cast<const uint16_t*>(&ro[i]);
+        const uint16_t* yp = reinterpret_cast<const uint16_t*>(&rd[i]);
+        float acc = 0.0f, sq = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float yf = bf2f(yp[e]);
+          acc = fmaf(bf2f(xp[e]), yf, acc);
+          sq = fmaf(yf, yf, sq);
+        }
+#pragma unroll
+        for (int o = CPS / 2; o >= 1; o >>= 1) {
+          acc += __shfl_xor(acc, o);
+          sq += __shfl_xor(sq, o);
+        }
+        dltv[i] = acc;
+        if (u / CPS < N) {
+          md = fmaxf(md, sq);
+          ml = fmaxf(ml, fabsf(acc));
+        }
+      }
+    }
+    float vq = 0.0f;
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = (float)vraw[kc][e];
+        vq = fmaf(x, x, vq);
+      }
+    vq += __shfl_xor(vq, 32);
+    if (jok) mv = vq;
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
       md = fmaxf(md, __shfl_xor(md, o));
@@ -270,109 +340,94 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
       sm.red[1][w] = mv;
       sm.red[2][w] = ml;
     }
-  }
-  __syncthreads();
-  float md = sm.red[0][0], mv = sm.red[1][0], ml = sm.red[2][0];
+  };
+  // spd bytes of block (qb, this wave's keys) of sequence s: rows
+  // 32 qb + 16 g + r, column j (rows past N read zero).
+  auto fetch = [&](int s, int qb, BT* dst) {
+    const int h = s * a.hpb + head;
+    const __amdgpu_buffer_rsrc_t rs =
+        make_rsrc_n(TR ? seq_spd_t(a, h) : seq_spd(a, h), (int64_t)N * ld);
+    if constexpr (TR) {
+      buf_u128(rs, (uint32_t)(jc * ld + 16 * g), (uint32_t)(qb * 32), reinterpret_cast<uint32_t*>(dst));
+    } else {
+      const uint32_t voff = (uint32_t)((qb * 32 + 16 * g) * ld + jc);
 #pragma unroll
-  for (int i = 1; i < kNW; ++i) {
-    md = fmaxf(md, sm.red[0][i]);
-    mv = fmaxf(mv, sm.red[1][i]);
-    ml = fmaxf(ml, sm.red[2][i]);
-  }
-  const float bound = 1.015f * (sqrtf(md) * sqrtf(mv) + ml);
+      for (int r = 0; r < 16; ++r) dst[r] = (uint8_t)buf_u8(rs, voff, (uint32_t)(r * ld));
+    }
+  };
+
+  // Fixed-point exponent F of the histogram: every term round(dS 2^F) stays
+  // below 2^30 in magnitude, using |dS_ij| <= |dO_i| |V_j| + |Dlt_i| (P <= 1)
+  // with the maxima of the sequence at hand. F only decreases; when it does,
+  // the histogram accumulated so far is shifted to the new scale.
   int fexp = 40;
-  if (bound > 0.0f && bound < INFINITY) {
-    int e;
-    frexpf(bound, &e);
-    fexp = 30 - e;
-    fexp = fexp > 40 ? 40 : (fexp < -100 ? -100 : fexp);
-  }
-  const float sF = ldexpf(1.0f, fexp);
-  const float sl2 = a.scale * kLog2e;
-  const float inv_sl2 = 1.0f / sl2;
-  const float gscale = a.scale * ldexpf(1.0f, -fexp);   // dK and dQ: scale 2^-F
+  bool used = false;
 
-  const int key = lane & 31;
-  const int j = w * 32 + key;           // this lane's key
-  const bool jok = j < N;
-  const int jc = jok ? j : N - 1;
-  const float* is_lane = (jok ? sm.init_s : sm.ninf) + 16 * g;
-  const ShortOffsets off;
-  const int ld = (int)a.ld_spd;
-  using BT = std::conditional_t<TR, uint32_t, uint8_t>;
-  constexpr int NBT = TR ? 4 : 16;
-
+  BT bA[NBT], bB[NBT];
+  issue(slot);
+  fetch(slot, w, bA);
+  stats();
   for (int seq = slot; seq < nseq; seq += nslots) {
     const int h = seq * a.hpb + head;
     const int64_t rowbase = (int64_t)h * N * DS;
-    const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + rowbase;
-    const uint16_t* oh = reinterpret_cast<const uint16_t*>(a.d_o) + rowbase;
-    const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + rowbase;
-    const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + rowbase;
-
-    // the previous sequence's readers are done with the tiles and slots
+    // the previous sequence's readers are done with the tiles and slots, and
+    // its histogram adds are complete
     __syncthreads();
     {
-      // Q, dO, K rows: item u = (tensor, row, chunk < DS/8); rows past N
-      // read zero (the resource ends at row N).
-      constexpr int PER = kRows * CPS;             // items per tensor (multiple of 64)
-      constexpr int NIT = 3 * PER;
-      constexpr int IPT = (NIT + kThreads - 1) / kThreads;
-      const __amdgpu_buffer_rsrc_t rq = make_rsrc_n(qh, (int64_t)N * DS * 2);
-      const __amdgpu_buffer_rsrc_t ro = make_rsrc_n(oh, (int64_t)N * DS * 2);
-      const __amdgpu_buffer_rsrc_t rk = make_rsrc_n(kh, (int64_t)N * DS * 2);
-      uint4 r[IPT];
+      float md = sm.red[0][0], mv = sm.red[1][0], ml = sm.red[2][0];
 #pragma unroll
-      for (int s = 0; s < IPT; ++s) {
-        const int u = tid + s * kThreads;
-        if (u < NIT) {            // wave-uniform: NIT is a multiple of 64
-          const int tn = u / PER, rem = u % PER;
-          const int row = rem / CPS, chunk = rem % CPS;
-          const uint32_t voff = (uint32_t)(row * DS * 2 + chunk * 16);
-          r[s] = buf_b128(tn == 0 ? rq : (tn == 1 ? ro : rk), voff);
-        }
+      for (int i = 1; i < kNW; ++i) {
+        md = fmaxf(md, sm.red[0][i]);
+        mv = fmaxf(mv, sm.red[1][i]);
+        ml = fmaxf(ml, sm.red[2][i]);
       }
-      float st = 0.0f;
-      if (tid < N) st = a.lse2[(int64_t)h * N + tid];
-      else if (tid >= kRows && tid - kRows < N) st = a.dlt[(int64_t)h * N + tid - kRows];
-#pragma unroll
-      for (int s = 0; s < IPT; ++s) {
-        const int u = tid + s * kThreads;
-        if (u < NIT) {
-          const int tn = u / PER, rem = u % PER;
-          const int row = rem / CPS, chunk = rem % CPS;
-          uint16_t* tile = tn == 0 ? sm.q : (tn == 1 ? sm.o : sm.k);
-          *reinterpret_cast<uint4*>(tile + row * D + swz_tile<D>(row, chunk) * 8) = r[s];
-        }
+      // a 1.5 % margin covers the rounding of P and of the products
+      const float bound = 1.015f * (sqrtf(md) * sqrtf(mv) + ml);
+      int fs = 40;
+      if (bound > 0.0f && bound < INFINITY) {
+        int e;
+        frexpf(bound, &e);                 // bound < 2^e
+        fs = 30 - e;
+        fs = fs > 40 ? 40 : (fs < -100 ? -100 : fs);
       }
-      if (tid < kRows)
-        sm.init_s[tid] = tid < N ? -st * inv_sl2 : -INFINITY;
-      else
-        sm.init_p[tid - kRows] = tid - kRows < N ? -st * sF : 0.0f;
+      if (fs < fexp) {                     // workgroup-uniform
+        if (used) {
+          const int sh = fexp - fs > 63 ? 63 : fexp - fs;
+          for (int t = tid; t < ShortSmem<NB>::ENT; t += kThreads)
+            sm.hist[t] = (unsigned long long)((long long)sm.hist[t] >> sh);
+        }
+        fexp = fs;
+      }
+      used = true;
     }
-    // K and 2^F V of this lane's key as B operands (keys past N: zero)
+    const float sF = ldexpf(1.0f, fexp);
+    const float gscale = a.scale * ldexpf(1.0f, -fexp);   // dK and dQ: scale 2^-F
+#pragma unroll
+    for (int i = 0; i < IPT; ++i) {
+      const int u = tid + i * kThreads;
+      if (u < PER) {
+        const int row = u / CPS, chunk = u % CPS;
+        const int lo = row * D + swz_tile<D>(row, chunk) * 8;
+        *reinterpret_cast<uint4*>(sm.q + lo) = rq[i];
+        *reinterpret_cast<uint4*>(sm.o + lo) = rd[i];
+        *reinterpret_cast<uint4*>(sm.k + lo) = rk[i];
+        if (chunk == 0) {
+          // S starts at -LSE log2 e / (scale log2 e) (-inf for an empty row
+          // or a row past N, so P = 0), dP at -Dlt 2^F
+          const float L = lsev[i];
+          sm.init_s[row] = (L == -INFINITY) ? -INFINITY : -(L * kLog2e) * inv_sl2;
+          sm.init_p[row] = row < N ? -dltv[i] * sF : 0.0f;
+        }
+      }
+    }
+    // K and 2^F V of this lane's key as B operands (the scale is exact in bf16)
     bf16x8 kf[D / 16], vf[D / 16];
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) {
-      const bool in = jok && kc * 16 + g * 8 < DS;
-      kf[kc] = in ? *reinterpret_cast<const bf16x8*>(kh + (int64_t)j * DS + kc * 16 + g * 8) : zero_bf16x8();
-      const bf16x8 v8 = in ? *reinterpret_cast<const bf16x8*>(vh + (int64_t)j * DS + kc * 16 + g * 8) : zero_bf16x8();
+      kf[kc] = kraw[kc];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) vf[kc][e] = (__bf16)((float)v8[e] * sF);
+      for (int e = 0; e < 8; ++e) vf[kc][e] = (__bf16)((float)vraw[kc][e] * sF);
     }
-
-    // spd bytes of block (qb, this wave's keys): rows 32 qb + 16 g + r, column j.
-    const __amdgpu_buffer_rsrc_t rs =
-        make_rsrc_n(TR ? seq_spd_t(a, h) : seq_spd(a, h), (int64_t)N * ld);
-    auto fetch = [&](int qb, BT* dst) {
-      if constexpr (TR) {
-        buf_u128(rs, (uint32_t)(jc * ld + 16 * g), (uint32_t)(qb * 32), reinterpret_cast<uint32_t*>(dst));
-      } else {
-        const uint32_t voff = (uint32_t)((qb * 32 + 16 * g) * ld + jc);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) dst[r] = (uint8_t)buf_u8(rs, voff, (uint32_t)(r * ld));
-      }
-    };
 
     f32x16 dk = zero_f32x16(), dv = zero_f32x16(), dq = zero_f32x16();
     const bool wact = w < nb;
@@ -386,29 +441,44 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
           const bf16x8 kt = lds_tr_operand(sm.k + (src * 32 + 8 * q) * D, off.tr[0], off.tr[1]);
-          const bf16x8 st = lds_tr_operand(&sm.xs[par][src][8 * q * D], off.tr[0], off.tr[1]);
-          dq = mfma32(kt, st, dq);
+          const bf16x8 sv = lds_tr_operand(&sm.xs[par][src][8 * q * D], off.tr[0], off.tr[1]);
+          dq = mfma32(kt, sv, dq);
         }
       }
     };
 
-    BT bA[NBT], bB[NBT];
-    fetch(w & 7, bA);
     wait_loads();
     __syncthreads();
 #pragma unroll 1
-    for (int t = 0; t < kNW; t += 2) {
-      fetch((w + t + 1) & 7, bB);
+    for (int t = 0; t < kNW - 2; t += 2) {
+      fetch(seq, (w + t + 1) & 7, bB);
       sched_fence();
       if (t > 0) step_b(t - 1, 1);
       step_a(t, sm.xs[0][w], bA);
       __syncthreads();
-      fetch((w + t + 2) & 7, bA);
+      fetch(seq, (w + t + 2) & 7, bA);
       sched_fence();
       step_b(t, 0);
       step_a(t + 1, sm.xs[1][w], bB);
       __syncthreads();
     }
+    // The last two steps, with the next sequence's loads issued at the start
+    // of the last one (the last sequence reloads itself, so the code is the
+    // same on every path and the waits stay exact).
+    fetch(seq, (w + kNW - 1) & 7, bB);
+    sched_fence();
+    step_b(kNW - 3, 1);
+    step_a(kNW - 2, sm.xs[0][w], bA);
+    __syncthreads();
+    {
+      const int nxt = seq + nslots < nseq ? seq + nslots : seq;
+      issue(nxt);
+      fetch(nxt, w, bA);
+    }
+    sched_fence();
+    step_b(kNW - 2, 0);
+    step_a(kNW - 1, sm.xs[1][w], bB);
+    __syncthreads();
     step_b(kNW - 1, 1);
 
     // dK, dV of key j; dQ of query w * 32 + key (features 8 u + 4 g .. + 3)
@@ -432,8 +502,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
         *reinterpret_cast<uint2*>(dqp + c) = pq;
       }
     }
+    // statistics of the next sequence (its loads were issued above)
+    stats();
   }
-
   __syncthreads();
   const double unscale = ldexp(1.0, -fexp);
   for (int bkt = tid; bkt < a.n_buckets; bkt += kThreads) {
@@ -442,6 +513,10 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     for (int c = 0; c < CPY; ++c) t += (long long)sm.hist[bkt * CPY + ((c + bkt) & (CPY - 1))];
     if (t != 0) atomicAdd(&a.dtable[(int64_t)head * a.n_buckets + bkt], (float)((double)t * unscale));
   }
+}
+
+__global__ __launch_bounds__(256) void zero_f32_kernel(float* p, int n) {
+  for (int t = threadIdx.x; t < n; t += 256) p[t] = 0.0f;
 }
 
 template <int DS, int NB>
@@ -474,6 +549,10 @@ bool bwd_short_applies(const BwdArgs& a, int d) {
 }
 
 hipError_t launch_bwd_short_bf16(const BwdArgs& a, int d, hipStream_t s) {
+  // dtable is cleared by a fill kernel (the workgroups add into it at their end)
+  hipLaunchKernelGGL(zero_f32_kernel, dim3(1), dim3(256), 0, s, a.dtable, a.hpb * a.n_buckets);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   if (a.n_buckets <= 127)
     launch_short_nb<128>(a, d, s);
   else

@@ -96,8 +96,8 @@ hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStrea
 hipError_t launch_bwd(const BwdArgs& a, int d, bool bf16, int phase, hipStream_t s);
 hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s);
 hipError_t launch_dq_bf16(const BwdArgs& a, int d, hipStream_t s);
-// Sequences of at most 256 rows (bf16, d <= 32, not a ring step): dK, dV,
-// dQ and dtable in one persistent kernel, after the prepare stage.
+// Sequences of at most 256 rows (bf16, d <= 32, not a ring step): the whole
+// backward (prepare stage, dK, dV, dQ, dtable) in one persistent kernel.
 bool bwd_short_applies(const BwdArgs& a, int d);
 hipError_t launch_bwd_short_bf16(const BwdArgs& a, int d, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, bool out_bf16, hipStream_t s);

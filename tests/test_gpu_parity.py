@@ -371,6 +371,57 @@ def test_batch_of_graphs(B, N, d, spd_kind, dt):
     assert rel_l2(to_np(dtab), dt_ref) <= TOL[dt]["grad"]
 
 
+@pytest.mark.parametrize("B,hpb,N,d,spd_kind", [
+    (12, 64, 80, 8, "per_graph"),       # 4 workgroup slots: 3 sequences per workgroup
+    (12, 64, 256, 32, "per_graph_t"),
+    (64, 8, 33, 16, "shared"),          # 32 slots: 2 sequences per workgroup
+])
+def test_batch_several_graphs_per_workgroup(B, hpb, N, d, spd_kind):
+    """Sequences of at most 256 nodes with more sequences than the fused
+    backward has workgroup slots, so each workgroup takes several sequences
+    of one head in turn. V and dO double every third of the batch, so a
+    workgroup's later sequences have larger gradient bounds: the fixed-point
+    exponent of its histogram drops and the sums accumulated so far are
+    rescaled. Every graph's O, LSE, dQ, dK, dV and the summed dtable equal
+    the oracle."""
+    nb = 12
+    g = np.random.default_rng(B * N + d + hpb)
+    shape = (B, hpb, N, d)
+    q, k, v = (g.standard_normal(shape).astype(np.float32) / np.float32(math.sqrt(d)) for _ in range(3))
+    do = g.standard_normal(shape).astype(np.float32)
+    grow = np.float32(2.0) ** ((np.arange(B) * 3) // B).astype(np.float32)
+    v *= grow[:, None, None, None]
+    do *= grow[:, None, None, None]
+    q, k, v, do = (synth.round_bf16(x) for x in (q, k, v, do))
+    table = (g.standard_normal((hpb, nb)) * 0.5).astype(np.float32)
+    if spd_kind == "shared":
+        spd = g.integers(0, nb + 2, size=(N, N)).astype(np.uint8)
+        spd_b = [spd] * B
+    else:
+        spd = g.integers(0, nb + 2, size=(B, N, N)).astype(np.uint8)
+        spd_b = list(spd)
+    Q, K, V, dO = (to_dev(x, torch.bfloat16) for x in (q, k, v, do))
+    T = to_dev(table)
+    S = to_dev(spd, torch.uint8)
+    St = to_dev(np.ascontiguousarray(np.swapaxes(spd, -1, -2)), torch.uint8) if spd_kind == "per_graph_t" else None
+    scale = 1.0 / math.sqrt(d)
+    say(f"batch bf16 B={B} hpb={hpb} N={N} d={d} {spd_kind} (several graphs per workgroup)")
+    O, L = gt.gt_attn_fwd_batch(Q, K, V, S, T, scale=scale)
+    dq, dk, dv, dtab = gt.gt_attn_bwd_batch(Q, K, V, S, T, O, L, dO, scale=scale, spd_t=St)
+    torch.cuda.synchronize()
+    dt_ref = np.zeros((hpb, nb))
+    for b in range(B):
+        ref = _oracle_full(q[b], k[b], v[b], do[b], table, spd_b[b], scale)
+        got = dict(o=to_np(O[b]), lse=to_np(L[b]), dq=to_np(dq[b]), dk=to_np(dk[b]),
+                   dv=to_np(dv[b]))
+        check_fwd(f"batch graph {b}", got["o"], got["lse"], ref["o"], ref["lse"], "bf16")
+        check_grads(f"batch graph {b}", got, ref, "bf16")
+        dt_ref += ref["dtable"]
+    err = rel_l2(to_np(dtab), dt_ref)
+    say(f"dtable rel-L2 {err:.3e}")
+    assert err <= TOL["bf16"]["grad"]
+
+
 def test_forward_is_deterministic():
     H, N, d, nb = 4, 777, 64, 20
     q, k, v, do, table, spd = _case(H, N, d, nb, seed=21, dt="bf16")
