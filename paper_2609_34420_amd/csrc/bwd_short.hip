@@ -205,7 +205,13 @@ __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets
   }
 }
 
-template <int DS, int NB, bool TR>
+// STAGE (no transpose given, spd rows 16-byte aligned): the spd block of a
+// step is loaded row-wise, 16 bytes per lane (lane l: row l / 2, bytes
+// 16 (l % 2) .. + 15 of the block's 32 x 32), written to the first KiB of
+// the wave's dS slot of that step (free until the block's dS is stored
+// there), and each lane reads its key's 16 query bytes back with two 8-bit
+// transposing LDS reads, instead of 16 byte gathers from global memory.
+template <int DS, int NB, bool TR, bool STAGE>
 __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) {
   constexpr int NKS = (DS + 15) / 16;   // 16-feature chunks of S and dP that hold data
   constexpr int CPS = DS / 8;           // 16-byte chunks per source row
@@ -248,8 +254,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   const float* is_lane = (jok ? sm.init_s : sm.ninf) + 16 * g;
   const ShortOffsets off;
   const int ld = (int)a.ld_spd;
-  using BT = std::conditional_t<TR, uint32_t, uint8_t>;
-  constexpr int NBT = TR ? 4 : 16;
+  using BT = std::conditional_t<TR || STAGE, uint32_t, uint8_t>;
+  constexpr int NBT = TR || STAGE ? 4 : 16;
+  static_assert(!(TR && STAGE), "one way of reading spd");
 
   // The loads of a sequence, issued one sequence ahead (during the last step
   // of the previous one) into registers: its Q, dO, K and O rows, item u =
@@ -343,11 +350,18 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   };
   // spd bytes of block (qb, this wave's keys) of sequence s: rows
   // 32 qb + 16 g + r, column j (rows past N read zero).
+  const uint32_t voff_st = (uint32_t)((lane >> 1) * ld + 16 * (lane & 1) + w * 32);
+  int off_tr8[2];   // byte offsets in the staged block of the two transposing reads
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+    off_tr8[hh] = (16 * g + 8 * hh + ((lane & 15) >> 1)) * 32 + 16 * ((lane >> 4) & 1) + 8 * (lane & 1);
   auto fetch = [&](int s, int qb, BT* dst) {
     const int h = s * a.hpb + head;
     const __amdgpu_buffer_rsrc_t rs =
         make_rsrc_n(TR ? seq_spd_t(a, h) : seq_spd(a, h), (int64_t)N * ld);
-    if constexpr (TR) {
+    if constexpr (STAGE) {
+      buf_u128(rs, voff_st, (uint32_t)(qb * 32 * ld), reinterpret_cast<uint32_t*>(dst));
+    } else if constexpr (TR) {
       buf_u128(rs, (uint32_t)(jc * ld + 16 * g), (uint32_t)(qb * 32), reinterpret_cast<uint32_t*>(dst));
     } else {
       const uint32_t voff = (uint32_t)((qb * 32 + 16 * g) * ld + jc);
@@ -372,7 +386,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     const int64_t rowbase = (int64_t)h * N * DS;
     // the previous sequence's readers are done with the tiles and slots, and
     // its histogram adds are complete
-    __syncthreads();
+    lds_barrier();
     {
       float md = sm.red[0][0], mv = sm.red[1][0], ml = sm.red[2][0];
 #pragma unroll
@@ -433,7 +447,26 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     const bool wact = w < nb;
     auto step_a = [&](int t, uint16_t* xs, const BT* b) {
       const int qb = (w + t) & 7;
-      if (wact && qb < nb) block_dkdv<NKS, NB>(sm, off, kf, vf, b, is_lane, sl2, qb, xs, dk, dv);
+      if (wact && qb < nb) {
+        if constexpr (STAGE) {
+          typedef int i32x2 __attribute__((ext_vector_type(2)));
+          typedef __attribute__((address_space(3))) i32x2* lds_i32x2;
+          uint8_t* st8 = reinterpret_cast<uint8_t*>(xs);
+          uint4 v4 = make_uint4(b[0], b[1], b[2], b[3]);
+          opaque(v4);
+          *reinterpret_cast<uint4*>(st8 + 16 * lane) = v4;
+          uint32_t wv[4];
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const i32x2 v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2)(void*)(st8 + off_tr8[hh]));
+            wv[2 * hh] = (uint32_t)v.x;
+            wv[2 * hh + 1] = (uint32_t)v.y;
+          }
+          block_dkdv<NKS, NB>(sm, off, kf, vf, wv, is_lane, sl2, qb, xs, dk, dv);
+        } else {
+          block_dkdv<NKS, NB>(sm, off, kf, vf, b, is_lane, sl2, qb, xs, dk, dv);
+        }
+      }
     };
     auto step_b = [&](int t, int par) {
       const int src = (w - t) & 7;      // key block whose dS for query block w was stored at step t
@@ -448,19 +481,19 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     };
 
     wait_loads();
-    __syncthreads();
+    lds_barrier();
 #pragma unroll 1
     for (int t = 0; t < kNW - 2; t += 2) {
       fetch(seq, (w + t + 1) & 7, bB);
       sched_fence();
       if (t > 0) step_b(t - 1, 1);
       step_a(t, sm.xs[0][w], bA);
-      __syncthreads();
+      lds_barrier();
       fetch(seq, (w + t + 2) & 7, bA);
       sched_fence();
       step_b(t, 0);
       step_a(t + 1, sm.xs[1][w], bB);
-      __syncthreads();
+      lds_barrier();
     }
     // The last two steps, with the next sequence's loads issued at the start
     // of the last one (the last sequence reloads itself, so the code is the
@@ -469,7 +502,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     sched_fence();
     step_b(kNW - 3, 1);
     step_a(kNW - 2, sm.xs[0][w], bA);
-    __syncthreads();
+    lds_barrier();
     {
       const int nxt = seq + nslots < nseq ? seq + nslots : seq;
       issue(nxt);
@@ -478,7 +511,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     sched_fence();
     step_b(kNW - 2, 0);
     step_a(kNW - 1, sm.xs[1][w], bB);
-    __syncthreads();
+    lds_barrier();
     step_b(kNW - 1, 1);
 
     // dK, dV of key j; dQ of query w * 32 + key (features 8 u + 4 g .. + 3)
@@ -505,7 +538,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     // statistics of the next sequence (its loads were issued above)
     stats();
   }
-  __syncthreads();
+  lds_barrier();
   const double unscale = ldexp(1.0, -fexp);
   for (int bkt = tid; bkt < a.n_buckets; bkt += kThreads) {
     long long t = 0;
@@ -527,9 +560,11 @@ void launch_short_t(const BwdArgs& a, hipStream_t s) {
   if (slots > nseq) slots = nseq;
   const dim3 grid((unsigned)(slots * a.hpb));
   if (a.spd_t)
-    hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, true>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, true, false>), grid, dim3(kThreads), 0, s, a);
+  else if (a.spd_vec)
+    hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, false, true>), grid, dim3(kThreads), 0, s, a);
   else
-    hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, false>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, false, false>), grid, dim3(kThreads), 0, s, a);
 }
 
 template <int NB>

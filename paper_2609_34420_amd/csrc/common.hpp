@@ -41,6 +41,15 @@ __device__ __forceinline__ void opaque(uint4& x) {
 __device__ __forceinline__ void opaque(uint32_t& x) { asm volatile("" : "+v"(x)); }
 __device__ __forceinline__ void opaque_f(float& x) { asm volatile("" : "+v"(x)); }
 
+// Workgroup barrier that orders LDS accesses only: each wave waits for its
+// own LDS operations (lgkmcnt), not for its global loads, so prefetches stay
+// in flight across it. For kernels whose waves share nothing but LDS.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Wait for every outstanding vector-memory load (s_waitcnt vmcnt(0) with the
 // other counters left free). Used once before a software-pipelined loop, so
 // that values loaded ahead of it are not treated as pending inside the loop,
