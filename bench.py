@@ -236,9 +236,10 @@ def measured_traffic(workload: str, kernel: str):
     return None if k is None else k["fetch_bytes"] + k["write_bytes"]
 
 
-# Device sources of the timed kernels (the host-side C ABI and the merge
-# kernel do not change what the counters measured).
-_HOST_OR_UNTIMED = {"api.hip", "merge.hip"}
+# Device sources of the kernels the traffic record measured: every source
+# except the host-side C ABI and the kernels that the full-width workloads
+# never launch (the merge, and the short-sequence forward and backward).
+_HOST_OR_UNTIMED = {"api.hip", "merge.hip", "fwd_short.hip", "bwd_short.hip"}
 
 
 def kernel_sources_sha256() -> str:

@@ -19,7 +19,7 @@ PKG = Path(__file__).resolve().parent
 CSRC = PKG / "csrc"
 LIB = PKG / "libgtattn.so"
 BUILD_DIR = PKG / "_build"
-SOURCES = ["api.hip", "fwd.hip", "bwd.hip", "bwd_dkdv.hip", "bwd_dq.hip", "bwd_short.hip", "merge.hip"]
+SOURCES = ["api.hip", "fwd.hip", "bwd.hip", "bwd_dkdv.hip", "bwd_dq.hip", "bwd_short.hip", "fwd_short.hip", "merge.hip"]
 ARCH = os.environ.get("GT_OFFLOAD_ARCH", "gfx950")
 
 

@@ -35,6 +35,7 @@
 #include "common.hpp"
 #include "kernels.hpp"
 #include "stage.hpp"
+#include "fwd_tile.hpp"
 
 namespace gt {
 
@@ -45,117 +46,6 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kBC = 64;            // keys per LDS tile
 constexpr int kQB = 2;             // 32-query blocks per wave
 constexpr int kKB = kBC / 32;      // 32-key blocks per tile
-constexpr float kBlockSumLimit = 256.0f;
-
-// Softmax state of one 32-query block (per lane: one query, one lane half).
-struct SoftmaxState {
-  float m;        // reference max (log2 units), -inf before any finite score
-  float mneg;     // -m, or 0 while m = -inf
-  float l;        // this lane half's partial row sum, relative to m
-};
-
-// Per-lane LDS element offsets of the operand reads (tile-relative; the
-// 32-key block and 8-key step offsets are immediates).
-template <int D>
-struct FwdOffsets {
-  int k[D / 16];          // K rows perm32(lane), feature chunk 2 kc + g
-  int v[2][D / 32];       // transposing reads h = 0, 1 of V, feature block cb
-  __device__ __forceinline__ FwdOffsets() {
-#pragma unroll
-    for (int kc = 0; kc < D / 16; ++kc) k[kc] = row_operand_off<D>(kc);
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int cb = 0; cb < D / 32; ++cb) v[h][cb] = tr_operand_off<D>(h, cb);
-  }
-};
-
-
-// p = 2^x for the lane's 16 keys, as two bf16x8 operands, and their sum.
-__device__ __forceinline__ float exp_block(const float (&x)[16], bf16x8& p0, bf16x8& p1) {
-  float p[16];
-#pragma unroll
-  for (int r = 0; r < 16; ++r) p[r] = exp2_fast(x[r]);
-  p0 = cvt_bf16x8(p);
-  p1 = cvt_bf16x8(p + 8);
-  return sum_bf16x8(p1, sum_bf16x8(p0, 0.0f));
-}
-
-// Softmax of one 32x32 score block s (accumulated as bias/scale + q.k) and
-// its P^T V product into acc. The exact path runs only when some lane's
-// block sum exceeds the limit (or is not finite) or a row has no reference.
-template <int D, bool MASK>
-__device__ __forceinline__ void softmax_pv(const f32x16& s, const bf16x8 (&vop)[2][D / 32],
-                                           int64_t jrem, float sl2, SoftmaxState& st,
-                                           f32x16 (&acc)[D / 32]) {
-  constexpr int NCB = D / 32;
-  const int g = (threadIdx.x >> 5) & 1;
-  float x[16];
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const float xv = fmaf(s[r], sl2, st.mneg);
-    if constexpr (MASK)
-      x[r] = (16 * g + r < jrem) ? xv : -INFINITY;
-    else
-      x[r] = xv;
-  }
-  bf16x8 p0, p1;
-  float bs = exp_block(x, p0, p1);
-  if (__any(!(bs <= kBlockSumLimit) || st.m == -INFINITY)) {
-    // Exact path: move the reference to the row max of this block. x holds
-    // scores relative to the old reference (absolute while there is none).
-    float mx = -INFINITY;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, x[r]);
-    mx -= st.mneg;
-    const float mall = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(st.m, mall);
-    const float alpha = (mnew == -INFINITY) ? 1.0f : exp2_fast(st.m - mnew);
-    st.l *= alpha;
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[cb][r] *= alpha;
-    const float mneg_new = (mnew == -INFINITY) ? 0.0f : -mnew;
-    const float shift = mneg_new - st.mneg;
-    st.m = mnew;
-    st.mneg = mneg_new;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) x[r] += shift;
-    bs = exp_block(x, p0, p1);
-  }
-  st.l += bs;
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) {
-    acc[cb] = mfma32(vop[0][cb], p0, acc[cb]);
-    acc[cb] = mfma32(vop[1][cb], p1, acc[cb]);
-  }
-}
-
-// Score product of one 32x32 unit: bias entries into the accumulator, then
-// the K operands of key block kb (read from the staged tile) times the
-// unit's Q^T.
-// NK: the 16-feature chunks that hold data (all D / 16, or fewer when the
-// source rows are narrower than the tile and the rest is zero).
-template <int D, int NK>
-__device__ __forceinline__ void issue_scores(const float* tab, const uint32_t (&w)[4], uint32_t lane4,
-                                             const uint16_t* sK, const int (&koff)[D / 16], int kb,
-                                             const bf16x8 (&q)[D / 16], f32x16& s) {
-  load_bias(tab, w, lane4, s);
-#pragma unroll
-  for (int kc = 0; kc < NK; ++kc) s = mfma32(lds_b128(sK + kb * 32 * D + koff[kc]), q[kc], s);
-}
-
-template <int D>
-__device__ __forceinline__ void read_v(const uint16_t* sV, const FwdOffsets<D>& off, int kb,
-                                       bf16x8 (&vop)[2][D / 32]) {
-#pragma unroll
-  for (int q = 0; q < 2; ++q)
-#pragma unroll
-    for (int cb = 0; cb < D / 32; ++cb)
-      vop[q][cb] = lds_tr_operand(sV + (kb * 32 + 8 * q) * D, off.v[0][cb], off.v[1][cb]);
-}
-
 // Unpipelined tile (ragged or unaligned shapes): for each 32-key block the
 // score products of both query blocks, then their softmax and P V.
 template <int D, int NK, bool MASK>
@@ -484,234 +374,6 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   }
 }
 
-// Persistent forward for sequences of 33 to 256 rows with at most 127
-// buckets (bf16 in and out, head dims 8, 16, 32 on 32-wide tiles; spd rows
-// 4-byte aligned). Each wave owns 32 queries, so a workgroup covers a whole
-// sequence, and the sequence's K and V (all rows) sit in LDS: one pair of
-// barriers per sequence instead of one barrier per key tile. The per-lane
-// bias table holds the byte values 0..127 (bytes of 128 or more are mapped
-// to the padding entry 127, bias 0) and an entry of -inf (128) that masks
-// the keys past N: with K and V that is 65 KB, so two workgroups share a
-// compute unit and every SIMD runs four waves. The workgroups are
-// persistent: workgroup w takes head (w mod hpb) of every (G / hpb)-th
-// sequence, fills the table once, and loads the next sequence's K, V and Q
-// rows into registers while it computes the current one. spd words stream
-// two key blocks ahead across sequences (read 16 bytes at a time from 4-byte
-// aligned offsets, through a resource that ends with the sequence's matrix);
-// the score product of key block kb + 1 is issued before the softmax of
-// block kb. TAIL: N is not a multiple of 32.
-constexpr int kShortTabEntries = 129;
-template <int DS, bool TAIL>
-__global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) {
-  constexpr int D = 32;
-  constexpr int NKC = D / 16;
-  constexpr int NKS = (DS + 15) / 16;
-  constexpr int NCB = D / 32;
-  constexpr int ROWS = 256;
-  constexpr int CPS = DS / 8;                   // 16-byte chunks per source row
-  constexpr int PER = ROWS * CPS;               // chunks per tensor (a multiple of 64)
-  constexpr int IPT = (PER + kThreads - 1) / kThreads;
-  __shared__ __attribute__((aligned(16))) uint16_t sK[ROWS * D], sV[ROWS * D];
-  __shared__ __attribute__((aligned(16))) float sTab[kShortTabEntries * 64];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, w = wave_id();
-  const int col = lane & 31, g = lane >> 5;
-  const uint32_t lane4 = (uint32_t)lane * 4u;
-  const int N = (int)a.Sq;
-  const int nkb = (N + 31) / 32;                // at least 2
-  const int G = (int)gridDim.x;
-  const int lw = (int)xcd_remap(blockIdx.x, G);
-  const int head = lw % a.hpb;
-  const int slot = lw / a.hpb;
-  const int nslots = G / a.hpb;
-  const int nseq = a.H / a.hpb;
-  const float sl2 = a.scale * kLog2e;
-  const int ld = (int)a.ld_spd;
-  const int qi = w * 32 + col;                  // this lane's query
-  const int qc = qi < N ? qi : N - 1;
-  const bool wact = w * 32 < N;
-  const FwdOffsets<D> off;
-
-  // table entry (b, lane) at float 64 b + lane: bias / scale for b below
-  // n_buckets, 0 up to 127, -inf at 128; zero K, V (features past the head
-  // dim stay zero)
-  {
-    const float inv_scale = 1.0f / a.scale;
-    const float* th = a.table + (int64_t)head * a.n_buckets;
-    for (int t = tid; t < kShortTabEntries * 16; t += kThreads) {
-      const int bk = t >> 4;
-      const float x = bk < 128 ? (bk < a.n_buckets ? th[bk] * inv_scale : 0.0f) : -INFINITY;
-      reinterpret_cast<float4*>(sTab)[t] = make_float4(x, x, x, x);
-    }
-    for (int t = tid; t < ROWS * D / 8; t += kThreads) {
-      reinterpret_cast<uint4*>(sK)[t] = make_uint4(0u, 0u, 0u, 0u);
-      reinterpret_cast<uint4*>(sV)[t] = make_uint4(0u, 0u, 0u, 0u);
-    }
-  }
-
-  // Loads of sequence s into registers: its K and V rows (item u = row *
-  // DS/8 + chunk, thread u mod 512; rows past N read zero) and this lane's
-  // Q row.
-  uint4 rk[IPT], rv[IPT];
-  bf16x8 qf[NKC], qn[NKC];
-  auto issue = [&](int s) {
-    const int h = s * a.hpb + head;
-    const int64_t rowbase = (int64_t)h * N * DS;
-    const int64_t nbytes = (int64_t)N * DS * 2;
-    const __amdgpu_buffer_rsrc_t sk = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.k) + rowbase, nbytes);
-    const __amdgpu_buffer_rsrc_t sv = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.v) + rowbase, nbytes);
-#pragma unroll
-    for (int i = 0; i < IPT; ++i) {
-      const int u = tid + i * kThreads;
-      if (u < PER) {
-        const uint32_t vo = (uint32_t)((u / CPS) * DS * 2 + (u % CPS) * 16);
-        rk[i] = buf_b128(sk, vo);
-        rv[i] = buf_b128(sv, vo);
-      }
-    }
-    const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + rowbase;
-#pragma unroll
-    for (int kc = 0; kc < NKC; ++kc)
-      qn[kc] = (kc * 16 + g * 8 < DS) ? *reinterpret_cast<const bf16x8*>(qh + (int64_t)qc * DS + kc * 16 + g * 8)
-                                      : zero_bf16x8();
-  };
-  auto spd_rs = [&](int s) {
-    const int h = s * a.hpb + head;
-    return make_rsrc_n(seq_spd(a, h), (int64_t)N * ld);
-  };
-  const uint32_t voff = (uint32_t)(qc * ld + 16 * g);
-  // Bucket words of key block kb as table entries: bytes of 128 or more to
-  // the padding entry 127; with TAIL, keys past N to the -inf entry.
-  auto entries = [&](const uint32_t (&wsrc)[4], int kb, uint32_t (&e)[4]) {
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      e[u] = wsrc[u];
-      opaque(e[u]);
-    }
-    if (__any(((e[0] | e[1] | e[2] | e[3]) & 0x80808080u) != 0)) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        uint32_t x = e[u];
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-          if ((x >> (8 * k + 7)) & 1u) x = (x & ~(0xffu << (8 * k))) | (0x7fu << (8 * k));
-        e[u] = x;
-      }
-    }
-    if constexpr (TAIL) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (kb * 32 + 16 * g + 4 * u >= N) e[u] = 0x80808080u;   // N is a multiple of 4
-    }
-  };
-
-  SoftmaxState st;
-  f32x16 acc[NCB];
-  uint32_t wd[3][4];                              // spd words of key blocks kb, kb + 1, kb + 2
-
-  // One sequence: its K, V, Q are in registers on entry (loaded during the
-  // previous one), and wd[0], wd[1] hold its first spd words. The spd words
-  // stream over (sequence, key block) two blocks ahead: past the last block
-  // come blocks 0 and 1 of the next sequence.
-  auto run = [&](int s) {
-    const int nxt = s + nslots < nseq ? s + nslots : s;
-    const __amdgpu_buffer_rsrc_t rs = spd_rs(s);
-    const __amdgpu_buffer_rsrc_t rn = spd_rs(nxt);
-    __syncthreads();            // the previous sequence's reads of K and V are done
-#pragma unroll
-    for (int i = 0; i < IPT; ++i) {
-      const int u = tid + i * kThreads;
-      if (u < PER) {
-        const int row = u / CPS, chunk = u % CPS;
-        const int lo = row * D + swz_tile<D>(row, chunk) * 8;
-        *reinterpret_cast<uint4*>(sK + lo) = rk[i];
-        *reinterpret_cast<uint4*>(sV + lo) = rv[i];
-      }
-    }
-#pragma unroll
-    for (int kc = 0; kc < NKC; ++kc) qf[kc] = qn[kc];
-    __syncthreads();            // K, V of this sequence visible
-    issue(nxt);
-    sched_fence();
-    st.m = -INFINITY;
-    st.mneg = 0.0f;
-    st.l = 0.0f;
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero_f32x16();
-    f32x16 sc;
-    if (wact) {
-      uint32_t e[4];
-      entries(wd[0], 0, e);
-      issue_scores<D, NKS>(sTab, e, lane4, sK, off.k, 0, qf, sc);
-    }
-#pragma unroll
-    for (int kb = 0; kb < ROWS / 32; ++kb) {
-      if (kb < nkb) {
-        // words of block kb + 2 (of the next sequence past the end)
-        {
-          const int kf = kb + 2;
-          uint32_t* dst = wd[(kb + 2) % 3];
-          if (kf < nkb)
-            buf_u128(rs, voff, (uint32_t)(kf * 32), dst);
-          else
-            buf_u128(rn, voff, (uint32_t)((kf - nkb) * 32), dst);
-        }
-        sched_fence();
-        if (wact) {
-          f32x16 sn;
-          if (kb + 1 < nkb) {
-            uint32_t e[4];
-            entries(wd[(kb + 1) % 3], kb + 1, e);
-            issue_scores<D, NKS>(sTab, e, lane4, sK, off.k, kb + 1, qf, sn);
-          }
-          bf16x8 vop[2][NCB];
-          read_v<D>(sV, off, kb, vop);
-          softmax_pv<D, false>(sc, vop, 32, sl2, st, acc);
-          sc = sn;
-        }
-      }
-    }
-    // the next sequence's first two word sets sit in wd[nkb % 3], wd[(nkb + 1) % 3]
-    if (nkb % 3 == 1) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) { const uint32_t t0 = wd[0][e]; wd[0][e] = wd[1][e]; wd[1][e] = wd[2][e]; wd[2][e] = t0; }
-    } else if (nkb % 3 == 2) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) { const uint32_t t2 = wd[2][e]; wd[2][e] = wd[1][e]; wd[1][e] = wd[0][e]; wd[0][e] = t2; }
-    }
-    // epilogue: O = O_acc / l, LSE = (m + log2 l) ln 2
-    if (wact) {
-      const float lt = st.l + __shfl_xor(st.l, 32);
-      if (qi < N) {
-        const int h = s * a.hpb + head;
-        const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
-        const float lse_out = lt > 0.0f ? (st.m + __log2f(lt)) * kLn2 : -INFINITY;
-        uint16_t* op = reinterpret_cast<uint16_t*>(a.o) + ((int64_t)h * N + qi) * DS;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int c = 8 * u + 4 * g;
-          if (c >= DS) continue;
-          uint2 pk;
-          pk.x = (uint32_t)f2bf(acc[0][4 * u] * inv) | ((uint32_t)f2bf(acc[0][4 * u + 1] * inv) << 16);
-          pk.y = (uint32_t)f2bf(acc[0][4 * u + 2] * inv) | ((uint32_t)f2bf(acc[0][4 * u + 3] * inv) << 16);
-          *reinterpret_cast<uint2*>(op + c) = pk;
-        }
-        if (g == 0) a.lse[(int64_t)h * N + qi] = lse_out;
-      }
-    }
-  };
-
-  issue(slot);
-  {
-    const __amdgpu_buffer_rsrc_t rs = spd_rs(slot);
-    buf_u128(rs, voff, 0u, wd[0]);
-    buf_u128(rs, voff, 32u, wd[1]);
-  }
-  for (int s = slot; s < nseq; s += nslots) run(s);
-  wait_vmcnt<0>();     // drain the loads issued for the last (repeated) sequence
-}
-
 // Vector-ALU path (fp32 inputs, any head dim): one thread per query row,
 // keys staged through LDS, fp32 math with the hardware exp2 and logf; o is
 // fp32.
@@ -809,23 +471,6 @@ hipError_t launch_fwd_bf16(const FwdArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)(nqb * a.H));
   const bool skip = a.Sq % BR != 0;
   const int nseq = a.H / a.hpb;
-  if constexpr (D == 32 && !OUT_F32) {
-    // sequences of at most 256 rows: the persistent whole-sequence kernel
-    if (!a.accumulate && a.row_off == 0 && a.col_off == 0 && a.Sq == a.Sk && a.Sq > 32 &&
-        a.Sq <= 256 && a.n_buckets <= 127 && a.H % a.hpb == 0 &&
-        reinterpret_cast<uintptr_t>(a.spd) % 4 == 0 && a.ld_spd % 4 == 0 && a.spd_bstride % 4 == 0) {
-      // two workgroups per compute unit where the registers allow four waves per SIMD
-      int slots = (DS <= 16 ? 512 : 256) / a.hpb;
-      if (slots < 1) slots = 1;
-      if (slots > nseq) slots = nseq;
-      const dim3 grids((unsigned)(slots * a.hpb));
-      if (a.Sq % 32 != 0)
-        hipLaunchKernelGGL((fwd_short_bf16_kernel<DS, true>), grids, dim3(kThreads), 0, s, a);
-      else
-        hipLaunchKernelGGL((fwd_short_bf16_kernel<DS, false>), grids, dim3(kThreads), 0, s, a);
-      return hipGetLastError();
-    }
-  }
   if constexpr (D == 32) {
     // batches of short sequences: two sequences per workgroup
     constexpr int BRP = kWaves / 2 * 32 * kQB;
@@ -862,6 +507,7 @@ hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStrea
   // bf16 runs on the matrix cores at every head dim: 8 and 16 on 32-wide
   // tiles whose extra features are zero. fp32 runs on the vector ALUs.
   if (bf16) {
+    if (!out_f32 && fwd_short_applies(a, d)) return launch_fwd_short_bf16(a, d, s);
     switch (d) {
       case 8: return out_f32 ? launch_fwd_bf16<32, 8, true>(a, s) : launch_fwd_bf16<32, 8, false>(a, s);
       case 16: return out_f32 ? launch_fwd_bf16<32, 16, true>(a, s) : launch_fwd_bf16<32, 16, false>(a, s);

@@ -92,6 +92,10 @@ struct MergeArgs {
 
 // Launchers return the hipError_t of the launch.
 hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStream_t s);
+// Sequences of 33 to 256 rows (bf16 in and out, d <= 32, at most 127
+// buckets, spd rows 4-byte aligned): the persistent whole-sequence forward.
+bool fwd_short_applies(const FwdArgs& a, int d);
+hipError_t launch_fwd_short_bf16(const FwdArgs& a, int d, hipStream_t s);
 // phase: -1 = all stages in order, 0 = prepare, 1 = dK/dV/dtable, 2 = dQ.
 hipError_t launch_bwd(const BwdArgs& a, int d, bool bf16, int phase, hipStream_t s);
 hipError_t launch_dkdv_bf16(const BwdArgs& a, int d, hipStream_t s);
