@@ -205,7 +205,7 @@ __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets
   }
 }
 
-// STAGE (no transpose given, spd rows 16-byte aligned): the spd block of a
+// STAGE (no transpose given, spd rows 4-byte aligned): the spd block of a
 // step is loaded row-wise, 16 bytes per lane (lane l: row l / 2, bytes
 // 16 (l % 2) .. + 15 of the block's 32 x 32), written to the first KiB of
 // the wave's dS slot of that step (free until the block's dS is stored
@@ -559,9 +559,12 @@ void launch_short_t(const BwdArgs& a, hipStream_t s) {
   if (slots < 1) slots = 1;
   if (slots > nseq) slots = nseq;
   const dim3 grid((unsigned)(slots * a.hpb));
+  // row-wise staging reads 16 bytes from 4-byte aligned offsets
+  const bool rows4 = reinterpret_cast<uintptr_t>(a.spd) % 4 == 0 && a.ld_spd % 4 == 0 &&
+                     a.spd_bstride % 4 == 0;
   if (a.spd_t)
     hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, true, false>), grid, dim3(kThreads), 0, s, a);
-  else if (a.spd_vec)
+  else if (rows4)
     hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, false, true>), grid, dim3(kThreads), 0, s, a);
   else
     hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, false, false>), grid, dim3(kThreads), 0, s, a);
