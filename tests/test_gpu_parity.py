@@ -422,6 +422,27 @@ def test_batch_several_graphs_per_workgroup(B, hpb, N, d, spd_kind):
     assert err <= TOL["bf16"]["grad"]
 
 
+@pytest.mark.parametrize("spd_t_kind", ["none", "transposed"])
+@pytest.mark.parametrize("nb,N,d", [(32, 200, 8), (127, 256, 32), (128, 200, 16), (200, 96, 8)])
+def test_every_byte_value_short(nb, N, d, spd_t_kind):
+    """spd bytes drawn from 0..255 on sequences of at most 256 nodes (the
+    short-sequence kernels): bytes at or past n_buckets give bias 0 and no
+    gradient, including bytes of 128 or more, which the short forward's
+    128-entry table and the fused backward's 128-bucket layout map to a
+    padding entry. N = 200 and 96 leave a partial last key block (the
+    forward masks those keys through its -inf entry)."""
+    H = 3
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=nb * 5 + N + len(spd_t_kind), dt="bf16", hi=256)
+    spd_t = np.ascontiguousarray(spd.T) if spd_t_kind == "transposed" else None
+    scale = 1.0 / math.sqrt(d)
+    tag = f"all bytes short nb={nb} N={N} d={d} spd_t={spd_t_kind}"
+    say(tag)
+    got = _run_full(q, k, v, do, table, spd, "bf16", scale, spd_t=spd_t)
+    ref = _oracle_full(q, k, v, do, table, spd, scale)
+    check_fwd(tag, got["o"], got["lse"], ref["o"], ref["lse"], "bf16")
+    check_grads(tag, got, ref, "bf16")
+
+
 def test_forward_is_deterministic():
     H, N, d, nb = 4, 777, 64, 20
     q, k, v, do, table, spd = _case(H, N, d, nb, seed=21, dt="bf16")
