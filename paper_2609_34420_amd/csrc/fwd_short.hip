@@ -188,11 +188,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
         }
         sched_fence();
         if (wact) {
+          // next block's scores, also past the last block (its K rows are the
+          // zero rows of the last copied tile or unused LDS, and the result
+          // is never read), so that the accumulator is never copied
           f32x16 sn;
-          if (kb + 1 < nkb) {
+          {
             uint32_t e[4];
             entries(wd[(kb + 1) % 3], kb + 1, e);
-            issue_scores<D, NKS>(sTab, e, lane4, sK, off.k, kb + 1, qf, sn);
+            issue_scores<D, NKS>(sTab, e, lane4, sK, off.k, (kb + 1) & 7, qf, sn);
           }
           bf16x8 vop[2][NCB];
           read_v<D>(sV, off, kb, vop);
