@@ -63,6 +63,7 @@ struct DkdvTiles {
   float init_s[2][kBQ];             // -LSE log2 e / (scale log2 e); -inf for empty rows
   float init_p[2][kBQ];             // -Dlt 2^F
   float red[3][kNW];
+  uint8_t stage[kNW][1024];         // per wave: a 32 x 32 block of spd bytes (row-wise staging)
 };
 constexpr uint32_t kTabBase = 65536;
 template <int D, int NB>
@@ -196,11 +197,15 @@ __device__ __forceinline__ void clamp_buckets(uint8_t (&b)[16]) {
 
 // b: this lane's 16 bucket indices, as 16 bytes (gathered from spd columns)
 // or as 4 words (a 16-byte row segment of spd_t).
-template <int D, int NKS, int NB, bool KTAIL, int BUF, int QS, typename BT>
+// STAGE: b holds 16 bytes of the block's spd rows (lane l: row l / 2 of the
+// 32-query sub-block, bytes 16 (l % 2) .. + 15 of the wave's 32 keys); they
+// are written to the wave's staging buffer and each lane reads its key's 16
+// query bytes back with two 8-bit transposing reads (off_tr8).
+template <int D, int NKS, int NB, bool KTAIL, int BUF, int QS, bool STAGE = false, typename BT>
 __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOffsets<D>& off,
                                               const bf16x8* kf, const bf16x8* vf,
                                               const BT* b, float sl2, bool jok,
-                                              f32x16* dk, f32x16* dv) {
+                                              f32x16* dk, f32x16* dv, const int* off_tr8 = nullptr) {
   constexpr int NKC = D / 16;
   constexpr int NCB = D / 32;
   const int lane = threadIdx.x & 63;
@@ -234,10 +239,25 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOff
   const uint32_t cpyb = (uint32_t)(lane & (CPY - 1)) * 8u | kTabBase;
   if constexpr (sizeof(BT) == 4) {
     uint32_t w[4];
+    if constexpr (STAGE) {
+      typedef int i32x2 __attribute__((ext_vector_type(2)));
+      typedef __attribute__((address_space(3))) i32x2* lds_i32x2;
+      uint8_t* st8 = sm.stage[wave_id()];
+      uint4 v4 = make_uint4(b[0], b[1], b[2], b[3]);
+      opaque(v4);                                  // keep the load's wait here
+      *reinterpret_cast<uint4*>(st8 + 16 * lane) = v4;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      w[u] = b[u];
-      opaque(w[u]);                                // keep the load's wait here
+      for (int hh = 0; hh < 2; ++hh) {
+        const i32x2 v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2)(void*)(st8 + off_tr8[hh]));
+        w[2 * hh] = (uint32_t)v.x;
+        w[2 * hh + 1] = (uint32_t)v.y;
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        w[u] = b[u];
+        opaque(w[u]);                              // keep the load's wait here
+      }
     }
     clamp_buckets<NB>(w);
 #pragma unroll
@@ -298,7 +318,7 @@ __device__ __forceinline__ void dkdv_subblock(DkdvSmem<D, NB>& sm, const DkdvOff
   }
 }
 
-template <int D, int DS, int NB, bool KTAIL, bool QFULL, bool TR>
+template <int D, int DS, int NB, bool KTAIL, bool QFULL, bool TR, bool STAGE>
 __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm, int h, int64_t key0,
                                           int64_t j, bool jok, int fexp) {
   constexpr int NKC = D / 16;
@@ -346,14 +366,32 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
   // Bucket indices of this lane's key: TR reads 16 queries as one 16-byte
   // row segment of spd_t (rows of this key block only; past the block's last
   // row a load reads zeros), else gathers 16 bytes of a spd column.
-  using BT = std::conditional_t<TR, uint32_t, uint8_t>;
-  constexpr int NBT = TR ? 4 : 16;
+  using BT = std::conditional_t<TR || STAGE, uint32_t, uint8_t>;
+  constexpr int NBT = TR || STAGE ? 4 : 16;
+  static_assert(!(TR && STAGE), "one way of reading spd");
   const __amdgpu_buffer_rsrc_t rs_t =
       make_rsrc_n(TR ? seq_spd_t(a, h) + key0 * ld : seq_spd(a, h), ((a.Sk - key0 < kBK ? a.Sk - key0 : kBK)) * ld);
   const uint32_t voff_t = (uint32_t)((jc - key0) * ld) + 16u * (uint32_t)g;
+  // STAGE: lane l loads row l / 2 of the sub-block, bytes 16 (l % 2) .. + 15
+  // of the wave's 32 keys, through a resource that starts at the sub-block's
+  // first row and ends with the last query row (rows past Sq read zero); the
+  // two transposing reads of the staged block give the lane its key's 16
+  // query bytes.
+  uint32_t voff_st = 0;
+  int off_tr8[2] = {0, 0};
+  if constexpr (STAGE) {
+    voff_st = (uint32_t)((lane >> 1) * ld) + (uint32_t)(wave_id() * 32 + 16 * (lane & 1));
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+      off_tr8[hh] = (16 * g + 8 * hh + ((lane & 15) >> 1)) * 32 + 16 * ((lane >> 4) & 1) + 8 * (lane & 1);
+  }
   auto fetch = [&](int64_t i_base, BT* dst) {
     if constexpr (TR) {
       buf_u128(rs_t, voff_t, (uint32_t)i_base, reinterpret_cast<uint32_t*>(dst));
+    } else if constexpr (STAGE) {
+      const int64_t ib = i_base < a.Sq ? i_base : a.Sq - 1;
+      const __amdgpu_buffer_rsrc_t rs = make_rsrc_n(spd_cols + ib * ld, (a.Sq - ib) * ld);
+      buf_u128(rs, voff_st + (uint32_t)((i_base - ib) * ld), 0u, reinterpret_cast<uint32_t*>(dst));
     } else {
       load_bytes<QFULL>(spd_cols, ld, i_base, a.Sq, key_off, reinterpret_cast<uint8_t*>(dst));
     }
@@ -378,10 +416,10 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
     fetch(i0 + 32, bB);
     st.load(qh, oh, lse2h, dlth, inext, a.Sq);
     sched_fence();
-    dkdv_subblock<D, (DS + 15) / 16, NB, KTAIL, BUF, 0>(sm, off, kf, vf, bA, sl2, jok, dk, dv);
+    dkdv_subblock<D, (DS + 15) / 16, NB, KTAIL, BUF, 0, STAGE>(sm, off, kf, vf, bA, sl2, jok, dk, dv, off_tr8);
     fetch(inext, bA);
     sched_fence();
-    dkdv_subblock<D, (DS + 15) / 16, NB, KTAIL, BUF, 1>(sm, off, kf, vf, bB, sl2, jok, dk, dv);
+    dkdv_subblock<D, (DS + 15) / 16, NB, KTAIL, BUF, 1, STAGE>(sm, off, kf, vf, bB, sl2, jok, dk, dv, off_tr8);
     if (more) st.template store<BUF ^ 1>(sm, inext, a.Sq, inv_sl2, sF);
     __syncthreads();
   };
@@ -436,7 +474,7 @@ __device__ __forceinline__ void dkdv_main(const BwdArgs& a, DkdvSmem<D, NB>& sm,
 
 // D: the tile's head dim (32 or 64); DS <= D: the head dim of the tensors
 // (8 and 16 run on 32-wide tiles whose extra features are zero).
-template <int D, int DS, int NB, bool QFULL, bool TR>
+template <int D, int DS, int NB, bool QFULL, bool TR, bool STAGE = false>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   constexpr int CPY = copies<NB>();
   __shared__ __attribute__((aligned(16))) DkdvSmem<D, NB> sm;
@@ -500,9 +538,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_bf16_kernel(BwdArgs a) {
   }
 
   if ((kblk + 1) * kBK <= a.Sk)
-    dkdv_main<D, DS, NB, false, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
+    dkdv_main<D, DS, NB, false, QFULL, TR, STAGE>(a, sm, h, kblk * kBK, j, jok, fexp);
   else
-    dkdv_main<D, DS, NB, true, QFULL, TR>(a, sm, h, kblk * kBK, j, jok, fexp);
+    dkdv_main<D, DS, NB, true, QFULL, TR, STAGE>(a, sm, h, kblk * kBK, j, jok, fexp);
 
   __syncthreads();
   const double unscale = ldexp(1.0, -fexp);
@@ -524,6 +562,9 @@ void launch_dkdv_t(const BwdArgs& a, hipStream_t s) {
       hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, DS, NB, true, true>), grid, dim3(kThreads), 0, s, a);
     else
       hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, DS, NB, false, true>), grid, dim3(kThreads), 0, s, a);
+  } else if (a.spd_vec) {
+    // rows 16-byte aligned: row-wise loads staged through LDS
+    hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, DS, NB, true, false, true>), grid, dim3(kThreads), 0, s, a);
   } else {
     if (qfull)
       hipLaunchKernelGGL((bwd_dkdv_bf16_kernel<D, DS, NB, true, false>), grid, dim3(kThreads), 0, s, a);
