@@ -115,7 +115,10 @@ struct ShortOffsets {
 // Block (query block qb, this wave's keys): S and dP, P and dS, the bias
 // reads and gradient adds, dV and dK, and dS (bf16) into slot xs.
 // b: the lane's 16 bucket indices (4 words of spd_t, or 16 gathered bytes).
-template <int NKS, int NB, typename BT>
+// SPROD: the statistics come with the products (features 8..10 of the Q and
+// dO rows hold -LSE / scale and -Dlt, and the lane's K and V operands ones and
+// 2^F there), so S and dP start from zero.
+template <int NKS, int NB, bool SPROD, typename BT>
 __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets& off,
                                            const bf16x8* kf, const bf16x8* vf, const BT* b,
                                            const float* is_lane, float sl2, int qb, uint16_t* xs,
@@ -125,7 +128,10 @@ __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets
   const int ib = qb * 32 + 16 * g;    // this lane half's first query
 
   f32x16 s, dp;
-  {
+  if constexpr (SPROD) {
+    s = zero_f32x16();
+    dp = zero_f32x16();
+  } else {
     const float4* is4 = reinterpret_cast<const float4*>(is_lane + qb * 32);
     const float4* ip4 = reinterpret_cast<const float4*>(&sm.init_p[ib]);
 #pragma unroll
@@ -211,7 +217,12 @@ __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets
 // the wave's dS slot of that step (free until the block's dS is stored
 // there), and each lane reads its key's 16 query bytes back with two 8-bit
 // transposing LDS reads, instead of 16 byte gathers from global memory.
-template <int DS, int NB, bool TR, bool STAGE>
+// SPROD (head dim 8, N a multiple of 32): the S and dP accumulators start at
+// zero, and -LSE / scale, -Dlt enter the products through the zero-padded
+// features 8..10 (three bf16 terms each, exact to about 2^-24) of the staged
+// Q and dO rows against ones and 2^F in the lane's K and V operands, instead
+// of eight LDS reads of statistics per block.
+template <int DS, int NB, bool TR, bool STAGE, bool SPROD = false>
 __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) {
   constexpr int NKS = (DS + 15) / 16;   // 16-feature chunks of S and dP that hold data
   constexpr int CPS = DS / 8;           // 16-byte chunks per source row
@@ -257,6 +268,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   using BT = std::conditional_t<TR || STAGE, uint32_t, uint8_t>;
   constexpr int NBT = TR || STAGE ? 4 : 16;
   static_assert(!(TR && STAGE), "one way of reading spd");
+  static_assert(!SPROD || DS == 8, "statistics through the padded features need DS = 8");
 
   // The loads of a sequence, issued one sequence ahead (during the last step
   // of the previous one) into registers: its Q, dO, K and O rows, item u =
@@ -429,8 +441,25 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
           // S starts at -LSE log2 e / (scale log2 e) (-inf for an empty row
           // or a row past N, so P = 0), dP at -Dlt 2^F
           const float L = lsev[i];
-          sm.init_s[row] = (L == -INFINITY) ? -INFINITY : -(L * kLog2e) * inv_sl2;
+          const float ss = (L == -INFINITY) ? -INFINITY : -(L * kLog2e) * inv_sl2;
+          sm.init_s[row] = ss;
           sm.init_p[row] = row < N ? -dltv[i] * sF : 0.0f;
+          if constexpr (SPROD) {
+            // features 8..10 of the row: the start as three bf16 terms
+            auto split3 = [](float x, uint4& c) {
+              const float h = (float)(__bf16)x;
+              const float r1 = (x == -INFINITY) ? 0.0f : x - h;
+              const float m = (float)(__bf16)r1;
+              const float l = r1 - m;
+              c = make_uint4((uint32_t)f2bf(h) | ((uint32_t)f2bf(m) << 16), (uint32_t)f2bf(l), 0u, 0u);
+            };
+            uint4 cq, co;
+            split3(ss, cq);
+            split3(row < N ? -dltv[i] : 0.0f, co);
+            const int lo1 = row * D + swz_tile<D>(row, 1) * 8;
+            *reinterpret_cast<uint4*>(sm.q + lo1) = cq;
+            *reinterpret_cast<uint4*>(sm.o + lo1) = co;
+          }
         }
       }
     }
@@ -441,6 +470,15 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
       kf[kc] = kraw[kc];
 #pragma unroll
       for (int e = 0; e < 8; ++e) vf[kc][e] = (__bf16)((float)vraw[kc][e] * sF);
+    }
+    if constexpr (SPROD) {
+      if (g == 1 && jok) {   // features 8..10 of the lane's K and V operands
+#pragma unroll
+        for (int e = 0; e < 3; ++e) {
+          kf[0][e] = (__bf16)1.0f;
+          vf[0][e] = (__bf16)sF;
+        }
+      }
     }
 
     f32x16 dk = zero_f32x16(), dv = zero_f32x16(), dq = zero_f32x16();
@@ -462,9 +500,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
             wv[2 * hh] = (uint32_t)v.x;
             wv[2 * hh + 1] = (uint32_t)v.y;
           }
-          block_dkdv<NKS, NB>(sm, off, kf, vf, wv, is_lane, sl2, qb, xs, dk, dv);
+          block_dkdv<NKS, NB, SPROD>(sm, off, kf, vf, wv, is_lane, sl2, qb, xs, dk, dv);
         } else {
-          block_dkdv<NKS, NB>(sm, off, kf, vf, b, is_lane, sl2, qb, xs, dk, dv);
+          block_dkdv<NKS, NB, SPROD>(sm, off, kf, vf, b, is_lane, sl2, qb, xs, dk, dv);
         }
       }
     };
@@ -562,6 +600,17 @@ void launch_short_t(const BwdArgs& a, hipStream_t s) {
   // row-wise staging reads 16 bytes from 4-byte aligned offsets
   const bool rows4 = reinterpret_cast<uintptr_t>(a.spd) % 4 == 0 && a.ld_spd % 4 == 0 &&
                      a.spd_bstride % 4 == 0;
+  if constexpr (DS == 8) {
+    if (a.Sq % 32 == 0) {     // no keys past N in any block
+      if (a.spd_t)
+        hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, true, false, true>), grid, dim3(kThreads), 0, s, a);
+      else if (rows4)
+        hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, false, true, true>), grid, dim3(kThreads), 0, s, a);
+      else
+        hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, false, false, true>), grid, dim3(kThreads), 0, s, a);
+      return;
+    }
+  }
   if (a.spd_t)
     hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, true, false>), grid, dim3(kThreads), 0, s, a);
   else if (rows4)
