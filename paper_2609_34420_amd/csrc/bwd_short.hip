@@ -286,32 +286,49 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     const __amdgpu_buffer_rsrc_t sd = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.d_o) + rowbase, nbytes);
     const __amdgpu_buffer_rsrc_t sk = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.k) + rowbase, nbytes);
     const __amdgpu_buffer_rsrc_t so = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.o) + rowbase, nbytes);
+    // Every load is issued (items past PER and features past the head dim
+    // read zero past the resource's end; the LSE of a row past N is replaced
+    // where it is used), so no loaded register merges with an older value
+    // and none is copied, which would wait for the load.
+    const __amdgpu_buffer_rsrc_t sl = make_rsrc_n(a.lse + (int64_t)h * N, (int64_t)N * 4);
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
       const int u = tid + i * kThreads;
-      if (u < PER) {            // wave-uniform
-        const uint32_t voff = (uint32_t)((u / CPS) * DS * 2 + (u % CPS) * 16);
-        rq[i] = buf_b128(sq, voff);
-        rd[i] = buf_b128(sd, voff);
-        rk[i] = buf_b128(sk, voff);
-        ro[i] = buf_b128(so, voff);
-        const int row = u / CPS;
-        lsev[i] = (u % CPS == 0 && row < N) ? a.lse[(int64_t)h * N + row] : -INFINITY;
-      }
+      const uint32_t voff = (uint32_t)((u / CPS) * DS * 2 + (u % CPS) * 16);   // >= nbytes past PER
+      rq[i] = buf_b128(sq, voff);
+      rd[i] = buf_b128(sd, voff);
+      rk[i] = buf_b128(sk, voff);
+      ro[i] = buf_b128(so, voff);
+      lsev[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(sl, (uint32_t)((u / CPS) * 4), 0, 0));
     }
-    const uint16_t* kh = reinterpret_cast<const uint16_t*>(a.k) + rowbase;
-    const uint16_t* vh = reinterpret_cast<const uint16_t*>(a.v) + rowbase;
+    const __amdgpu_buffer_rsrc_t sv = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.v) + rowbase, nbytes);
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) {
       const bool in = jok && kc * 16 + g * 8 < DS;
-      kraw[kc] = in ? *reinterpret_cast<const bf16x8*>(kh + (int64_t)j * DS + kc * 16 + g * 8) : zero_bf16x8();
-      vraw[kc] = in ? *reinterpret_cast<const bf16x8*>(vh + (int64_t)j * DS + kc * 16 + g * 8) : zero_bf16x8();
+      // (out of range: moved past the end by kZeroChunk, without a branch)
+      const uint32_t ko = (uint32_t)((jc * DS + kc * 16 + g * 8) * 2) + (in ? 0u : kZeroChunk);
+      kraw[kc] = __builtin_bit_cast(bf16x8, buf_b128(sk, ko));
+      vraw[kc] = __builtin_bit_cast(bf16x8, buf_b128(sv, ko));
     }
   };
   // Statistics of the loaded sequence (the prepare stage's definitions and
   // order of operations): Dlt = dO . O and |dO|^2 per row, reduced over the
   // DS/8 lanes of the row; |V|^2 per key; their maxima per wave into red.
   auto stats = [&]() {
+    // the loaded registers pass through an empty asm here, so no use of
+    // them is moved ahead of this point (in particular into the last step,
+    // where it would wait for loads meant to overlap that step)
+#pragma unroll
+    for (int i = 0; i < IPT; ++i) {
+      opaque(ro[i]);
+      opaque(rd[i]);
+    }
+#pragma unroll
+    for (int kc = 0; kc < D / 16; ++kc) {
+      uint4 x = __builtin_bit_cast(uint4, vraw[kc]);
+      opaque(x);
+      vraw[kc] = __builtin_bit_cast(bf16x8, x);
+    }
     float md = 0.0f, mv = 0.0f, ml = 0.0f;
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
@@ -440,7 +457,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
         if (chunk == 0) {
           // S starts at -LSE log2 e / (scale log2 e) (-inf for an empty row
           // or a row past N, so P = 0), dP at -Dlt 2^F
-          const float L = lsev[i];
+          const float L = row < N ? lsev[i] : -INFINITY;
           const float ss = (L == -INFINITY) ? -INFINITY : -(L * kLog2e) * inv_sl2;
           sm.init_s[row] = ss;
           sm.init_p[row] = row < N ? -dltv[i] * sF : 0.0f;

@@ -13,6 +13,118 @@ namespace {
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 
+// x as three bf16 terms hi + mid + lo (exact to about 2^-24 of |x|; -inf
+// gives hi = -inf and zero terms).
+__device__ __forceinline__ void split3(float x, __bf16& h, __bf16& m, __bf16& l) {
+  h = (__bf16)x;
+  const float r1 = (x == -INFINITY) ? 0.0f : x - (float)h;
+  m = (__bf16)r1;
+  l = (__bf16)(r1 - (float)m);
+}
+
+// c times the 8 bf16 values of v as three bf16 vectors.
+__device__ __forceinline__ void split3_scaled(const uint4& v, float c, uint4& hi, uint4& mid, uint4& lo) {
+  const bf16x8 x = __builtin_bit_cast(bf16x8, v);
+  bf16x8 h, m, l;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    __bf16 a, b, d;
+    split3((float)x[i] * c, a, b, d);
+    h[i] = a;
+    m[i] = b;
+    l[i] = d;
+  }
+  hi = __builtin_bit_cast(uint4, h);
+  mid = __builtin_bit_cast(uint4, m);
+  lo = __builtin_bit_cast(uint4, l);
+}
+
+// Head dim 8, N a multiple of 32 (XP): the score product yields the
+// exponent itself (the mask of a partial last key block would need more
+// registers than four waves per SIMD leave). The key
+// rows hold c k (c = scale log2 e) as three bf16 terms in features 0..23 and
+// ones in 24..26; the lane's query operand holds q against each of the
+// three terms and -r (r: the lane's reference, three bf16 terms) against the
+// ones; the accumulator starts from bias log2 e. So x = bias log2 e +
+// c q.k - r needs no vector work before its exp2. The value rows hold a
+// one in feature 8, so the P V product also accumulates the row sum of P.
+// The reference is kept 7 above the largest exponent seen when it is set,
+// so every P of a block is below 2 unless some exponent has risen 8 or more
+// above the row max: a bit test on the packed bf16 P finds that (or a
+// non-finite P) and takes the exact path, which moves the reference and
+// rescales the accumulators (row sum included) and the already issued
+// scores of the next block.
+constexpr float kRefHeadroom = 7.0f;
+
+// p = 2^x as bf16, four at a time (the scheduling fences keep the fp32
+// values from being held all at once beside x, which stays live for the
+// exact path).
+__device__ __forceinline__ void exp_only(const float (&x)[16], bf16x8& p0, bf16x8& p1) {
+#pragma unroll
+  for (int r = 0; r < 16; r += 4) {
+    const float e0 = exp2_fast(x[r]), e1 = exp2_fast(x[r + 1]);
+    const float e2 = exp2_fast(x[r + 2]), e3 = exp2_fast(x[r + 3]);
+    bf16x8& d = r < 8 ? p0 : p1;
+    d[r & 7] = (__bf16)e0;
+    d[(r & 7) + 1] = (__bf16)e1;
+    d[(r & 7) + 2] = (__bf16)e2;
+    d[(r & 7) + 3] = (__bf16)e3;
+    sched_fence();
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void softmax_pv_xp(const f32x16& s, f32x16& sn, const bf16x8 (&vop)[2][D / 32],
+                                              SoftmaxState& st, bf16x8& qm, f32x16 (&acc)[D / 32]) {
+  constexpr int NCB = D / 32;
+  const int g = (threadIdx.x >> 5) & 1;
+  float x[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) x[r] = s[r];
+  bf16x8 p0, p1;
+  exp_only(x, p0, p1);
+  const uint4 u0 = __builtin_bit_cast(uint4, p0), u1 = __builtin_bit_cast(uint4, p1);
+  const uint32_t any_big = (u0.x | u0.y | u0.z | u0.w | u1.x | u1.y | u1.z | u1.w) & 0x40004000u;
+  if (__any(any_big != 0u || st.m == -INFINITY)) {
+    // x holds exponents relative to the old reference (absolute while there
+    // is none, mneg = 0)
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, x[r]);
+    mx -= st.mneg;
+    const float mall = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(st.m, mall + kRefHeadroom);
+    const float alpha = (mnew == -INFINITY) ? 1.0f : exp2_fast(st.m - mnew);
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[cb][r] *= alpha;
+    const float mneg_new = (mnew == -INFINITY) ? 0.0f : -mnew;
+    const float shift = mneg_new - st.mneg;
+    st.m = mnew;
+    st.mneg = mneg_new;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      x[r] += shift;
+      sn[r] += shift;
+    }
+    if (g == 1) {
+      __bf16 h, m, l;
+      split3(mneg_new, h, m, l);
+      qm = zero_bf16x8();
+      qm[0] = h;
+      qm[1] = m;
+      qm[2] = l;
+    }
+    exp_only(x, p0, p1);
+  }
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    acc[cb] = mfma32(vop[0][cb], p0, acc[cb]);
+    acc[cb] = mfma32(vop[1][cb], p1, acc[cb]);
+  }
+}
+
 // Persistent forward for sequences of 33 to 256 rows with at most 127
 // buckets (bf16 in and out, head dims 8, 16, 32 on 32-wide tiles; spd rows
 // 4-byte aligned). Each wave owns 32 queries, so a workgroup covers a whole
@@ -40,6 +152,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
   constexpr int CPS = DS / 8;                   // 16-byte chunks per source row
   constexpr int PER = ROWS * CPS;               // chunks per tensor (a multiple of 64)
   constexpr int IPT = (PER + kThreads - 1) / kThreads;
+  constexpr bool XP = DS == 8 && !TAIL;         // exponents from the score product
+  constexpr int NKP = XP ? 2 : NKS;             // 16-feature chunks of the score product
+  // alternating score sets where registers allow (one workgroup per compute
+  // unit at d = 32); at d <= 16 the copy keeps four waves per SIMD
+  constexpr bool ALT = DS > 16;
   __shared__ __attribute__((aligned(16))) uint16_t sK[ROWS * D], sV[ROWS * D];
   __shared__ __attribute__((aligned(16))) float sTab[kShortTabEntries * 64];
 
@@ -62,20 +179,25 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
   const bool wact = w * 32 < N;
   const FwdOffsets<D> off;
 
-  // table entry (b, lane) at float 64 b + lane: bias / scale for b below
-  // n_buckets, 0 up to 127, -inf at 128; zero K, V (features past the head
-  // dim stay zero)
+  // table entry (b, lane) at float 64 b + lane: bias / scale (XP: bias
+  // log2 e) for b below n_buckets, 0 up to 127, -inf at 128; zero K, V
+  // (features past the head dim stay zero; XP: the ones of feature 24..26
+  // of K and feature 8 of V)
   {
-    const float inv_scale = 1.0f / a.scale;
+    const float tmul = XP ? kLog2e : 1.0f / a.scale;
     const float* th = a.table + (int64_t)head * a.n_buckets;
     for (int t = tid; t < kShortTabEntries * 16; t += kThreads) {
       const int bk = t >> 4;
-      const float x = bk < 128 ? (bk < a.n_buckets ? th[bk] * inv_scale : 0.0f) : -INFINITY;
+      const float x = bk < 128 ? (bk < a.n_buckets ? th[bk] * tmul : 0.0f) : -INFINITY;
       reinterpret_cast<float4*>(sTab)[t] = make_float4(x, x, x, x);
     }
+    constexpr uint32_t kOne = 0x3f80u;           // bf16 1.0
     for (int t = tid; t < ROWS * D / 8; t += kThreads) {
-      reinterpret_cast<uint4*>(sK)[t] = make_uint4(0u, 0u, 0u, 0u);
-      reinterpret_cast<uint4*>(sV)[t] = make_uint4(0u, 0u, 0u, 0u);
+      const int row = t >> 2, ch = t & 3;
+      const int lo = row * D + swz_tile<D>(row, ch) * 8;
+      const bool k1 = XP && ch == 3, v1 = XP && ch == 1;
+      *reinterpret_cast<uint4*>(sK + lo) = make_uint4(k1 ? kOne | (kOne << 16) : 0u, k1 ? kOne : 0u, 0u, 0u);
+      *reinterpret_cast<uint4*>(sV + lo) = make_uint4(v1 ? kOne : 0u, 0u, 0u, 0u);
     }
   }
 
@@ -83,7 +205,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
   // DS/8 + chunk, thread u mod 512; rows past N read zero) and this lane's
   // Q row.
   uint4 rk[IPT], rv[IPT];
-  bf16x8 qf[NKC], qn[NKC];
+  bf16x8 qf[NKC], qn[XP ? 1 : NKC];
   auto issue = [&](int s) {
     const int h = s * a.hpb + head;
     const int64_t rowbase = (int64_t)h * N * DS;
@@ -100,10 +222,15 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
       }
     }
     const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + rowbase;
+    if constexpr (XP) {
+      // the q row (the second operand is formed from it when the sequence starts)
+      qn[0] = *reinterpret_cast<const bf16x8*>(qh + (int64_t)qc * DS);
+    } else {
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc)
-      qn[kc] = (kc * 16 + g * 8 < DS) ? *reinterpret_cast<const bf16x8*>(qh + (int64_t)qc * DS + kc * 16 + g * 8)
-                                      : zero_bf16x8();
+      for (int kc = 0; kc < NKC; ++kc)
+        qn[kc] = (kc * 16 + g * 8 < DS) ? *reinterpret_cast<const bf16x8*>(qh + (int64_t)qc * DS + kc * 16 + g * 8)
+                                        : zero_bf16x8();
+    }
   };
   auto spd_rs = [&](int s) {
     const int h = s * a.hpb + head;
@@ -154,12 +281,26 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
       if (u < PER) {
         const int row = u / CPS, chunk = u % CPS;
         const int lo = row * D + swz_tile<D>(row, chunk) * 8;
-        *reinterpret_cast<uint4*>(sK + lo) = rk[i];
+        if constexpr (XP) {
+          uint4 hi, mid, low;
+          split3_scaled(rk[i], sl2, hi, mid, low);
+          *reinterpret_cast<uint4*>(sK + lo) = hi;
+          *reinterpret_cast<uint4*>(sK + row * D + swz_tile<D>(row, 1) * 8) = mid;
+          *reinterpret_cast<uint4*>(sK + row * D + swz_tile<D>(row, 2) * 8) = low;
+        } else {
+          *reinterpret_cast<uint4*>(sK + lo) = rk[i];
+        }
         *reinterpret_cast<uint4*>(sV + lo) = rv[i];
       }
     }
+    if constexpr (XP) {
+      // q against the three key terms; zero against the ones (no reference yet)
+      qf[0] = qn[0];
+      qf[1] = g == 0 ? qn[0] : zero_bf16x8();
+    } else {
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc) qf[kc] = qn[kc];
+      for (int kc = 0; kc < NKC; ++kc) qf[kc] = qn[kc];
+    }
     __syncthreads();            // K, V of this sequence visible
     issue(nxt);
     sched_fence();
@@ -168,39 +309,64 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
     st.l = 0.0f;
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) acc[cb] = zero_f32x16();
-    f32x16 sc;
-    if (wact) {
-      uint32_t e[4];
-      entries(wd[0], 0, e);
-      issue_scores<D, NKS>(sTab, e, lane4, sK, off.k, 0, qf, sc);
-    }
-#pragma unroll
-    for (int kb = 0; kb < ROWS / 32; ++kb) {
-      if (kb < nkb) {
-        // words of block kb + 2 (of the next sequence past the end)
+    // Key block kb: the words of block kb + 2 are fetched (of the next
+    // sequence past the end: one load whatever the source, so the wait for
+    // block kb + 1's words leaves it in flight), block kb + 1's scores go
+    // into sn (also past the last block: its K rows are the zero rows of
+    // the last copied tile or unused LDS, and the result is never read),
+    // and block kb's scores sc are softmaxed into acc.
+    auto block = [&](int kb, f32x16& sc, f32x16& sn) {
+      {
+        const int kf = kb + 2;
+        const bool here = kf < nkb;
+        const __amdgpu_buffer_rsrc_t src = here ? rs : rn;
+        buf_u128(src, voff, (uint32_t)((here ? kf : kf - nkb) * 32), wd[(kb + 2) % 3]);
+      }
+      sched_fence();
+      if (wact) {
         {
-          const int kf = kb + 2;
-          uint32_t* dst = wd[(kb + 2) % 3];
-          if (kf < nkb)
-            buf_u128(rs, voff, (uint32_t)(kf * 32), dst);
-          else
-            buf_u128(rn, voff, (uint32_t)((kf - nkb) * 32), dst);
+          uint32_t e[4];
+          entries(wd[(kb + 1) % 3], kb + 1, e);
+          issue_scores<D, NKP>(sTab, e, lane4, sK, off.k, (kb + 1) & 7, qf, sn);
         }
-        sched_fence();
-        if (wact) {
-          // next block's scores, also past the last block (its K rows are the
-          // zero rows of the last copied tile or unused LDS, and the result
-          // is never read), so that the accumulator is never copied
-          f32x16 sn;
-          {
-            uint32_t e[4];
-            entries(wd[(kb + 1) % 3], kb + 1, e);
-            issue_scores<D, NKS>(sTab, e, lane4, sK, off.k, (kb + 1) & 7, qf, sn);
-          }
-          bf16x8 vop[2][NCB];
-          read_v<D>(sV, off, kb, vop);
+        bf16x8 vop[2][NCB];
+        read_v<D>(sV, off, kb, vop);
+        if constexpr (XP)
+          softmax_pv_xp<D>(sc, sn, vop, st, qf[1], acc);
+        else
           softmax_pv<D, false>(sc, vop, 32, sl2, st, acc);
-          sc = sn;
+        if constexpr (!ALT) sc = sn;
+      }
+    };
+    if constexpr (ALT) {
+      // the score sets of the even and odd blocks alternate, so neither is
+      // copied (the break keeps a softmaxed set from being live afterwards)
+      f32x16 sa, sb;
+      if (wact) {
+        uint32_t e[4];
+        entries(wd[0], 0, e);
+        issue_scores<D, NKP>(sTab, e, lane4, sK, off.k, 0, qf, sa);
+      }
+#pragma unroll
+      for (int kb = 0; kb < ROWS / 32; ++kb) {
+        if (kb >= nkb) break;
+        if (kb & 1)
+          block(kb, sb, sa);
+        else
+          block(kb, sa, sb);
+      }
+    } else {
+      f32x16 sc;
+      if (wact) {
+        uint32_t e[4];
+        entries(wd[0], 0, e);
+        issue_scores<D, NKP>(sTab, e, lane4, sK, off.k, 0, qf, sc);
+      }
+#pragma unroll
+      for (int kb = 0; kb < ROWS / 32; ++kb) {
+        if (kb < nkb) {
+          f32x16 sn;
+          block(kb, sc, sn);
         }
       }
     }
@@ -214,7 +380,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
     }
     // epilogue: O = O_acc / l, LSE = (m + log2 l) ln 2
     if (wact) {
-      const float lt = st.l + __shfl_xor(st.l, 32);
+      // XP: the row sum is O^T row 8, register 4 of the lane half g = 0
+      const float lt = XP ? __shfl(acc[0][4], col) : st.l + __shfl_xor(st.l, 32);
       if (qi < N) {
         const int h = s * a.hpb + head;
         const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;

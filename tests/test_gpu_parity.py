@@ -88,20 +88,22 @@ def test_ragged_sizes(N, d, dt):
             assert np.abs(got[name]).max() <= 1e-6, name
 
 
-@pytest.mark.parametrize("d", [8, 32, 64])
-def test_large_and_rising_scores(d):
+@pytest.mark.parametrize("d,N", [(8, 600), (32, 600), (64, 600), (8, 256), (16, 256), (8, 200), (32, 200)])
+def test_large_and_rising_scores(d, N):
     """Score ranges far past the forward's block-sum limit, bf16. Head 0:
     large Q, K and table entries (scores spread over tens of units, so the
     softmax is nearly one-hot). Head 1: every query's scores rise along the
     keys (q_i . k_j grows with j, up to about 170), so each new key block
     moves the row max and the exact rescaling path runs on every block.
+    N = 256 and 200 run the short-sequence kernels (whole-sequence forward,
+    fused backward), N = 600 the full-width ones.
     (The fp32 bars are absolute and sized for scores of order one.) The
     backward is checked as a function of its inputs, to the relative bar
     except head 1's dQ on the matrix cores (see below)."""
     dt = "bf16"
-    H, N, nb = 2, 600, 12
-    q, k, v, do, table, spd = _case(H, N, d, nb, seed=40 + d, dt=dt, table_std=4.0, qkv_std=1.5)
-    g = np.random.default_rng(41 + d)
+    H, nb = 2, 12
+    q, k, v, do, table, spd = _case(H, N, d, nb, seed=40 + d + (N % 600), dt=dt, table_std=4.0, qkv_std=1.5)
+    g = np.random.default_rng(41 + d + (N % 600))
     u = np.abs(g.standard_normal(d)) + 0.1
     u /= np.linalg.norm(u)
     span = 40.0 * math.sqrt(d)                     # scores up to span * scale * max|q|
@@ -111,7 +113,7 @@ def test_large_and_rising_scores(d):
     v *= 0.25                                      # exact in bf16
     q, k = synth.round_bf16(q.astype(np.float32)), synth.round_bf16(k.astype(np.float32))
     scale = 1.0 / math.sqrt(d)
-    say(f"large scores {dt} d={d}")
+    say(f"large scores {dt} d={d} N={N}")
     td = tdtype(dt)
     Q, K, V, dO = (to_dev(x, td) for x in (q, k, v, do))
     T, S = to_dev(table), to_dev(spd, torch.uint8)
