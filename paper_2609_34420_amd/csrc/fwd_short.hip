@@ -12,6 +12,7 @@ namespace {
 
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 // x as three bf16 terms hi + mid + lo (exact to about 2^-24 of |x|; -inf
 // gives hi = -inf and zero terms).
@@ -125,6 +126,43 @@ __device__ __forceinline__ void softmax_pv_xp(const f32x16& s, f32x16& sn, const
   }
 }
 
+// XP, the first key block of a sequence (no reference yet, acc = 0): the
+// reference is set from the block's maxima before the one exp2, and the
+// next block's scores, issued without a reference, are moved to it.
+template <int D>
+__device__ __forceinline__ void softmax_first_xp(const f32x16& s, f32x16& sn, const bf16x8 (&vop)[2][D / 32],
+                                                 SoftmaxState& st, bf16x8& qm, f32x16 (&acc)[D / 32]) {
+  constexpr int NCB = D / 32;
+  const int g = (threadIdx.x >> 5) & 1;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
+  const float mall = fmaxf(mx, __shfl_xor(mx, 32));
+  st.m = mall + kRefHeadroom;                       // -inf stays -inf
+  st.mneg = (st.m == -INFINITY) ? 0.0f : -st.m;
+  float x[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    x[r] = s[r] + st.mneg;
+    sn[r] += st.mneg;
+  }
+  if (g == 1) {
+    __bf16 h, m, l;
+    split3(st.mneg, h, m, l);
+    qm = zero_bf16x8();
+    qm[0] = h;
+    qm[1] = m;
+    qm[2] = l;
+  }
+  bf16x8 p0, p1;
+  exp_only(x, p0, p1);
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    acc[cb] = mfma32(vop[0][cb], p0, acc[cb]);
+    acc[cb] = mfma32(vop[1][cb], p1, acc[cb]);
+  }
+}
+
 // Persistent forward for sequences of 33 to 256 rows with at most 127
 // buckets (bf16 in and out, head dims 8, 16, 32 on 32-wide tiles; spd rows
 // 4-byte aligned). Each wave owns 32 queries, so a workgroup covers a whole
@@ -143,7 +181,7 @@ __device__ __forceinline__ void softmax_pv_xp(const f32x16& s, f32x16& sn, const
 // block kb. TAIL: N is not a multiple of 32.
 constexpr int kShortTabEntries = 129;
 template <int DS, bool TAIL>
-__global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) {
+__global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_kernel(FwdArgs a) {
   constexpr int D = 32;
   constexpr int NKC = D / 16;
   constexpr int NKS = (DS + 15) / 16;
@@ -154,9 +192,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
   constexpr int IPT = (PER + kThreads - 1) / kThreads;
   constexpr bool XP = DS == 8 && !TAIL;         // exponents from the score product
   constexpr int NKP = XP ? 2 : NKS;             // 16-feature chunks of the score product
-  // alternating score sets where registers allow (one workgroup per compute
-  // unit at d = 32); at d <= 16 the copy keeps four waves per SIMD
-  constexpr bool ALT = DS > 16;
+  // alternating score sets where registers allow: at d = 32 (one workgroup
+  // per compute unit) and at d = 8 without a partial key block; elsewhere
+  // the copy keeps four waves per SIMD without spilling
+  constexpr bool ALT = DS == 32 || XP;
   __shared__ __attribute__((aligned(16))) uint16_t sK[ROWS * D], sV[ROWS * D];
   __shared__ __attribute__((aligned(16))) float sTab[kShortTabEntries * 64];
 
@@ -331,9 +370,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
         }
         bf16x8 vop[2][NCB];
         read_v<D>(sV, off, kb, vop);
-        if constexpr (XP)
-          softmax_pv_xp<D>(sc, sn, vop, st, qf[1], acc);
-        else
+        if constexpr (XP) {
+          if (kb == 0)
+            softmax_first_xp<D>(sc, sn, vop, st, qf[1], acc);
+          else
+            softmax_pv_xp<D>(sc, sn, vop, st, qf[1], acc);
+        } else
           softmax_pv<D, false>(sc, vop, 32, sl2, st, acc);
         if constexpr (!ALT) sc = sn;
       }
@@ -383,20 +425,26 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_short_bf16_kernel(FwdArgs a) 
       // XP: the row sum is O^T row 8, register 4 of the lane half g = 0
       const float lt = XP ? __shfl(acc[0][4], col) : st.l + __shfl_xor(st.l, 32);
       if (qi < N) {
+        // stores through resources over this head's rows (scalar bases,
+        // 32-bit lane offsets: no 64-bit address is kept across sequences)
         const int h = s * a.hpb + head;
         const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
         const float lse_out = lt > 0.0f ? (st.m + __log2f(lt)) * kLn2 : -INFINITY;
-        uint16_t* op = reinterpret_cast<uint16_t*>(a.o) + ((int64_t)h * N + qi) * DS;
+        const __amdgpu_buffer_rsrc_t ro =
+            make_rsrc_n(reinterpret_cast<uint16_t*>(a.o) + (int64_t)h * N * DS, (int64_t)N * DS * 2);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int c = 8 * u + 4 * g;
           if (c >= DS) continue;
-          uint2 pk;
-          pk.x = (uint32_t)f2bf(acc[0][4 * u] * inv) | ((uint32_t)f2bf(acc[0][4 * u + 1] * inv) << 16);
-          pk.y = (uint32_t)f2bf(acc[0][4 * u + 2] * inv) | ((uint32_t)f2bf(acc[0][4 * u + 3] * inv) << 16);
-          *reinterpret_cast<uint2*>(op + c) = pk;
+          u32x2 pk;
+          pk[0] = (uint32_t)f2bf(acc[0][4 * u] * inv) | ((uint32_t)f2bf(acc[0][4 * u + 1] * inv) << 16);
+          pk[1] = (uint32_t)f2bf(acc[0][4 * u + 2] * inv) | ((uint32_t)f2bf(acc[0][4 * u + 3] * inv) << 16);
+          __builtin_amdgcn_raw_buffer_store_b64(pk, ro, (uint32_t)((qi * DS + c) * 2), 0, 0);
         }
-        if (g == 0) a.lse[(int64_t)h * N + qi] = lse_out;
+        if (g == 0) {
+          const __amdgpu_buffer_rsrc_t rl = make_rsrc_n(a.lse + (int64_t)h * N, (int64_t)N * 4);
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(lse_out), rl, (uint32_t)(qi * 4), 0, 0);
+        }
       }
     }
   };
