@@ -196,7 +196,11 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
   // per compute unit) and at d = 8 without a partial key block; elsewhere
   // the copy keeps four waves per SIMD without spilling
   constexpr bool ALT = DS == 32 || XP;
-  __shared__ __attribute__((aligned(16))) uint16_t sK[ROWS * D], sV[ROWS * D];
+  // K has 192 rows of padding: block (kb + 1) mod 8 of the last slice, read
+  // past the last block of a sequence (its product is never used), stays in
+  // the array at any slice size
+  constexpr int KROWS = ROWS + 192;
+  __shared__ __attribute__((aligned(16))) uint16_t sK[KROWS * D], sV[ROWS * D];
   __shared__ __attribute__((aligned(16))) float sTab[kShortTabEntries * 64];
 
   const int tid = threadIdx.x;
@@ -205,17 +209,26 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
   const uint32_t lane4 = (uint32_t)lane * 4u;
   const int N = (int)a.Sq;
   const int nkb = (N + 31) / 32;                // at least 2
+  // P sequences of the head at once (N <= 128: 2, N <= 64: 4): sequence slot
+  // p = w / GW of a group holds LDS rows p R .. p R + R - 1 and its waves
+  // take query blocks wl = w mod GW.
+  const int lgp = N > 128 ? 0 : (N > 64 ? 1 : 2);
+  const int P = 1 << lgp, GW = kWaves >> lgp, R = ROWS >> lgp;
+  const int p = w >> (3 - lgp), wl = w & (GW - 1);
   const int G = (int)gridDim.x;
   const int lw = (int)xcd_remap(blockIdx.x, G);
   const int head = lw % a.hpb;
   const int slot = lw / a.hpb;
   const int nslots = G / a.hpb;
   const int nseq = a.H / a.hpb;
+  const int ngroups = (nseq + P - 1) >> lgp;
   const float sl2 = a.scale * kLog2e;
   const int ld = (int)a.ld_spd;
-  const int qi = w * 32 + col;                  // this lane's query
+  const int qi = wl * 32 + col;                 // this lane's query (in its sequence)
   const int qc = qi < N ? qi : N - 1;
-  const bool wact = w * 32 < N;
+  const bool wrows = wl * 32 < N;               // the wave owns query rows
+  const uint16_t* sKp = sK + p * R * D;         // this wave's slice of K and V
+  const uint16_t* sVp = sV + p * R * D;
   const FwdOffsets<D> off;
 
   // table entry (b, lane) at float 64 b + lane: bias / scale (XP: bias
@@ -231,36 +244,45 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
       reinterpret_cast<float4*>(sTab)[t] = make_float4(x, x, x, x);
     }
     constexpr uint32_t kOne = 0x3f80u;           // bf16 1.0
-    for (int t = tid; t < ROWS * D / 8; t += kThreads) {
+    for (int t = tid; t < KROWS * D / 8; t += kThreads) {
       const int row = t >> 2, ch = t & 3;
       const int lo = row * D + swz_tile<D>(row, ch) * 8;
       const bool k1 = XP && ch == 3, v1 = XP && ch == 1;
       *reinterpret_cast<uint4*>(sK + lo) = make_uint4(k1 ? kOne | (kOne << 16) : 0u, k1 ? kOne : 0u, 0u, 0u);
-      *reinterpret_cast<uint4*>(sV + lo) = make_uint4(v1 ? kOne : 0u, 0u, 0u, 0u);
+      if (row < ROWS) *reinterpret_cast<uint4*>(sV + lo) = make_uint4(v1 ? kOne : 0u, 0u, 0u, 0u);
     }
   }
 
-  // Loads of sequence s into registers: its K and V rows (item u = row *
-  // DS/8 + chunk, thread u mod 512; rows past N read zero) and this lane's
+  // The wave's sequence in group gi (clamped to the batch for loads).
+  auto seq_of = [&](int gi) { return (gi << lgp) + p; };
+  auto clamp_seq = [&](int s) { return s < nseq ? s : nseq - 1; };
+  // Loads of group gi into registers: its K and V rows (item u = row *
+  // DS/8 + chunk, thread u mod 512; row r is row r mod R of the group's
+  // sequence r / R; rows past N or past the batch read zero) and this lane's
   // Q row.
   uint4 rk[IPT], rv[IPT];
   bf16x8 qf[NKC], qn[XP ? 1 : NKC];
-  auto issue = [&](int s) {
-    const int h = s * a.hpb + head;
-    const int64_t rowbase = (int64_t)h * N * DS;
-    const int64_t nbytes = (int64_t)N * DS * 2;
-    const __amdgpu_buffer_rsrc_t sk = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.k) + rowbase, nbytes);
-    const __amdgpu_buffer_rsrc_t sv = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.v) + rowbase, nbytes);
+  auto issue = [&](int gi) {
+    // resources from the group's first sequence (this head) to the end of
+    // the tensors; the P sequences' rows are hpb N DS elements apart
+    const int64_t base = ((int64_t)(gi << lgp) * a.hpb + head) * N * DS;
+    const int64_t left = ((int64_t)a.H * N * DS - base) * 2;
+    const int64_t nbytes = left < (int64_t)kZeroChunk ? left : (int64_t)kZeroChunk;
+    const __amdgpu_buffer_rsrc_t sk = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.k) + base, nbytes);
+    const __amdgpu_buffer_rsrc_t sv = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.v) + base, nbytes);
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
       const int u = tid + i * kThreads;
       if (u < PER) {
-        const uint32_t vo = (uint32_t)((u / CPS) * DS * 2 + (u % CPS) * 16);
+        const int r = u / CPS, pr = r / R, lr = r - pr * R;
+        const bool ok = lr < N && (gi << lgp) + pr < nseq;
+        const uint32_t vo = ok ? (uint32_t)(((pr * a.hpb) * N + lr) * DS * 2 + (u % CPS) * 16) : kZeroChunk;
         rk[i] = buf_b128(sk, vo);
         rv[i] = buf_b128(sv, vo);
       }
     }
-    const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + rowbase;
+    const int h = clamp_seq(seq_of(gi)) * a.hpb + head;
+    const uint16_t* qh = reinterpret_cast<const uint16_t*>(a.q) + (int64_t)h * N * DS;
     if constexpr (XP) {
       // the q row (the second operand is formed from it when the sequence starts)
       qn[0] = *reinterpret_cast<const bf16x8*>(qh + (int64_t)qc * DS);
@@ -305,14 +327,17 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
   f32x16 acc[NCB];
   uint32_t wd[3][4];                              // spd words of key blocks kb, kb + 1, kb + 2
 
-  // One sequence: its K, V, Q are in registers on entry (loaded during the
-  // previous one), and wd[0], wd[1] hold its first spd words. The spd words
-  // stream over (sequence, key block) two blocks ahead: past the last block
-  // come blocks 0 and 1 of the next sequence.
-  auto run = [&](int s) {
-    const int nxt = s + nslots < nseq ? s + nslots : s;
-    const __amdgpu_buffer_rsrc_t rs = spd_rs(s);
-    const __amdgpu_buffer_rsrc_t rn = spd_rs(nxt);
+  // One group: its K, V, Q are in registers on entry (loaded during the
+  // previous one), and wd[0], wd[1] hold the first spd words of the wave's
+  // sequence. The spd words stream over (group, key block) two blocks ahead:
+  // past the last block come blocks 0 and 1 of the wave's sequence in the
+  // next group.
+  auto run = [&](int gi) {
+    const int s = seq_of(gi);
+    const bool wact = wrows && s < nseq;
+    const int gnx = gi + nslots < ngroups ? gi + nslots : gi;
+    const __amdgpu_buffer_rsrc_t rs = spd_rs(clamp_seq(s));
+    const __amdgpu_buffer_rsrc_t rn = spd_rs(clamp_seq(seq_of(gnx)));
     __syncthreads();            // the previous sequence's reads of K and V are done
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
@@ -340,8 +365,8 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
 #pragma unroll
       for (int kc = 0; kc < NKC; ++kc) qf[kc] = qn[kc];
     }
-    __syncthreads();            // K, V of this sequence visible
-    issue(nxt);
+    __syncthreads();            // K, V of this group visible
+    issue(gnx);
     sched_fence();
     st.m = -INFINITY;
     st.mneg = 0.0f;
@@ -351,8 +376,8 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
     // Key block kb: the words of block kb + 2 are fetched (of the next
     // sequence past the end: one load whatever the source, so the wait for
     // block kb + 1's words leaves it in flight), block kb + 1's scores go
-    // into sn (also past the last block: its K rows are the zero rows of
-    // the last copied tile or unused LDS, and the result is never read),
+    // into sn (also past the last block: rows of the slice, of the next
+    // slice or of the padding, and the result is never read),
     // and block kb's scores sc are softmaxed into acc.
     auto block = [&](int kb, f32x16& sc, f32x16& sn) {
       {
@@ -366,10 +391,10 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
         {
           uint32_t e[4];
           entries(wd[(kb + 1) % 3], kb + 1, e);
-          issue_scores<D, NKP>(sTab, e, lane4, sK, off.k, (kb + 1) & 7, qf, sn);
+          issue_scores<D, NKP>(sTab, e, lane4, sKp, off.k, (kb + 1) & 7, qf, sn);
         }
         bf16x8 vop[2][NCB];
-        read_v<D>(sV, off, kb, vop);
+        read_v<D>(sVp, off, kb, vop);
         if constexpr (XP) {
           if (kb == 0)
             softmax_first_xp<D>(sc, sn, vop, st, qf[1], acc);
@@ -387,7 +412,7 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
       if (wact) {
         uint32_t e[4];
         entries(wd[0], 0, e);
-        issue_scores<D, NKP>(sTab, e, lane4, sK, off.k, 0, qf, sa);
+        issue_scores<D, NKP>(sTab, e, lane4, sKp, off.k, 0, qf, sa);
       }
 #pragma unroll
       for (int kb = 0; kb < ROWS / 32; ++kb) {
@@ -402,7 +427,7 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
       if (wact) {
         uint32_t e[4];
         entries(wd[0], 0, e);
-        issue_scores<D, NKP>(sTab, e, lane4, sK, off.k, 0, qf, sc);
+        issue_scores<D, NKP>(sTab, e, lane4, sKp, off.k, 0, qf, sc);
       }
 #pragma unroll
       for (int kb = 0; kb < ROWS / 32; ++kb) {
@@ -427,7 +452,7 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
       if (qi < N) {
         // stores through resources over this head's rows (scalar bases,
         // 32-bit lane offsets: no 64-bit address is kept across sequences)
-        const int h = s * a.hpb + head;
+        const int h = s * a.hpb + head;   // s < nseq here
         const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
         const float lse_out = lt > 0.0f ? (st.m + __log2f(lt)) * kLn2 : -INFINITY;
         const __amdgpu_buffer_rsrc_t ro =
@@ -451,21 +476,23 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
 
   issue(slot);
   {
-    const __amdgpu_buffer_rsrc_t rs = spd_rs(slot);
+    const __amdgpu_buffer_rsrc_t rs = spd_rs(clamp_seq(seq_of(slot)));
     buf_u128(rs, voff, 0u, wd[0]);
     buf_u128(rs, voff, 32u, wd[1]);
   }
-  for (int s = slot; s < nseq; s += nslots) run(s);
+  for (int gi = slot; gi < ngroups; gi += nslots) run(gi);
   wait_vmcnt<0>();     // drain the loads issued for the last (repeated) sequence
 }
 
 template <int DS>
 void launch_short_t(const FwdArgs& a, hipStream_t s) {
   const int nseq = a.H / a.hpb;
+  const int lgp = a.Sq > 128 ? 0 : (a.Sq > 64 ? 1 : 2);          // sequences per workgroup: 2^lgp
+  const int ngroups = (nseq + (1 << lgp) - 1) >> lgp;
   // two workgroups per compute unit where the registers allow four waves per SIMD
   int slots = (DS <= 16 ? 512 : 256) / a.hpb;
   if (slots < 1) slots = 1;
-  if (slots > nseq) slots = nseq;
+  if (slots > ngroups) slots = ngroups;
   const dim3 grid((unsigned)(slots * a.hpb));
   if (a.Sq % 32 != 0)
     hipLaunchKernelGGL((fwd_short_bf16_kernel<DS, true>), grid, dim3(kThreads), 0, s, a);
@@ -476,8 +503,11 @@ void launch_short_t(const FwdArgs& a, hipStream_t s) {
 }  // namespace
 
 bool fwd_short_applies(const FwdArgs& a, int d) {
+  // (a group of up to 4 sequences is read through one resource of at most
+  // 2^30 bytes)
   return d <= 32 && !a.accumulate && a.row_off == 0 && a.col_off == 0 && a.Sq == a.Sk &&
          a.Sq > 32 && a.Sq <= 256 && a.n_buckets <= 127 && a.hpb >= 1 && a.H % a.hpb == 0 &&
+         (int64_t)4 * a.hpb * a.Sq * d * 2 < ((int64_t)1 << 30) &&
          reinterpret_cast<uintptr_t>(a.spd) % 4 == 0 && a.ld_spd % 4 == 0 && a.spd_bstride % 4 == 0;
 }
 

@@ -377,15 +377,20 @@ def test_batch_of_graphs(B, N, d, spd_kind, dt):
     (12, 64, 80, 8, "per_graph"),       # 4 workgroup slots: 3 sequences per workgroup
     (12, 64, 256, 32, "per_graph_t"),
     (64, 8, 33, 16, "shared"),          # 32 slots: 2 sequences per workgroup
+    (21, 64, 128, 8, "per_graph"),      # forward: pairs of sequences, 11 pairs on 8 slots
+    (19, 128, 50, 16, "shared"),        # forward: 4 sequences at once, last group of 3
+    (9, 128, 64, 32, "per_graph_t"),    # forward: 4 at once at d = 32, 3 groups on 2 slots
+    (7, 64, 100, 16, "per_graph"),      # forward: pairs with a partial last key block
 ])
 def test_batch_several_graphs_per_workgroup(B, hpb, N, d, spd_kind):
     """Sequences of at most 256 nodes with more sequences than the fused
     backward has workgroup slots, so each workgroup takes several sequences
-    of one head in turn. V and dO double every third of the batch, so a
-    workgroup's later sequences have larger gradient bounds: the fixed-point
-    exponent of its histogram drops and the sums accumulated so far are
-    rescaled. Every graph's O, LSE, dQ, dK, dV and the summed dtable equal
-    the oracle."""
+    of one head in turn (the forward takes 2 or 4 sequences at once at
+    N <= 128 or 64, and several such groups in turn). V and dO double every
+    third of the batch, so a workgroup's later sequences have larger
+    gradient bounds: the fixed-point exponent of its histogram drops and
+    the sums accumulated so far are rescaled. Every graph's O, LSE, dQ, dK,
+    dV and the summed dtable equal the oracle."""
     nb = 12
     g = np.random.default_rng(B * N + d + hpb)
     shape = (B, hpb, N, d)
