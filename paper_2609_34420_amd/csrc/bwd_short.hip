@@ -118,21 +118,23 @@ struct ShortOffsets {
 // SPROD: the statistics come with the products (features 8..10 of the Q and
 // dO rows hold -LSE / scale and -Dlt, and the lane's K and V operands ones and
 // 2^F there), so S and dP start from zero.
+// rb: first LDS row of the wave's sequence (its slice when several
+// sequences share the workgroup).
 template <int NKS, int NB, bool SPROD, typename BT>
 __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets& off,
                                            const bf16x8* kf, const bf16x8* vf, const BT* b,
-                                           const float* is_lane, float sl2, int qb, uint16_t* xs,
+                                           const float* is_lane, float sl2, int rb, int qb, uint16_t* xs,
                                            f32x16& dk, f32x16& dv) {
   const int lane = threadIdx.x & 63;
   const int g = lane >> 5;
-  const int ib = qb * 32 + 16 * g;    // this lane half's first query
+  const int ib = rb + qb * 32 + 16 * g;   // this lane half's first query (LDS row)
 
   f32x16 s, dp;
   if constexpr (SPROD) {
     s = zero_f32x16();
     dp = zero_f32x16();
   } else {
-    const float4* is4 = reinterpret_cast<const float4*>(is_lane + qb * 32);
+    const float4* is4 = reinterpret_cast<const float4*>(is_lane + rb + qb * 32);
     const float4* ip4 = reinterpret_cast<const float4*>(&sm.init_p[ib]);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -143,8 +145,8 @@ __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets
   }
 #pragma unroll
   for (int kc = 0; kc < NKS; ++kc) {
-    s = mfma32(lds_b128(sm.q + qb * 32 * D + off.row[kc]), kf[kc], s);
-    dp = mfma32(lds_b128(sm.o + qb * 32 * D + off.row[kc]), vf[kc], dp);
+    s = mfma32(lds_b128(sm.q + (rb + qb * 32) * D + off.row[kc]), kf[kc], s);
+    dp = mfma32(lds_b128(sm.o + (rb + qb * 32) * D + off.row[kc]), vf[kc], dp);
   }
   float p[16], ds[16];
   uint32_t addr[16];   // LDS byte offset of table entry (bucket, copy) from sm
@@ -203,7 +205,7 @@ __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets
   for (int q = 0; q < 2; ++q) {
     const bf16x8 pb = cvt_bf16x8(p + 8 * q);
     const bf16x8 db = cvt_bf16x8(ds + 8 * q);
-    const int base = (qb * 32 + 8 * q) * D;
+    const int base = (rb + qb * 32 + 8 * q) * D;
     dv = mfma32(lds_tr_operand(sm.o + base, off.tr[0], off.tr[1]), pb, dv);
     dk = mfma32(lds_tr_operand(sm.q + base, off.tr[0], off.tr[1]), db, dk);
     // queries 16 g + 8 q .. + 7 of this key: chunk 2 g + q of slot row `key`
@@ -236,6 +238,13 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   const int w = wave_id();
   const int N = (int)a.Sq;
   const int nb = (N + 31) / 32;
+  // P sequences of the head at once (N <= 128: 2, N <= 64: 4): sequence
+  // slot p = w / GW of a group holds LDS rows p R .. p R + R - 1, and its GW
+  // waves run the diagonal schedule over GW blocks (wl = w mod GW).
+  const int lgp = N > 128 ? 0 : (N > 64 ? 1 : 2);
+  const int P = 1 << lgp, GW = kNW >> lgp, R = kRows >> lgp;
+  const int p = w >> (3 - lgp), wl = w & (GW - 1);
+  const int rb = p * R;
 
   const int G = (int)gridDim.x;
   const int lw = (int)xcd_remap(blockIdx.x, G);
@@ -243,6 +252,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   const int slot = lw / a.hpb;
   const int nslots = G / a.hpb;
   const int nseq = a.H / a.hpb;
+  const int ngroups = (nseq + P - 1) >> lgp;
+  auto seq_of = [&](int gi) { return (gi << lgp) + p; };
+  auto clamp_seq = [&](int s) { return s < nseq ? s : nseq - 1; };
 
   // Table (times log2 e) and histogram of this workgroup's head; zero tiles
   // (features past the head dim and rows past N stay zero); -inf starts.
@@ -259,7 +271,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   const float sl2 = a.scale * kLog2e;
   const float inv_sl2 = 1.0f / sl2;
   const int key = lane & 31;
-  const int j = w * 32 + key;           // this lane's key
+  const int j = wl * 32 + key;          // this lane's key (in its sequence)
   const bool jok = j < N;
   const int jc = jok ? j : N - 1;
   const float* is_lane = (jok ? sm.init_s : sm.ninf) + 16 * g;
@@ -278,36 +290,50 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   uint4 rq[IPT], rd[IPT], rk[IPT], ro[IPT];
   float lsev[IPT], dltv[IPT];
   bf16x8 kraw[D / 16], vraw[D / 16];
-  auto issue = [&](int s) {
-    const int h = s * a.hpb + head;
-    const int64_t rowbase = (int64_t)h * N * DS;
-    const int64_t nbytes = (int64_t)N * DS * 2;
-    const __amdgpu_buffer_rsrc_t sq = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.q) + rowbase, nbytes);
-    const __amdgpu_buffer_rsrc_t sd = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.d_o) + rowbase, nbytes);
-    const __amdgpu_buffer_rsrc_t sk = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.k) + rowbase, nbytes);
-    const __amdgpu_buffer_rsrc_t so = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.o) + rowbase, nbytes);
+  auto issue = [&](int gi) {
+    // rows of the group through resources from its first sequence (this
+    // head) to the end of the tensors (at most 2^30 bytes); the P sequences'
+    // rows are hpb N DS elements apart, row r of the group is row r mod R of
+    // its sequence r / R
+    const int64_t base = ((int64_t)(gi << lgp) * a.hpb + head) * N * DS;
+    const int64_t left = ((int64_t)a.H * N * DS - base) * 2;
+    const int64_t nbytes = left < (int64_t)kZeroChunk ? left : (int64_t)kZeroChunk;
+    const __amdgpu_buffer_rsrc_t sq = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.q) + base, nbytes);
+    const __amdgpu_buffer_rsrc_t sd = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.d_o) + base, nbytes);
+    const __amdgpu_buffer_rsrc_t sk = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.k) + base, nbytes);
+    const __amdgpu_buffer_rsrc_t so = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.o) + base, nbytes);
     // Every load is issued (items past PER and features past the head dim
     // read zero past the resource's end; the LSE of a row past N is replaced
     // where it is used), so no loaded register merges with an older value
     // and none is copied, which would wait for the load.
-    const __amdgpu_buffer_rsrc_t sl = make_rsrc_n(a.lse + (int64_t)h * N, (int64_t)N * 4);
+    const int64_t lbase = (base / DS);
+    const int64_t lleft = ((int64_t)a.H * N - lbase) * 4;
+    const __amdgpu_buffer_rsrc_t sl =
+        make_rsrc_n(a.lse + lbase, lleft < (int64_t)kZeroChunk ? lleft : (int64_t)kZeroChunk);
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
       const int u = tid + i * kThreads;
-      const uint32_t voff = (uint32_t)((u / CPS) * DS * 2 + (u % CPS) * 16);   // >= nbytes past PER
+      const int r = u / CPS, pr = r >> (8 - lgp), lr = r & (R - 1);
+      const bool ok = u < PER && lr < N && (gi << lgp) + pr < nseq;
+      const int prow = pr * a.hpb * N + lr;          // row in the resources
+      const uint32_t voff = ok ? (uint32_t)(prow * DS * 2 + (u % CPS) * 16) : kZeroChunk;
       rq[i] = buf_b128(sq, voff);
       rd[i] = buf_b128(sd, voff);
       rk[i] = buf_b128(sk, voff);
       ro[i] = buf_b128(so, voff);
-      lsev[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(sl, (uint32_t)((u / CPS) * 4), 0, 0));
+      lsev[i] = __uint_as_float(
+          __builtin_amdgcn_raw_buffer_load_b32(sl, ok ? (uint32_t)(prow * 4) : kZeroChunk, 0, 0));
     }
-    const __amdgpu_buffer_rsrc_t sv = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.v) + rowbase, nbytes);
+    // this lane's key of the wave's sequence
+    const int64_t wbase = ((int64_t)clamp_seq(seq_of(gi)) * a.hpb + head) * N * DS;
+    const __amdgpu_buffer_rsrc_t sk1 = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.k) + wbase, (int64_t)N * DS * 2);
+    const __amdgpu_buffer_rsrc_t sv = make_rsrc_n(reinterpret_cast<const uint16_t*>(a.v) + wbase, (int64_t)N * DS * 2);
 #pragma unroll
     for (int kc = 0; kc < D / 16; ++kc) {
       const bool in = jok && kc * 16 + g * 8 < DS;
       // (out of range: moved past the end by kZeroChunk, without a branch)
       const uint32_t ko = (uint32_t)((jc * DS + kc * 16 + g * 8) * 2) + (in ? 0u : kZeroChunk);
-      kraw[kc] = __builtin_bit_cast(bf16x8, buf_b128(sk, ko));
+      kraw[kc] = __builtin_bit_cast(bf16x8, buf_b128(sk1, ko));
       vraw[kc] = __builtin_bit_cast(bf16x8, buf_b128(sv, ko));
     }
   };
@@ -349,7 +375,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
           sq += __shfl_xor(sq, o);
         }
         dltv[i] = acc;
-        if (u / CPS < N) {
+        if (((u / CPS) & (R - 1)) < N) {     // rows past N (or of no sequence) hold zeros
           md = fmaxf(md, sq);
           ml = fmaxf(ml, fabsf(acc));
         }
@@ -379,7 +405,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   };
   // spd bytes of block (qb, this wave's keys) of sequence s: rows
   // 32 qb + 16 g + r, column j (rows past N read zero).
-  const uint32_t voff_st = (uint32_t)((lane >> 1) * ld + 16 * (lane & 1) + w * 32);
+  const uint32_t voff_st = (uint32_t)((lane >> 1) * ld + 16 * (lane & 1) + wl * 32);
   int off_tr8[2];   // byte offsets in the staged block of the two transposing reads
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh)
@@ -408,10 +434,12 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
 
   BT bA[NBT], bB[NBT];
   issue(slot);
-  fetch(slot, w, bA);
+  fetch(clamp_seq(seq_of(slot)), wl, bA);
   stats();
-  for (int seq = slot; seq < nseq; seq += nslots) {
-    const int h = seq * a.hpb + head;
+  for (int gi = slot; gi < ngroups; gi += nslots) {
+    const int seq = seq_of(gi);            // this wave's sequence (none if >= nseq)
+    const int seqc = clamp_seq(seq);
+    const int h = seqc * a.hpb + head;
     const int64_t rowbase = (int64_t)h * N * DS;
     // the previous sequence's readers are done with the tiles and slots, and
     // its histogram adds are complete
@@ -457,10 +485,11 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
         if (chunk == 0) {
           // S starts at -LSE log2 e / (scale log2 e) (-inf for an empty row
           // or a row past N, so P = 0), dP at -Dlt 2^F
-          const float L = row < N ? lsev[i] : -INFINITY;
+          const bool rin = (row & (R - 1)) < N && (gi << lgp) + (row >> (8 - lgp)) < nseq;
+          const float L = rin ? lsev[i] : -INFINITY;
           const float ss = (L == -INFINITY) ? -INFINITY : -(L * kLog2e) * inv_sl2;
           sm.init_s[row] = ss;
-          sm.init_p[row] = row < N ? -dltv[i] * sF : 0.0f;
+          sm.init_p[row] = rin ? -dltv[i] * sF : 0.0f;
           if constexpr (SPROD) {
             // features 8..10 of the row: the start as three bf16 terms
             auto split3 = [](float x, uint4& c) {
@@ -472,7 +501,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
             };
             uint4 cq, co;
             split3(ss, cq);
-            split3(row < N ? -dltv[i] : 0.0f, co);
+            split3(rin ? -dltv[i] : 0.0f, co);
             const int lo1 = row * D + swz_tile<D>(row, 1) * 8;
             *reinterpret_cast<uint4*>(sm.q + lo1) = cq;
             *reinterpret_cast<uint4*>(sm.o + lo1) = co;
@@ -499,9 +528,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     }
 
     f32x16 dk = zero_f32x16(), dv = zero_f32x16(), dq = zero_f32x16();
-    const bool wact = w < nb;
+    const bool wact = wl < nb && seq < nseq;
     auto step_a = [&](int t, uint16_t* xs, const BT* b) {
-      const int qb = (w + t) & 7;
+      const int qb = (wl + t) & (GW - 1);
       if (wact && qb < nb) {
         if constexpr (STAGE) {
           typedef int i32x2 __attribute__((ext_vector_type(2)));
@@ -517,19 +546,19 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
             wv[2 * hh] = (uint32_t)v.x;
             wv[2 * hh + 1] = (uint32_t)v.y;
           }
-          block_dkdv<NKS, NB, SPROD>(sm, off, kf, vf, wv, is_lane, sl2, qb, xs, dk, dv);
+          block_dkdv<NKS, NB, SPROD>(sm, off, kf, vf, wv, is_lane, sl2, rb, qb, xs, dk, dv);
         } else {
-          block_dkdv<NKS, NB, SPROD>(sm, off, kf, vf, b, is_lane, sl2, qb, xs, dk, dv);
+          block_dkdv<NKS, NB, SPROD>(sm, off, kf, vf, b, is_lane, sl2, rb, qb, xs, dk, dv);
         }
       }
     };
     auto step_b = [&](int t, int par) {
-      const int src = (w - t) & 7;      // key block whose dS for query block w was stored at step t
+      const int src = (wl - t) & (GW - 1);   // key block whose dS for query block wl was stored at step t
       if (wact && src < nb) {
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
-          const bf16x8 kt = lds_tr_operand(sm.k + (src * 32 + 8 * q) * D, off.tr[0], off.tr[1]);
-          const bf16x8 sv = lds_tr_operand(&sm.xs[par][src][8 * q * D], off.tr[0], off.tr[1]);
+          const bf16x8 kt = lds_tr_operand(sm.k + (rb + src * 32 + 8 * q) * D, off.tr[0], off.tr[1]);
+          const bf16x8 sv = lds_tr_operand(&sm.xs[par][p * GW + src][8 * q * D], off.tr[0], off.tr[1]);
           dq = mfma32(kt, sv, dq);
         }
       }
@@ -538,39 +567,39 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     wait_loads();
     lds_barrier();
 #pragma unroll 1
-    for (int t = 0; t < kNW - 2; t += 2) {
-      fetch(seq, (w + t + 1) & 7, bB);
+    for (int t = 0; t < GW - 2; t += 2) {
+      fetch(seqc, (wl + t + 1) & (GW - 1), bB);
       sched_fence();
       if (t > 0) step_b(t - 1, 1);
       step_a(t, sm.xs[0][w], bA);
       lds_barrier();
-      fetch(seq, (w + t + 2) & 7, bA);
+      fetch(seqc, (wl + t + 2) & (GW - 1), bA);
       sched_fence();
       step_b(t, 0);
       step_a(t + 1, sm.xs[1][w], bB);
       lds_barrier();
     }
-    // The last two steps, with the next sequence's loads issued at the start
-    // of the last one (the last sequence reloads itself, so the code is the
+    // The last two steps, with the next group's loads issued at the start
+    // of the last one (the last group reloads itself, so the code is the
     // same on every path and the waits stay exact).
-    fetch(seq, (w + kNW - 1) & 7, bB);
+    fetch(seqc, (wl + GW - 1) & (GW - 1), bB);
     sched_fence();
-    step_b(kNW - 3, 1);
-    step_a(kNW - 2, sm.xs[0][w], bA);
+    if (GW > 2) step_b(GW - 3, 1);
+    step_a(GW - 2, sm.xs[0][w], bA);
     lds_barrier();
     {
-      const int nxt = seq + nslots < nseq ? seq + nslots : seq;
-      issue(nxt);
-      fetch(nxt, w, bA);
+      const int gnx = gi + nslots < ngroups ? gi + nslots : gi;
+      issue(gnx);
+      fetch(clamp_seq(seq_of(gnx)), wl, bA);
     }
     sched_fence();
-    step_b(kNW - 2, 0);
-    step_a(kNW - 1, sm.xs[1][w], bB);
+    step_b(GW - 2, 0);
+    step_a(GW - 1, sm.xs[1][w], bB);
     lds_barrier();
-    step_b(kNW - 1, 1);
+    step_b(GW - 1, 1);
 
-    // dK, dV of key j; dQ of query w * 32 + key (features 8 u + 4 g .. + 3)
-    if (jok) {
+    // dK, dV of key j; dQ of query j (features 8 u + 4 g .. + 3)
+    if (jok && seq < nseq) {
       uint16_t* dkp = reinterpret_cast<uint16_t*>(a.dk) + rowbase + (int64_t)j * DS;
       uint16_t* dvp = reinterpret_cast<uint16_t*>(a.dv) + rowbase + (int64_t)j * DS;
       uint16_t* dqp = reinterpret_cast<uint16_t*>(a.dq) + rowbase + (int64_t)j * DS;
@@ -610,9 +639,11 @@ __global__ __launch_bounds__(256) void zero_f32_kernel(float* p, int n) {
 template <int DS, int NB>
 void launch_short_t(const BwdArgs& a, hipStream_t s) {
   const int nseq = a.H / a.hpb;
+  const int lgp = a.Sq > 128 ? 0 : (a.Sq > 64 ? 1 : 2);          // sequences per workgroup: 2^lgp
+  const int ngroups = (nseq + (1 << lgp) - 1) >> lgp;
   int slots = kMaxGridShort / a.hpb;
   if (slots < 1) slots = 1;
-  if (slots > nseq) slots = nseq;
+  if (slots > ngroups) slots = ngroups;
   const dim3 grid((unsigned)(slots * a.hpb));
   // row-wise staging reads 16 bytes from 4-byte aligned offsets
   const bool rows4 = reinterpret_cast<uintptr_t>(a.spd) % 4 == 0 && a.ld_spd % 4 == 0 &&
@@ -648,8 +679,11 @@ void launch_short_nb(const BwdArgs& a, int d, hipStream_t s) {
 }  // namespace
 
 bool bwd_short_applies(const BwdArgs& a, int d) {
+  // (a group of up to 4 sequences is read through one resource of at most
+  // 2^30 bytes)
   return d <= 32 && !a.accumulate && a.row_off == 0 && a.col_off == 0 && a.Sq == a.Sk &&
-         a.Sq >= 1 && a.Sq <= kRows && a.hpb >= 1 && a.H % a.hpb == 0;
+         a.Sq >= 1 && a.Sq <= kRows && a.hpb >= 1 && a.H % a.hpb == 0 &&
+         (int64_t)4 * a.hpb * a.Sq * d * 2 < ((int64_t)1 << 30);
 }
 
 hipError_t launch_bwd_short_bf16(const BwdArgs& a, int d, hipStream_t s) {

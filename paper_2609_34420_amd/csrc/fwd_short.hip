@@ -163,22 +163,25 @@ __device__ __forceinline__ void softmax_first_xp(const f32x16& s, f32x16& sn, co
   }
 }
 
-// Persistent forward for sequences of 33 to 256 rows with at most 127
-// buckets (bf16 in and out, head dims 8, 16, 32 on 32-wide tiles; spd rows
-// 4-byte aligned). Each wave owns 32 queries, so a workgroup covers a whole
-// sequence, and the sequence's K and V (all rows) sit in LDS: one pair of
-// barriers per sequence instead of one barrier per key tile. The per-lane
-// bias table holds the byte values 0..127 (bytes of 128 or more are mapped
-// to the padding entry 127, bias 0) and an entry of -inf (128) that masks
-// the keys past N: with K and V that is 65 KB, so two workgroups share a
-// compute unit and every SIMD runs four waves. The workgroups are
-// persistent: workgroup w takes head (w mod hpb) of every (G / hpb)-th
-// sequence, fills the table once, and loads the next sequence's K, V and Q
-// rows into registers while it computes the current one. spd words stream
-// two key blocks ahead across sequences (read 16 bytes at a time from 4-byte
-// aligned offsets, through a resource that ends with the sequence's matrix);
-// the score product of key block kb + 1 is issued before the softmax of
-// block kb. TAIL: N is not a multiple of 32.
+// Persistent forward for sequences of at most 256 rows, N a multiple of 4,
+// with at most 127 buckets (bf16 in and out, head dims 8, 16, 32 on 32-wide
+// tiles; spd rows 4-byte aligned). Each wave owns 32 queries, and the
+// sequence's K and V (all rows) sit in LDS: one pair of barriers per
+// sequence instead of one barrier per key tile. At N > 128 a workgroup
+// covers one sequence; shorter ones are packed, 2, 4 or 8 sequences of the
+// head at once (N <= 128, 64, 32), each in its own slice of the K and V
+// rows with 4, 2 or 1 waves. The per-lane bias table holds the byte values
+// 0..127 (bytes of 128 or more are mapped to the padding entry 127, bias 0)
+// and an entry of -inf (128) that masks the keys past N: with K and V that
+// is about 71 KB, so two workgroups share a compute unit and every SIMD
+// runs four waves. The workgroups are persistent: workgroup w takes head
+// (w mod hpb) of every (G / hpb)-th group of sequences, fills the table
+// once, and loads the next group's K, V and Q rows into registers while it
+// computes the current one. spd words stream two key blocks ahead across
+// groups (read 16 bytes at a time from 4-byte aligned offsets, through a
+// resource that ends with the sequence's matrix); the score product of key
+// block kb + 1 is issued before the softmax of block kb. TAIL: keys past N
+// in the last block (N not a multiple of 32, or N <= 32).
 constexpr int kShortTabEntries = 129;
 template <int DS, bool TAIL>
 __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_kernel(FwdArgs a) {
@@ -196,11 +199,12 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
   // per compute unit) and at d = 8 without a partial key block; elsewhere
   // the copy keeps four waves per SIMD without spilling
   constexpr bool ALT = DS == 32 || XP;
-  // K has 192 rows of padding: block (kb + 1) mod 8 of the last slice, read
-  // past the last block of a sequence (its product is never used), stays in
-  // the array at any slice size
-  constexpr int KROWS = ROWS + 192;
-  __shared__ __attribute__((aligned(16))) uint16_t sK[KROWS * D], sV[ROWS * D];
+  // Padding rows (zero): the K rows of block nkb mod 8, read past the last
+  // block of a sequence (the product is never used), and at N <= 32 the K
+  // and V rows of the masked second block of the last slice stay in the
+  // arrays (their P is 0, and the V rows must be finite)
+  constexpr int KROWS = ROWS + 64, VROWS = ROWS + 32;
+  __shared__ __attribute__((aligned(16))) uint16_t sK[KROWS * D], sV[VROWS * D];
   __shared__ __attribute__((aligned(16))) float sTab[kShortTabEntries * 64];
 
   const int tid = threadIdx.x;
@@ -208,11 +212,13 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
   const int col = lane & 31, g = lane >> 5;
   const uint32_t lane4 = (uint32_t)lane * 4u;
   const int N = (int)a.Sq;
-  const int nkb = (N + 31) / 32;                // at least 2
-  // P sequences of the head at once (N <= 128: 2, N <= 64: 4): sequence slot
-  // p = w / GW of a group holds LDS rows p R .. p R + R - 1 and its waves
-  // take query blocks wl = w mod GW.
-  const int lgp = N > 128 ? 0 : (N > 64 ? 1 : 2);
+  // key blocks: at least 2 (N <= 32 has a second block whose keys are all
+  // masked, so the spd stream below needs no case of its own)
+  const int nkb = N > 32 ? (N + 31) / 32 : 2;
+  // P sequences of the head at once (N <= 128: 2, N <= 64: 4, N <= 32: 8):
+  // sequence slot p = w / GW of a group holds LDS rows p R .. p R + R - 1
+  // and its waves take query blocks wl = w mod GW.
+  const int lgp = N > 128 ? 0 : (N > 64 ? 1 : (N > 32 ? 2 : 3));
   const int P = 1 << lgp, GW = kWaves >> lgp, R = ROWS >> lgp;
   const int p = w >> (3 - lgp), wl = w & (GW - 1);
   const int G = (int)gridDim.x;
@@ -249,7 +255,7 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
       const int lo = row * D + swz_tile<D>(row, ch) * 8;
       const bool k1 = XP && ch == 3, v1 = XP && ch == 1;
       *reinterpret_cast<uint4*>(sK + lo) = make_uint4(k1 ? kOne | (kOne << 16) : 0u, k1 ? kOne : 0u, 0u, 0u);
-      if (row < ROWS) *reinterpret_cast<uint4*>(sV + lo) = make_uint4(v1 ? kOne : 0u, 0u, 0u, 0u);
+      if (row < VROWS) *reinterpret_cast<uint4*>(sV + lo) = make_uint4(v1 ? kOne : 0u, 0u, 0u, 0u);
     }
   }
 
@@ -487,14 +493,14 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
 template <int DS>
 void launch_short_t(const FwdArgs& a, hipStream_t s) {
   const int nseq = a.H / a.hpb;
-  const int lgp = a.Sq > 128 ? 0 : (a.Sq > 64 ? 1 : 2);          // sequences per workgroup: 2^lgp
+  const int lgp = a.Sq > 128 ? 0 : (a.Sq > 64 ? 1 : (a.Sq > 32 ? 2 : 3));   // 2^lgp sequences per workgroup
   const int ngroups = (nseq + (1 << lgp) - 1) >> lgp;
   // two workgroups per compute unit where the registers allow four waves per SIMD
   int slots = (DS <= 16 ? 512 : 256) / a.hpb;
   if (slots < 1) slots = 1;
   if (slots > ngroups) slots = ngroups;
   const dim3 grid((unsigned)(slots * a.hpb));
-  if (a.Sq % 32 != 0)
+  if (a.Sq % 32 != 0 || a.Sq <= 32)   // keys past N masked (at N <= 32 the whole second block)
     hipLaunchKernelGGL((fwd_short_bf16_kernel<DS, true>), grid, dim3(kThreads), 0, s, a);
   else
     hipLaunchKernelGGL((fwd_short_bf16_kernel<DS, false>), grid, dim3(kThreads), 0, s, a);
@@ -503,11 +509,12 @@ void launch_short_t(const FwdArgs& a, hipStream_t s) {
 }  // namespace
 
 bool fwd_short_applies(const FwdArgs& a, int d) {
-  // (a group of up to 4 sequences is read through one resource of at most
+  // (a group of up to 8 sequences is read through one resource of at most
   // 2^30 bytes)
   return d <= 32 && !a.accumulate && a.row_off == 0 && a.col_off == 0 && a.Sq == a.Sk &&
-         a.Sq > 32 && a.Sq <= 256 && a.n_buckets <= 127 && a.hpb >= 1 && a.H % a.hpb == 0 &&
-         (int64_t)4 * a.hpb * a.Sq * d * 2 < ((int64_t)1 << 30) &&
+         a.Sq >= 1 && a.Sq <= 256 && a.Sq % 4 == 0 &&   // (keys past N are masked by spd words)
+         a.n_buckets <= 127 && a.hpb >= 1 && a.H % a.hpb == 0 &&
+         (int64_t)8 * a.hpb * a.Sq * d * 2 < ((int64_t)1 << 30) &&
          reinterpret_cast<uintptr_t>(a.spd) % 4 == 0 && a.ld_spd % 4 == 0 && a.spd_bstride % 4 == 0;
 }
 

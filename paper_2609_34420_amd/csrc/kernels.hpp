@@ -92,8 +92,9 @@ struct MergeArgs {
 
 // Launchers return the hipError_t of the launch.
 hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStream_t s);
-// Sequences of 33 to 256 rows (bf16 in and out, d <= 32, at most 127
-// buckets, spd rows 4-byte aligned): the persistent whole-sequence forward.
+// Sequences of at most 256 rows, N a multiple of 4 (bf16 in and out,
+// d <= 32, at most 127 buckets, spd rows 4-byte aligned): the persistent
+// whole-sequence forward.
 bool fwd_short_applies(const FwdArgs& a, int d);
 hipError_t launch_fwd_short_bf16(const FwdArgs& a, int d, hipStream_t s);
 // phase: -1 = all stages in order, 0 = prepare, 1 = dK/dV/dtable, 2 = dQ.

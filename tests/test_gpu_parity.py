@@ -381,6 +381,9 @@ def test_batch_of_graphs(B, N, d, spd_kind, dt):
     (19, 128, 50, 16, "shared"),        # forward: 4 sequences at once, last group of 3
     (9, 128, 64, 32, "per_graph_t"),    # forward: 4 at once at d = 32, 3 groups on 2 slots
     (7, 64, 100, 16, "per_graph"),      # forward: pairs with a partial last key block
+    (40, 8, 32, 8, "per_graph"),        # forward: 8 sequences at once (backward: 4)
+    (37, 16, 20, 16, "per_graph_t"),    # N <= 32 with a partial block, last group of 5
+    (64, 8, 12, 32, "shared"),
 ])
 def test_batch_several_graphs_per_workgroup(B, hpb, N, d, spd_kind):
     """Sequences of at most 256 nodes with more sequences than the fused
