@@ -15,9 +15,14 @@
 // in registers across the 8 steps, and every stored block is read by one
 // wave. The slots are double buffered by step parity.
 //
+// Shorter sequences are packed: at N <= 128 (64) a workgroup takes 2 (4)
+// sequences of its head at once, each in its own slice of the LDS rows with
+// 4 (2) waves that run the same diagonal schedule over 4 (2) blocks, so no
+// wave waits through steps that hold no block of its sequence.
+//
 // The workgroups are persistent: there are at most 256 of them (one per
 // compute unit, the kernel holds 160 KiB of LDS) and workgroup w takes head
-// (w mod hpb) of every (G / hpb)-th sequence, G the grid size. Its bias table
+// (w mod hpb) of every (G / hpb)-th group of sequences, G the grid size. Its bias table
 // and gradient histogram (the key-stationary kernel's layout and fixed-point
 // scheme) stay in LDS across its sequences: the table is filled and the
 // histogram flushed once. The histogram's power-of-two scale follows the
