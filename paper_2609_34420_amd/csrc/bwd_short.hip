@@ -15,10 +15,10 @@
 // in registers across the 8 steps, and every stored block is read by one
 // wave. The slots are double buffered by step parity.
 //
-// Shorter sequences are packed: at N <= 128 (64) a workgroup takes 2 (4)
-// sequences of its head at once, each in its own slice of the LDS rows with
-// 4 (2) waves that run the same diagonal schedule over 4 (2) blocks, so no
-// wave waits through steps that hold no block of its sequence.
+// Shorter sequences are packed: at N <= 128 (64, 32) a workgroup takes 2
+// (4, 8) sequences of its head at once, each in its own slice of the LDS
+// rows with 4 (2, 1) waves that run the same diagonal schedule over 4 (2, 1)
+// blocks, so no wave waits through steps that hold no block of its sequence.
 //
 // The workgroups are persistent: there are at most 256 of them (one per
 // compute unit, the kernel holds 160 KiB of LDS) and workgroup w takes head
@@ -243,10 +243,11 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   const int w = wave_id();
   const int N = (int)a.Sq;
   const int nb = (N + 31) / 32;
-  // P sequences of the head at once (N <= 128: 2, N <= 64: 4): sequence
-  // slot p = w / GW of a group holds LDS rows p R .. p R + R - 1, and its GW
-  // waves run the diagonal schedule over GW blocks (wl = w mod GW).
-  const int lgp = N > 128 ? 0 : (N > 64 ? 1 : 2);
+  // P sequences of the head at once (N <= 128: 2, N <= 64: 4, N <= 32: 8):
+  // sequence slot p = w / GW of a group holds LDS rows p R .. p R + R - 1,
+  // and its GW waves run the diagonal schedule over GW blocks (wl = w mod
+  // GW; one wave and one step at N <= 32).
+  const int lgp = N > 128 ? 0 : (N > 64 ? 1 : (N > 32 ? 2 : 3));
   const int P = 1 << lgp, GW = kNW >> lgp, R = kRows >> lgp;
   const int p = w >> (3 - lgp), wl = w & (GW - 1);
   const int rb = p * R;
@@ -587,10 +588,11 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     // The last two steps, with the next group's loads issued at the start
     // of the last one (the last group reloads itself, so the code is the
     // same on every path and the waits stay exact).
+    // (GW = 1: only the last step, whose block is also in bB)
     fetch(seqc, (wl + GW - 1) & (GW - 1), bB);
     sched_fence();
     if (GW > 2) step_b(GW - 3, 1);
-    step_a(GW - 2, sm.xs[0][w], bA);
+    if (GW > 1) step_a(GW - 2, sm.xs[0][w], bA);
     lds_barrier();
     {
       const int gnx = gi + nslots < ngroups ? gi + nslots : gi;
@@ -598,7 +600,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
       fetch(clamp_seq(seq_of(gnx)), wl, bA);
     }
     sched_fence();
-    step_b(GW - 2, 0);
+    if (GW > 1) step_b(GW - 2, 0);
     step_a(GW - 1, sm.xs[1][w], bB);
     lds_barrier();
     step_b(GW - 1, 1);
@@ -644,7 +646,7 @@ __global__ __launch_bounds__(256) void zero_f32_kernel(float* p, int n) {
 template <int DS, int NB>
 void launch_short_t(const BwdArgs& a, hipStream_t s) {
   const int nseq = a.H / a.hpb;
-  const int lgp = a.Sq > 128 ? 0 : (a.Sq > 64 ? 1 : 2);          // sequences per workgroup: 2^lgp
+  const int lgp = a.Sq > 128 ? 0 : (a.Sq > 64 ? 1 : (a.Sq > 32 ? 2 : 3));   // 2^lgp sequences per workgroup
   const int ngroups = (nseq + (1 << lgp) - 1) >> lgp;
   int slots = kMaxGridShort / a.hpb;
   if (slots < 1) slots = 1;
@@ -684,11 +686,11 @@ void launch_short_nb(const BwdArgs& a, int d, hipStream_t s) {
 }  // namespace
 
 bool bwd_short_applies(const BwdArgs& a, int d) {
-  // (a group of up to 4 sequences is read through one resource of at most
+  // (a group of up to 8 sequences is read through one resource of at most
   // 2^30 bytes)
   return d <= 32 && !a.accumulate && a.row_off == 0 && a.col_off == 0 && a.Sq == a.Sk &&
          a.Sq >= 1 && a.Sq <= kRows && a.hpb >= 1 && a.H % a.hpb == 0 &&
-         (int64_t)4 * a.hpb * a.Sq * d * 2 < ((int64_t)1 << 30);
+         (int64_t)8 * a.hpb * a.Sq * d * 2 < ((int64_t)1 << 30);
 }
 
 hipError_t launch_bwd_short_bf16(const BwdArgs& a, int d, hipStream_t s) {
