@@ -120,9 +120,10 @@ struct ShortOffsets {
 // Block (query block qb, this wave's keys): S and dP, P and dS, the bias
 // reads and gradient adds, dV and dK, and dS (bf16) into slot xs.
 // b: the lane's 16 bucket indices (4 words of spd_t, or 16 gathered bytes).
-// SPROD: the statistics come with the products (features 8..10 of the Q and
-// dO rows hold -LSE / scale and -Dlt, and the lane's K and V operands ones and
-// 2^F there), so S and dP start from zero.
+// SPROD: the statistics come with the products (features DS..DS+2 of the Q
+// and dO rows hold -LSE / scale and -Dlt, and the lane's K and V operands
+// ones and 2^F there; NKS then counts the chunk that holds them), so S and dP
+// start from zero.
 // rb: first LDS row of the wave's sequence (its slice when several
 // sequences share the workgroup).
 template <int NKS, int NB, bool SPROD, typename BT>
@@ -224,11 +225,12 @@ __device__ __forceinline__ void block_dkdv(ShortSmem<NB>& sm, const ShortOffsets
 // the wave's dS slot of that step (free until the block's dS is stored
 // there), and each lane reads its key's 16 query bytes back with two 8-bit
 // transposing LDS reads, instead of 16 byte gathers from global memory.
-// SPROD (head dim 8, N a multiple of 32): the S and dP accumulators start at
-// zero, and -LSE / scale, -Dlt enter the products through the zero-padded
-// features 8..10 (three bf16 terms each, exact to about 2^-24) of the staged
-// Q and dO rows against ones and 2^F in the lane's K and V operands, instead
-// of eight LDS reads of statistics per block.
+// SPROD (head dims 8 and 16, N a multiple of 32): the S and dP accumulators
+// start at zero, and -LSE / scale, -Dlt enter the products through the
+// zero-padded features DS..DS+2 (three bf16 terms each, exact to about 2^-24)
+// of the staged Q and dO rows against ones and 2^F in the lane's K and V
+// operands, instead of eight LDS reads of statistics per block (at DS = 16
+// one more 16-feature chunk of S and dP).
 template <int DS, int NB, bool TR, bool STAGE, bool SPROD = false>
 __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) {
   constexpr int NKS = (DS + 15) / 16;   // 16-feature chunks of S and dP that hold data
@@ -286,7 +288,8 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
   using BT = std::conditional_t<TR || STAGE, uint32_t, uint8_t>;
   constexpr int NBT = TR || STAGE ? 4 : 16;
   static_assert(!(TR && STAGE), "one way of reading spd");
-  static_assert(!SPROD || DS == 8, "statistics through the padded features need DS = 8");
+  static_assert(!SPROD || DS <= 16, "statistics through the padded features need DS <= 16");
+  constexpr int NKSP = SPROD ? (DS + 3 + 15) / 16 : NKS;   // chunks of S and dP with the statistics
 
   // The loads of a sequence, issued one sequence ahead (during the last step
   // of the previous one) into registers: its Q, dO, K and O rows, item u =
@@ -497,7 +500,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
           sm.init_s[row] = ss;
           sm.init_p[row] = rin ? -dltv[i] * sF : 0.0f;
           if constexpr (SPROD) {
-            // features 8..10 of the row: the start as three bf16 terms
+            // features DS..DS+2 of the row: the start as three bf16 terms
             auto split3 = [](float x, uint4& c) {
               const float h = (float)(__bf16)x;
               const float r1 = (x == -INFINITY) ? 0.0f : x - h;
@@ -508,7 +511,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
             uint4 cq, co;
             split3(ss, cq);
             split3(rin ? -dltv[i] : 0.0f, co);
-            const int lo1 = row * D + swz_tile<D>(row, 1) * 8;
+            const int lo1 = row * D + swz_tile<D>(row, DS / 8) * 8;
             *reinterpret_cast<uint4*>(sm.q + lo1) = cq;
             *reinterpret_cast<uint4*>(sm.o + lo1) = co;
           }
@@ -524,11 +527,13 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
       for (int e = 0; e < 8; ++e) vf[kc][e] = (__bf16)((float)vraw[kc][e] * sF);
     }
     if constexpr (SPROD) {
-      if (g == 1 && jok) {   // features 8..10 of the lane's K and V operands
+      // features DS..DS+2 of the lane's K and V operands: chunk DS / 16,
+      // lane half (DS / 8) & 1
+      if (g == ((DS / 8) & 1) && jok) {
 #pragma unroll
         for (int e = 0; e < 3; ++e) {
-          kf[0][e] = (__bf16)1.0f;
-          vf[0][e] = (__bf16)sF;
+          kf[DS / 16][e] = (__bf16)1.0f;
+          vf[DS / 16][e] = (__bf16)sF;
         }
       }
     }
@@ -552,9 +557,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
             wv[2 * hh] = (uint32_t)v.x;
             wv[2 * hh + 1] = (uint32_t)v.y;
           }
-          block_dkdv<NKS, NB, SPROD>(sm, off, kf, vf, wv, is_lane, sl2, rb, qb, xs, dk, dv);
+          block_dkdv<NKSP, NB, SPROD>(sm, off, kf, vf, wv, is_lane, sl2, rb, qb, xs, dk, dv);
         } else {
-          block_dkdv<NKS, NB, SPROD>(sm, off, kf, vf, b, is_lane, sl2, rb, qb, xs, dk, dv);
+          block_dkdv<NKSP, NB, SPROD>(sm, off, kf, vf, b, is_lane, sl2, rb, qb, xs, dk, dv);
         }
       }
     };
@@ -655,7 +660,7 @@ void launch_short_t(const BwdArgs& a, hipStream_t s) {
   // row-wise staging reads 16 bytes from 4-byte aligned offsets
   const bool rows4 = reinterpret_cast<uintptr_t>(a.spd) % 4 == 0 && a.ld_spd % 4 == 0 &&
                      a.spd_bstride % 4 == 0;
-  if constexpr (DS == 8) {
+  if constexpr (DS <= 16) {
     if (a.Sq % 32 == 0) {     // no keys past N in any block
       if (a.spd_t)
         hipLaunchKernelGGL((bwd_short_bf16_kernel<DS, NB, true, false, true>), grid, dim3(kThreads), 0, s, a);

@@ -384,6 +384,8 @@ def test_batch_of_graphs(B, N, d, spd_kind, dt):
     (40, 8, 32, 8, "per_graph"),        # forward: 8 sequences at once (backward: 4)
     (37, 16, 20, 16, "per_graph_t"),    # N <= 32 with a partial block, last group of 5
     (64, 8, 12, 32, "shared"),
+    (10, 64, 96, 16, "per_graph_t"),    # d = 16, N a multiple of 32: statistics in the products
+    (12, 32, 64, 16, "per_graph"),
 ])
 def test_batch_several_graphs_per_workgroup(B, hpb, N, d, spd_kind):
     """Sequences of at most 256 nodes with more sequences than the fused
