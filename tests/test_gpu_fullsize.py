@@ -14,8 +14,8 @@ The oracle cannot materialise N x N at N = 131072, so the checks are:
 At N = 16384 the oracle runs over every row. Each workload's GPU work runs
 once (a module fixture that keeps host copies of what the checks need), and
 so does the oracle, every head in its own worker process; one test per head
-then compares. Every per-head comparison applies the whole-tensor bars of
-the benchmark spec to that head's slice, which is stricter than to the tensor.
+then compares. Every per-head comparison applies the whole-tensor parity
+bars to that head's slice, which is stricter than to the tensor.
 """
 import gc
 import math
