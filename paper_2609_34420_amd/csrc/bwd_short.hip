@@ -27,7 +27,7 @@
 // scheme) stay in LDS across its sequences: the table is filled and the
 // histogram flushed once. The histogram's power-of-two scale follows the
 // largest norm bound seen so far (it only decreases; the accumulated sums are
-// shifted when it does). A sequence's loads are issued during the last step
+// shifted when it does). A group's loads are issued during the last step
 // of the one before. The hpb heads of a sequence run on one XCD at about the
 // same time, so they share its spd bytes in L2.
 //
@@ -436,7 +436,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
 
   // Fixed-point exponent F of the histogram: every term round(dS 2^F) stays
   // below 2^30 in magnitude, using |dS_ij| <= |dO_i| |V_j| + |Dlt_i| (P <= 1)
-  // with the maxima of the sequence at hand. F only decreases; when it does,
+  // with the maxima of the sequences at hand. F only decreases; when it does,
   // the histogram accumulated so far is shifted to the new scale.
   int fexp = 40;
   bool used = false;
@@ -450,7 +450,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_short_bf16_kernel(BwdArgs a) 
     const int seqc = clamp_seq(seq);
     const int h = seqc * a.hpb + head;
     const int64_t rowbase = (int64_t)h * N * DS;
-    // the previous sequence's readers are done with the tiles and slots, and
+    // the previous group's readers are done with the tiles and slots, and
     // its histogram adds are complete
     lds_barrier();
     {

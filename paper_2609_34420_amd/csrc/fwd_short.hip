@@ -344,7 +344,7 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
     const int gnx = gi + nslots < ngroups ? gi + nslots : gi;
     const __amdgpu_buffer_rsrc_t rs = spd_rs(clamp_seq(s));
     const __amdgpu_buffer_rsrc_t rn = spd_rs(clamp_seq(seq_of(gnx)));
-    __syncthreads();            // the previous sequence's reads of K and V are done
+    __syncthreads();            // the previous group's reads of K and V are done
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
       const int u = tid + i * kThreads;
