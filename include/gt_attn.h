@@ -87,7 +87,11 @@ gt_status_t gt_attn_fwd(const void* q, const void* k, const void* v,
  *   table    [H, n_buckets] fp32, shared by the batch
  *   lse      [B, H, N] fp32 (written)
  * B >= 1, spd_bstride >= 0; otherwise as gt_attn_fwd, which is this call
- * with B = 1. Deterministic. */
+ * with B = 1. Deterministic. Performance: in bf16 with d <= 32, graphs of at
+ * most 256 nodes (N a multiple of 4 for the forward, spd rows 4-byte aligned)
+ * run on persistent whole-sequence kernels that also pack 2, 4 or 8 graphs
+ * of at most 128, 64 or 32 nodes to a workgroup; the backward of such graphs
+ * is one fused kernel. */
 gt_status_t gt_attn_fwd_batch(const void* q, const void* k, const void* v,
                               const uint8_t* spd, int64_t spd_bstride,
                               const float* table, int32_t n_buckets,
