@@ -163,6 +163,34 @@ __device__ __forceinline__ void softmax_first_xp(const f32x16& s, f32x16& sn, co
   }
 }
 
+// The first key block of a sequence on the FMA path (no reference yet,
+// acc = 0, l = 0): the reference is set to the block's row max before the
+// one exp2, as the exact path of softmax_pv would after a first exp2.
+template <int D>
+__device__ __forceinline__ void softmax_first(const f32x16& s, const bf16x8 (&vop)[2][D / 32], float sl2,
+                                              SoftmaxState& st, f32x16 (&acc)[D / 32]) {
+  constexpr int NCB = D / 32;
+  float x[16];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    x[r] = s[r] * sl2;
+    mx = fmaxf(mx, x[r]);
+  }
+  const float mall = fmaxf(mx, __shfl_xor(mx, 32));
+  st.m = mall;
+  st.mneg = (mall == -INFINITY) ? 0.0f : -mall;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) x[r] += st.mneg;
+  bf16x8 p0, p1;
+  st.l = exp_block(x, p0, p1);
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    acc[cb] = mfma32(vop[0][cb], p0, acc[cb]);
+    acc[cb] = mfma32(vop[1][cb], p1, acc[cb]);
+  }
+}
+
 // Persistent forward for sequences of at most 256 rows, N a multiple of 4,
 // with at most 127 buckets (bf16 in and out, head dims 8, 16, 32 on 32-wide
 // tiles; spd rows 4-byte aligned). Each wave owns 32 queries, and the
@@ -406,8 +434,12 @@ __global__ __launch_bounds__(kThreads, DS <= 16 ? 4 : 2) void fwd_short_bf16_ker
             softmax_first_xp<D>(sc, sn, vop, st, qf[1], acc);
           else
             softmax_pv_xp<D>(sc, sn, vop, st, qf[1], acc);
-        } else
-          softmax_pv<D, false>(sc, vop, 32, sl2, st, acc);
+        } else {
+          if (kb == 0)
+            softmax_first<D>(sc, vop, sl2, st, acc);
+          else
+            softmax_pv<D, false>(sc, vop, 32, sl2, st, acc);
+        }
         if constexpr (!ALT) sc = sn;
       }
     };
