@@ -216,9 +216,15 @@ __device__ __forceinline__ void store_grad(float* base, int64_t idx, float x, bo
     base[idx] = x;
 }
 
+// The vector-ALU kernels split each row's loop between eight adjacent threads
+// (keys for dQ, queries for dK / dV) and add their partial sums by lane
+// shuffles at the end.
+constexpr int kValuSplit = 8;
+
 template <int D>
 __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
-  constexpr int TK = 64;             // keys per LDS tile, in blocks of 16
+  constexpr int TK = 16 * kValuSplit; // keys per LDS tile: one 16-key block per split
+  constexpr int RPB = 128 / kValuSplit;
   __shared__ __attribute__((aligned(16))) float sK[TK][D];
   __shared__ __attribute__((aligned(16))) float sV[TK][D];
   __shared__ float sT[256];
@@ -226,9 +232,10 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
   // need the unquantised dS
   __shared__ float sH[256];
   const int tid = threadIdx.x;
-  const int64_t nqb = (a.Sq + 127) / 128;
+  const int sp = tid % kValuSplit;   // this thread's 16-key block of each tile
+  const int64_t nqb = (a.Sq + RPB - 1) / RPB;
   const int h = (int)(blockIdx.x / nqb);
-  const int64_t i = (blockIdx.x % nqb) * 128 + tid;
+  const int64_t i = (blockIdx.x % nqb) * RPB + tid / kValuSplit;
   for (int t = tid; t < 256; t += 128) {
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
     sH[t] = 0.0f;
@@ -258,38 +265,44 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
       sV[r][c] = in ? vg[hk + (j0 + r) * D + c] : 0.0f;
     }
     __syncthreads();
-    if (!ok || L == -INFINITY) continue;
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
-    // blocks of 16 keys: their spd bytes in one load
-    for (int r0 = 0; r0 < nk; r0 += 16) {
-      uint32_t w[4];
-      if (a.spd_vec && r0 + 16 <= nk) {
-        const uint4 v4 = *reinterpret_cast<const uint4*>(srow + j0 + r0);
-        w[0] = v4.x; w[1] = v4.y; w[2] = v4.z; w[3] = v4.w;
-      } else {
-        load_spd16_bytes(srow, j0 + r0, a.Sk, w);
-      }
-      const int nr = nk - r0 < 16 ? nk - r0 : 16;
-      for (int r = 0; r < nr; ++r) {
-        const int key = r0 + r;
-        float sc = 0.0f, dp = 0.0f;
+    const int r0 = sp * 16;
+    if (!ok || L == -INFINITY || r0 >= nk) continue;
+    // this thread's block of 16 keys: their spd bytes in one load
+    uint32_t w[4];
+    if (a.spd_vec && r0 + 16 <= nk) {
+      const uint4 v4 = *reinterpret_cast<const uint4*>(srow + j0 + r0);
+      w[0] = v4.x; w[1] = v4.y; w[2] = v4.z; w[3] = v4.w;
+    } else {
+      load_spd16_bytes(srow, j0 + r0, a.Sk, w);
+    }
+    const int nr = nk - r0 < 16 ? nk - r0 : 16;
+    for (int r = 0; r < nr; ++r) {
+      const int key = r0 + r;
+      float sc = 0.0f, dp = 0.0f;
 #pragma unroll
-        for (int c = 0; c < D; ++c) {
-          sc = fmaf(qv[c], sK[key][c], sc);
-          dp = fmaf(dov[c], sV[key][c], dp);
-        }
-        const uint32_t b = (w[r >> 2] >> (8 * (r & 3))) & 0xffu;
-        const float p = exp2_fast((sc + sT[b] - L) * kLog2e);
-        const float ds = p * (dp - dlt);
-#pragma unroll
-        for (int c = 0; c < D; ++c) acc[c] = fmaf(ds, sK[key][c], acc[c]);
-        if (b < (uint32_t)a.n_buckets) atomicAdd(&sH[b], ds);
+      for (int c = 0; c < D; ++c) {
+        sc = fmaf(qv[c], sK[key][c], sc);
+        dp = fmaf(dov[c], sV[key][c], dp);
       }
+      const uint32_t b = (w[r >> 2] >> (8 * (r & 3))) & 0xffu;
+      const float p = exp2_fast((sc + sT[b] - L) * kLog2e);
+      const float ds = p * (dp - dlt);
+#pragma unroll
+      for (int c = 0; c < D; ++c) acc[c] = fmaf(ds, sK[key][c], acc[c]);
+      if (b < (uint32_t)a.n_buckets) atomicAdd(&sH[b], ds);
     }
   }
+  // the row's partial sums (adjacent lanes)
+#pragma unroll
+  for (int c = 0; c < D; ++c)
+#pragma unroll
+    for (int o = 1; o < kValuSplit; o <<= 1) acc[c] += __shfl_xor(acc[c], o);
   if (ok) {
 #pragma unroll
-    for (int c = 0; c < D; ++c) store_grad(reinterpret_cast<float*>(a.dq), hq + i * D + c, acc[c] * a.scale, a.accumulate);
+    for (int c = 0; c < D; ++c)
+      if (c % kValuSplit == sp)
+        store_grad(reinterpret_cast<float*>(a.dq), hq + i * D + c, acc[c] * a.scale, a.accumulate);
   }
   __syncthreads();
   float* dth = a.dtable + (int64_t)table_row(a, h) * a.n_buckets;
@@ -299,15 +312,17 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
 
 template <int D>
 __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
-  constexpr int TQ = 32;
+  constexpr int TQ = 8 * kValuSplit;  // queries per LDS tile: 8 per split
+  constexpr int RPB = 128 / kValuSplit;
   __shared__ float sQ[TQ][D];
   __shared__ float sO[TQ][D];
   __shared__ float sL[TQ], sD[TQ];
   __shared__ float sT[256];
   const int tid = threadIdx.x;
-  const int64_t nkb = (a.Sk + 127) / 128;
+  const int sp = tid % kValuSplit;   // this thread's 8 queries of each tile
+  const int64_t nkb = (a.Sk + RPB - 1) / RPB;
   const int h = (int)(blockIdx.x / nkb);
-  const int64_t j = (blockIdx.x % nkb) * 128 + tid;
+  const int64_t j = (blockIdx.x % nkb) * RPB + tid / kValuSplit;
   for (int t = tid; t < 256; t += 128)
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
@@ -337,7 +352,8 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
     __syncthreads();
     if (!ok) continue;
     const int nq = (int)((a.Sq - i0) < TQ ? (a.Sq - i0) : TQ);
-    for (int r = 0; r < nq; ++r) {
+    const int e = (sp + 1) * (TQ / kValuSplit) < nq ? (sp + 1) * (TQ / kValuSplit) : nq;
+    for (int r = sp * (TQ / kValuSplit); r < e; ++r) {
       if (sL[r] == -INFINITY) continue;
       float s = 0.0f, dp = 0.0f;
 #pragma unroll
@@ -354,9 +370,18 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
       }
     }
   }
+  // the key's partial sums (adjacent lanes)
+#pragma unroll
+  for (int c = 0; c < D; ++c)
+#pragma unroll
+    for (int o = 1; o < kValuSplit; o <<= 1) {
+      dk[c] += __shfl_xor(dk[c], o);
+      dv[c] += __shfl_xor(dv[c], o);
+    }
   if (!ok) return;
 #pragma unroll
   for (int c = 0; c < D; ++c) {
+    if (c % kValuSplit != sp) continue;
     store_grad(reinterpret_cast<float*>(a.dk), hk + j * D + c, dk[c] * a.scale, a.accumulate);
     store_grad(reinterpret_cast<float*>(a.dv), hk + j * D + c, dv[c], a.accumulate);
   }
@@ -394,7 +419,8 @@ hipError_t launch_bwd_t(const BwdArgs& a, bool bf16, int phase, hipStream_t s) {
     return e;
   }
   // vector-ALU path (fp32): dK/dV in phase 1, dQ and dtable in phase 2
-  const int64_t nkb = (a.Sk + 127) / 128, nqb = (a.Sq + 127) / 128;
+  constexpr int RPB = 128 / kValuSplit;
+  const int64_t nkb = (a.Sk + RPB - 1) / RPB, nqb = (a.Sq + RPB - 1) / RPB;
   if (phase < 0 || phase == 1) {
     hipLaunchKernelGGL((bwd_dkdv_valu_kernel<D>), dim3((unsigned)(nkb * a.H)), dim3(128), 0, s, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -374,19 +374,24 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   }
 }
 
-// Vector-ALU path (fp32 inputs, any head dim): one thread per query row,
-// keys staged through LDS, fp32 math with the hardware exp2 and logf; o is
-// fp32.
+// Vector-ALU path (fp32 inputs, any head dim): eight adjacent threads per
+// query row, keys staged through LDS 128 at a time and split between the
+// eight (thread s takes the 16-key block s of every tile), each with its own
+// online softmax; the eight states are combined by lane shuffles at the end.
+// fp32 math with the hardware exp2 and logf; o is fp32.
+constexpr int kValuSplit = 8;
 template <int D>
 __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
-  constexpr int TK = 64;             // keys per LDS tile, in blocks of 16
+  constexpr int TK = 16 * kValuSplit; // keys per LDS tile: one 16-key block per split
+  constexpr int RPB = 128 / kValuSplit;
   __shared__ __attribute__((aligned(16))) float sK[TK][D];
   __shared__ __attribute__((aligned(16))) float sV[TK][D];
   __shared__ float sT[256];
   const int tid = threadIdx.x;
-  const int64_t nqb = (a.Sq + 127) / 128;
+  const int sp = tid % kValuSplit;   // this thread's 16-key block of each tile
+  const int64_t nqb = (a.Sq + RPB - 1) / RPB;
   const int h = (int)(blockIdx.x / nqb);
-  const int64_t i = (blockIdx.x % nqb) * 128 + tid;
+  const int64_t i = (blockIdx.x % nqb) * RPB + tid / kValuSplit;
   for (int t = tid; t < 256; t += 128)
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
   const float* qg = reinterpret_cast<const float*>(a.q);
@@ -411,57 +416,74 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
       sV[r][c] = in ? vg[hk + (j0 + r) * D + c] : 0.0f;
     }
     __syncthreads();
-    if (!ok) continue;
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
-    // blocks of 16 keys: their spd bytes in one load, one running-max update
-    for (int r0 = 0; r0 < nk; r0 += 16) {
-      uint32_t w[4];
-      if (a.spd_vec && r0 + 16 <= nk) {
-        const uint4 v4 = *reinterpret_cast<const uint4*>(srow + j0 + r0);
-        w[0] = v4.x; w[1] = v4.y; w[2] = v4.z; w[3] = v4.w;
-      } else {
-        load_spd16_bytes(srow, j0 + r0, a.Sk, w);
-      }
-      float sc[16];
-      float bm = -INFINITY;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = sT[(w[r >> 2] >> (8 * (r & 3))) & 0xffu];
-#pragma unroll
-        for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[r0 + r][c], x);
-        sc[r] = (r0 + r < nk) ? x : -INFINITY;
-        bm = fmaxf(bm, sc[r]);
-      }
-      if (bm == -INFINITY) continue;
-      if (bm > m) {
-        const float alpha = (m == -INFINITY) ? 0.0f : exp2_fast((m - bm) * kLog2e);
-        l *= alpha;
-#pragma unroll
-        for (int c = 0; c < D; ++c) acc[c] *= alpha;
-        m = bm;
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = exp2_fast((sc[r] - m) * kLog2e);
-        l += p;
-#pragma unroll
-        for (int c = 0; c < D; ++c) acc[c] = fmaf(p, sV[r0 + r][c], acc[c]);
-      }
+    const int r0 = sp * 16;
+    if (!ok || r0 >= nk) continue;
+    // this thread's block of 16 keys: their spd bytes in one load, one
+    // running-max update
+    uint32_t w[4];
+    if (a.spd_vec && r0 + 16 <= nk) {
+      const uint4 v4 = *reinterpret_cast<const uint4*>(srow + j0 + r0);
+      w[0] = v4.x; w[1] = v4.y; w[2] = v4.z; w[3] = v4.w;
+    } else {
+      load_spd16_bytes(srow, j0 + r0, a.Sk, w);
     }
+    float sc[16];
+    float bm = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float x = sT[(w[r >> 2] >> (8 * (r & 3))) & 0xffu];
+#pragma unroll
+      for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[r0 + r][c], x);
+      sc[r] = (r0 + r < nk) ? x : -INFINITY;
+      bm = fmaxf(bm, sc[r]);
+    }
+    if (bm == -INFINITY) continue;
+    if (bm > m) {
+      const float alpha = (m == -INFINITY) ? 0.0f : exp2_fast((m - bm) * kLog2e);
+      l *= alpha;
+#pragma unroll
+      for (int c = 0; c < D; ++c) acc[c] *= alpha;
+      m = bm;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float p = exp2_fast((sc[r] - m) * kLog2e);
+      l += p;
+#pragma unroll
+      for (int c = 0; c < D; ++c) acc[c] = fmaf(p, sV[r0 + r][c], acc[c]);
+    }
+  }
+  // combine the states of the row (adjacent lanes): max, then each
+  // state scaled to it and summed
+  float mall = m;
+#pragma unroll
+  for (int o = 1; o < kValuSplit; o <<= 1) mall = fmaxf(mall, __shfl_xor(mall, o));
+  const float wgt = (m == -INFINITY) ? 0.0f : exp2_fast((m - mall) * kLog2e);
+  l *= wgt;
+#pragma unroll
+  for (int o = 1; o < kValuSplit; o <<= 1) l += __shfl_xor(l, o);
+#pragma unroll
+  for (int c = 0; c < D; ++c) {
+    acc[c] *= wgt;
+#pragma unroll
+    for (int o = 1; o < kValuSplit; o <<= 1) acc[c] += __shfl_xor(acc[c], o);
   }
   if (!ok) return;
   float inv = l > 0.0f ? 1.0f / l : 0.0f;
-  float lse_out = l > 0.0f ? m + logf(l) : -INFINITY;
+  float lse_out = l > 0.0f ? mall + logf(l) : -INFINITY;
   float wo = 0.0f;     // weight of the running state (accumulate mode)
   if (a.accumulate) {
     float wb;
     lse_merge_weights(a.lse[(int64_t)h * a.Sq + i], lse_out, wo, wb, lse_out);
     inv *= wb;
   }
+  // every thread of the row writes features c = sp mod 8; the first the LSE
   float* op = reinterpret_cast<float*>(a.o) + hq + i * D;
 #pragma unroll
-  for (int c = 0; c < D; ++c) op[c] = wo != 0.0f ? fmaf(op[c], wo, acc[c] * inv) : acc[c] * inv;
-  a.lse[(int64_t)h * a.Sq + i] = lse_out;
+  for (int c = 0; c < D; ++c)
+    if (c % kValuSplit == sp) op[c] = wo != 0.0f ? fmaf(op[c], wo, acc[c] * inv) : acc[c] * inv;
+  if (sp == 0) a.lse[(int64_t)h * a.Sq + i] = lse_out;
 }
 
 template <int D, int DS, bool OUT_F32>
@@ -515,7 +537,7 @@ hipError_t launch_fwd(const FwdArgs& a, int d, bool bf16, bool out_f32, hipStrea
       default: return out_f32 ? launch_fwd_bf16<64, 64, true>(a, s) : launch_fwd_bf16<64, 64, false>(a, s);
     }
   }
-  const dim3 grid((unsigned)((a.Sq + 127) / 128 * a.H));
+  const dim3 grid((unsigned)((a.Sq + 128 / kValuSplit - 1) / (128 / kValuSplit) * a.H));
   switch (d) {
     case 8: hipLaunchKernelGGL((fwd_valu_kernel<8>), grid, dim3(128), 0, s, a); break;
     case 16: hipLaunchKernelGGL((fwd_valu_kernel<16>), grid, dim3(128), 0, s, a); break;
