@@ -216,14 +216,15 @@ __device__ __forceinline__ void store_grad(float* base, int64_t idx, float x, bo
     base[idx] = x;
 }
 
-// The vector-ALU kernels split each row's loop between eight adjacent threads
-// (keys for dQ, queries for dK / dV) and add their partial sums by lane
-// shuffles at the end.
-constexpr int kValuSplit = 8;
+// The vector-ALU kernels split each row's loop between kValuSplit adjacent
+// threads (keys for dQ, queries for dK / dV) and add their partial sums by
+// lane shuffles at the end.
+constexpr int kValuSplit = 16;
 
 template <int D>
 __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
-  constexpr int TK = 16 * kValuSplit; // keys per LDS tile: one 16-key block per split
+  constexpr int KB = 128 / kValuSplit; // keys per thread per LDS tile
+  constexpr int TK = KB * kValuSplit;
   constexpr int RPB = 128 / kValuSplit;
   __shared__ __attribute__((aligned(16))) float sK[TK][D];
   __shared__ __attribute__((aligned(16))) float sV[TK][D];
@@ -232,7 +233,7 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
   // need the unquantised dS
   __shared__ float sH[256];
   const int tid = threadIdx.x;
-  const int sp = tid % kValuSplit;   // this thread's 16-key block of each tile
+  const int sp = tid % kValuSplit;   // this thread's key block of each tile
   const int64_t nqb = (a.Sq + RPB - 1) / RPB;
   const int h = (int)(blockIdx.x / nqb);
   const int64_t i = (blockIdx.x % nqb) * RPB + tid / kValuSplit;
@@ -258,25 +259,15 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
   const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
     __syncthreads();
-    for (int t = tid; t < TK * D; t += 128) {
-      const int r = t / D, c = t % D;
-      const bool in = j0 + r < a.Sk;
-      sK[r][c] = in ? kg[hk + (j0 + r) * D + c] : 0.0f;
-      sV[r][c] = in ? vg[hk + (j0 + r) * D + c] : 0.0f;
-    }
+    stage_rows_f32<TK, D, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
     __syncthreads();
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
-    const int r0 = sp * 16;
+    const int r0 = sp * KB;
     if (!ok || L == -INFINITY || r0 >= nk) continue;
-    // this thread's block of 16 keys: their spd bytes in one load
+    // this thread's block of KB keys: their spd bytes in one load
     uint32_t w[4];
-    if (a.spd_vec && r0 + 16 <= nk) {
-      const uint4 v4 = *reinterpret_cast<const uint4*>(srow + j0 + r0);
-      w[0] = v4.x; w[1] = v4.y; w[2] = v4.z; w[3] = v4.w;
-    } else {
-      load_spd16_bytes(srow, j0 + r0, a.Sk, w);
-    }
-    const int nr = nk - r0 < 16 ? nk - r0 : 16;
+    load_spd_block<KB>(srow, j0 + r0, a.Sk, a.spd_vec && r0 + KB <= nk, w);
+    const int nr = nk - r0 < KB ? nk - r0 : KB;
     for (int r = 0; r < nr; ++r) {
       const int key = r0 + r;
       float sc = 0.0f, dp = 0.0f;
@@ -312,14 +303,15 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
 
 template <int D>
 __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
-  constexpr int TQ = 8 * kValuSplit;  // queries per LDS tile: 8 per split
+  constexpr int QB = 64 / kValuSplit;  // queries per thread per LDS tile
+  constexpr int TQ = QB * kValuSplit;
   constexpr int RPB = 128 / kValuSplit;
-  __shared__ float sQ[TQ][D];
-  __shared__ float sO[TQ][D];
+  __shared__ __attribute__((aligned(16))) float sQ[TQ][D];
+  __shared__ __attribute__((aligned(16))) float sO[TQ][D];
   __shared__ float sL[TQ], sD[TQ];
   __shared__ float sT[256];
   const int tid = threadIdx.x;
-  const int sp = tid % kValuSplit;   // this thread's 8 queries of each tile
+  const int sp = tid % kValuSplit;   // this thread's queries of each tile
   const int64_t nkb = (a.Sk + RPB - 1) / RPB;
   const int h = (int)(blockIdx.x / nkb);
   const int64_t j = (blockIdx.x % nkb) * RPB + tid / kValuSplit;
@@ -338,12 +330,8 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
   }
   for (int64_t i0 = 0; i0 < a.Sq; i0 += TQ) {
     __syncthreads();
-    for (int t = tid; t < TQ * D; t += 128) {
-      const int r = t / D, c = t % D;
-      const bool in = i0 + r < a.Sq;
-      sQ[r][c] = in ? reinterpret_cast<const float*>(a.q)[hq + (i0 + r) * D + c] : 0.0f;
-      sO[r][c] = in ? reinterpret_cast<const float*>(a.d_o)[hq + (i0 + r) * D + c] : 0.0f;
-    }
+    stage_rows_f32<TQ, D, 128>(reinterpret_cast<const float*>(a.q) + hq, reinterpret_cast<const float*>(a.d_o) + hq,
+                               i0, a.Sq, sQ, sO);
     for (int t = tid; t < TQ; t += 128) {
       const bool in = i0 + t < a.Sq;
       sL[t] = in ? a.lse[(int64_t)h * a.Sq + i0 + t] : -INFINITY;
@@ -352,8 +340,8 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
     __syncthreads();
     if (!ok) continue;
     const int nq = (int)((a.Sq - i0) < TQ ? (a.Sq - i0) : TQ);
-    const int e = (sp + 1) * (TQ / kValuSplit) < nq ? (sp + 1) * (TQ / kValuSplit) : nq;
-    for (int r = sp * (TQ / kValuSplit); r < e; ++r) {
+    const int e = (sp + 1) * QB < nq ? (sp + 1) * QB : nq;
+    for (int r = sp * QB; r < e; ++r) {
       if (sL[r] == -INFINITY) continue;
       float s = 0.0f, dp = 0.0f;
 #pragma unroll

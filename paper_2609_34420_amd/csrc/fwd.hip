@@ -374,21 +374,22 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_bf16_kernel(FwdArgs a) {
   }
 }
 
-// Vector-ALU path (fp32 inputs, any head dim): eight adjacent threads per
-// query row, keys staged through LDS 128 at a time and split between the
-// eight (thread s takes the 16-key block s of every tile), each with its own
-// online softmax; the eight states are combined by lane shuffles at the end.
+// Vector-ALU path (fp32 inputs, any head dim): kValuSplit adjacent threads
+// per query row, keys staged through LDS 128 at a time and split between
+// them (thread s takes the KB-key block s of every tile), each with its own
+// online softmax; the states are combined by lane shuffles at the end.
 // fp32 math with the hardware exp2 and logf; o is fp32.
-constexpr int kValuSplit = 8;
+constexpr int kValuSplit = 16;
 template <int D>
 __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
-  constexpr int TK = 16 * kValuSplit; // keys per LDS tile: one 16-key block per split
+  constexpr int KB = 128 / kValuSplit; // keys per thread per LDS tile
+  constexpr int TK = KB * kValuSplit;
   constexpr int RPB = 128 / kValuSplit;
   __shared__ __attribute__((aligned(16))) float sK[TK][D];
   __shared__ __attribute__((aligned(16))) float sV[TK][D];
   __shared__ float sT[256];
   const int tid = threadIdx.x;
-  const int sp = tid % kValuSplit;   // this thread's 16-key block of each tile
+  const int sp = tid % kValuSplit;   // this thread's key block of each tile
   const int64_t nqb = (a.Sq + RPB - 1) / RPB;
   const int h = (int)(blockIdx.x / nqb);
   const int64_t i = (blockIdx.x % nqb) * RPB + tid / kValuSplit;
@@ -409,29 +410,19 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   float m = -INFINITY, l = 0.0f;     // running max (natural units) and sum relative to it
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
     __syncthreads();
-    for (int t = tid; t < TK * D; t += 128) {
-      const int r = t / D, c = t % D;
-      const bool in = j0 + r < a.Sk;
-      sK[r][c] = in ? kg[hk + (j0 + r) * D + c] : 0.0f;
-      sV[r][c] = in ? vg[hk + (j0 + r) * D + c] : 0.0f;
-    }
+    stage_rows_f32<TK, D, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
     __syncthreads();
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
-    const int r0 = sp * 16;
+    const int r0 = sp * KB;
     if (!ok || r0 >= nk) continue;
-    // this thread's block of 16 keys: their spd bytes in one load, one
+    // this thread's block of KB keys: their spd bytes in one load, one
     // running-max update
     uint32_t w[4];
-    if (a.spd_vec && r0 + 16 <= nk) {
-      const uint4 v4 = *reinterpret_cast<const uint4*>(srow + j0 + r0);
-      w[0] = v4.x; w[1] = v4.y; w[2] = v4.z; w[3] = v4.w;
-    } else {
-      load_spd16_bytes(srow, j0 + r0, a.Sk, w);
-    }
-    float sc[16];
+    load_spd_block<KB>(srow, j0 + r0, a.Sk, a.spd_vec && r0 + KB <= nk, w);
+    float sc[KB];
     float bm = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
+    for (int r = 0; r < KB; ++r) {
       float x = sT[(w[r >> 2] >> (8 * (r & 3))) & 0xffu];
 #pragma unroll
       for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[r0 + r][c], x);
@@ -447,7 +438,7 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
       m = bm;
     }
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
+    for (int r = 0; r < KB; ++r) {
       const float p = exp2_fast((sc[r] - m) * kLog2e);
       l += p;
 #pragma unroll
@@ -478,7 +469,7 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
     lse_merge_weights(a.lse[(int64_t)h * a.Sq + i], lse_out, wo, wb, lse_out);
     inv *= wb;
   }
-  // every thread of the row writes features c = sp mod 8; the first the LSE
+  // every thread of the row writes the features c = sp mod kValuSplit; the first the LSE
   float* op = reinterpret_cast<float*>(a.o) + hq + i * D;
 #pragma unroll
   for (int c = 0; c < D; ++c)
