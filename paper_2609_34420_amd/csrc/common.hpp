@@ -181,22 +181,20 @@ __device__ __forceinline__ void load_spd16_bytes(const uint8_t* row, int64_t j, 
 }
 
 
-// spd bytes j .. j + KB - 1 (KB = 16, 8 or 4) of a row into w (bytes past
+// spd bytes j .. j + KB - 1 (KB = 16 or 8) of a row into w (bytes past
 // `limit` as 0, words past the block 0): one aligned load of KB bytes when
 // `vec` (the whole block in range and the row 16-byte aligned), else bytes.
 template <int KB>
 __device__ __forceinline__ void load_spd_block(const uint8_t* row, int64_t j, int64_t limit, bool vec,
                                                uint32_t w[4]) {
-  static_assert(KB == 16 || KB == 8 || KB == 4, "spd block of 4, 8 or 16 bytes");
+  static_assert(KB == 16 || KB == 8, "spd block of 8 or 16 bytes");
   if (vec) {
     if constexpr (KB == 16) {
       const uint4 v4 = *reinterpret_cast<const uint4*>(row + j);
       w[0] = v4.x; w[1] = v4.y; w[2] = v4.z; w[3] = v4.w;
-    } else if constexpr (KB == 8) {
+    } else {
       const uint2 v2 = *reinterpret_cast<const uint2*>(row + j);
       w[0] = v2.x; w[1] = v2.y; w[2] = 0; w[3] = 0;
-    } else {
-      w[0] = *reinterpret_cast<const uint32_t*>(row + j); w[1] = 0; w[2] = 0; w[3] = 0;
     }
   } else {
     load_spd16_bytes(row, j, limit - j < KB ? limit : j + KB, w);
@@ -204,31 +202,22 @@ __device__ __forceinline__ void load_spd_block(const uint8_t* row, int64_t j, in
 }
 
 // Rows r0 .. r0 + R - 1 of two row-major fp32 [nrows, D] tensors into LDS
-// tiles by NT threads, rows past nrows as zero: 16-byte loads and stores
-// when both sources are 16-byte aligned (D is a multiple of 4), else 4-byte.
+// tiles by NT threads, rows past nrows as zero, in 16-byte loads and stores.
+// x and y are 16-byte aligned: the entry points reject unaligned tensors, and
+// a head's rows start at a multiple of 16 bytes since D is a multiple of 4.
 template <int R, int D, int NT>
 __device__ __forceinline__ void stage_rows_f32(const float* x, const float* y, int64_t r0, int64_t nrows,
                                                float (*sx)[D], float (*sy)[D]) {
   static_assert(D % 4 == 0, "rows of whole 16-byte chunks");
-  const int tid = threadIdx.x;
-  if (((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(y)) & 15) == 0) {
-    for (int t = tid; t < R * D / 4; t += NT) {
-      const int r = t / (D / 4), c = (t % (D / 4)) * 4;
-      float4 u = make_float4(0.0f, 0.0f, 0.0f, 0.0f), v = u;
-      if (r0 + r < nrows) {
-        u = *reinterpret_cast<const float4*>(x + (r0 + r) * D + c);
-        v = *reinterpret_cast<const float4*>(y + (r0 + r) * D + c);
-      }
-      *reinterpret_cast<float4*>(&sx[r][c]) = u;
-      *reinterpret_cast<float4*>(&sy[r][c]) = v;
+  for (int t = (int)threadIdx.x; t < R * D / 4; t += NT) {
+    const int r = t / (D / 4), c = (t % (D / 4)) * 4;
+    float4 u = make_float4(0.0f, 0.0f, 0.0f, 0.0f), v = u;
+    if (r0 + r < nrows) {
+      u = *reinterpret_cast<const float4*>(x + (r0 + r) * D + c);
+      v = *reinterpret_cast<const float4*>(y + (r0 + r) * D + c);
     }
-  } else {
-    for (int t = tid; t < R * D; t += NT) {
-      const int r = t / D, c = t % D;
-      const bool in = r0 + r < nrows;
-      sx[r][c] = in ? x[(r0 + r) * D + c] : 0.0f;
-      sy[r][c] = in ? y[(r0 + r) * D + c] : 0.0f;
-    }
+    *reinterpret_cast<float4*>(&sx[r][c]) = u;
+    *reinterpret_cast<float4*>(&sy[r][c]) = v;
   }
 }
 }  // namespace gt
