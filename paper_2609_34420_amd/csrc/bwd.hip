@@ -226,8 +226,9 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
   constexpr int KB = 128 / kValuSplit; // keys per thread per LDS tile
   constexpr int TK = KB * kValuSplit;
   constexpr int RPB = 128 / kValuSplit;
-  __shared__ __attribute__((aligned(16))) float sK[TK][D];
-  __shared__ __attribute__((aligned(16))) float sV[TK][D];
+  constexpr int LR = valu_tile_rows<TK, KB>(), DP = valu_row_stride<D>();
+  __shared__ __attribute__((aligned(16))) float sK[LR][DP];
+  __shared__ __attribute__((aligned(16))) float sV[LR][DP];
   __shared__ float sT[256];
   // dtable histogram in fp32: LDS float atomics are slow, but fp32 inputs
   // need the unquantised dS
@@ -259,7 +260,7 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
   const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
     __syncthreads();
-    stage_rows_f32<TK, D, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
+    stage_rows_f32<TK, D, KB, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
     __syncthreads();
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
     const int r0 = sp * KB;
@@ -270,17 +271,18 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
     const int nr = nk - r0 < KB ? nk - r0 : KB;
     for (int r = 0; r < nr; ++r) {
       const int key = r0 + r;
+      const int lr = valu_row<KB>(key);
       float sc = 0.0f, dp = 0.0f;
 #pragma unroll
       for (int c = 0; c < D; ++c) {
-        sc = fmaf(qv[c], sK[key][c], sc);
-        dp = fmaf(dov[c], sV[key][c], dp);
+        sc = fmaf(qv[c], sK[lr][c], sc);
+        dp = fmaf(dov[c], sV[lr][c], dp);
       }
       const uint32_t b = (w[r >> 2] >> (8 * (r & 3))) & 0xffu;
       const float p = exp2_fast((sc + sT[b] - L) * kLog2e);
       const float ds = p * (dp - dlt);
 #pragma unroll
-      for (int c = 0; c < D; ++c) acc[c] = fmaf(ds, sK[key][c], acc[c]);
+      for (int c = 0; c < D; ++c) acc[c] = fmaf(ds, sK[lr][c], acc[c]);
       if (b < (uint32_t)a.n_buckets) atomicAdd(&sH[b], ds);
     }
   }
@@ -306,15 +308,19 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
   constexpr int QB = 64 / kValuSplit;  // queries per thread per LDS tile
   constexpr int TQ = QB * kValuSplit;
   constexpr int RPB = 128 / kValuSplit;
-  __shared__ __attribute__((aligned(16))) float sQ[TQ][D];
-  __shared__ __attribute__((aligned(16))) float sO[TQ][D];
+  constexpr int LR = valu_tile_rows<TQ, QB>(), DP = valu_row_stride<D>();
+  __shared__ __attribute__((aligned(16))) float sQ[LR][DP];
+  __shared__ __attribute__((aligned(16))) float sO[LR][DP];
   __shared__ float sL[TQ], sD[TQ];
   __shared__ float sT[256];
+  __shared__ uint8_t sS[TQ][RPB];    // spd of the tile's queries x this workgroup's keys
   const int tid = threadIdx.x;
   const int sp = tid % kValuSplit;   // this thread's queries of each tile
   const int64_t nkb = (a.Sk + RPB - 1) / RPB;
   const int h = (int)(blockIdx.x / nkb);
-  const int64_t j = (blockIdx.x % nkb) * RPB + tid / kValuSplit;
+  const int64_t jb = (blockIdx.x % nkb) * RPB;
+  const int jl = tid / kValuSplit;   // this thread's key within the workgroup
+  const int64_t j = jb + jl;
   for (int t = tid; t < 256; t += 128)
     sT[t] = (t < a.n_buckets) ? a.table[(int64_t)table_row(a, h) * a.n_buckets + t] : 0.0f;
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
@@ -330,12 +336,17 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
   }
   for (int64_t i0 = 0; i0 < a.Sq; i0 += TQ) {
     __syncthreads();
-    stage_rows_f32<TQ, D, 128>(reinterpret_cast<const float*>(a.q) + hq, reinterpret_cast<const float*>(a.d_o) + hq,
+    stage_rows_f32<TQ, D, QB, 128>(reinterpret_cast<const float*>(a.q) + hq, reinterpret_cast<const float*>(a.d_o) + hq,
                                i0, a.Sq, sQ, sO);
     for (int t = tid; t < TQ; t += 128) {
       const bool in = i0 + t < a.Sq;
       sL[t] = in ? a.lse[(int64_t)h * a.Sq + i0 + t] : -INFINITY;
       sD[t] = in ? a.dlt[(int64_t)h * a.Sq + i0 + t] : 0.0f;
+    }
+    // the tile's spd bytes, issued together rather than one per score in the loop
+    for (int t = tid; t < TQ * RPB; t += 128) {
+      const int r = t / RPB, c = t % RPB;
+      sS[r][c] = (i0 + r < a.Sq && jb + c < a.Sk) ? sbase[(i0 + r) * a.ld_spd + jb + c] : (uint8_t)0;
     }
     __syncthreads();
     if (!ok) continue;
@@ -343,18 +354,19 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
     const int e = (sp + 1) * QB < nq ? (sp + 1) * QB : nq;
     for (int r = sp * QB; r < e; ++r) {
       if (sL[r] == -INFINITY) continue;
+      const int lr = valu_row<QB>(r);
       float s = 0.0f, dp = 0.0f;
 #pragma unroll
       for (int c = 0; c < D; ++c) {
-        s = fmaf(sQ[r][c], kv[c], s);
-        dp = fmaf(sO[r][c], vv[c], dp);
+        s = fmaf(sQ[lr][c], kv[c], s);
+        dp = fmaf(sO[lr][c], vv[c], dp);
       }
-      const float p = exp2_fast((s + sT[sbase[(i0 + r) * a.ld_spd + j]] - sL[r]) * kLog2e);
+      const float p = exp2_fast((s + sT[sS[r][jl]] - sL[r]) * kLog2e);
       const float ds = p * (dp - sD[r]);
 #pragma unroll
       for (int c = 0; c < D; ++c) {
-        dv[c] = fmaf(p, sO[r][c], dv[c]);
-        dk[c] = fmaf(ds, sQ[r][c], dk[c]);
+        dv[c] = fmaf(p, sO[lr][c], dv[c]);
+        dk[c] = fmaf(ds, sQ[lr][c], dk[c]);
       }
     }
   }

@@ -201,13 +201,29 @@ __device__ __forceinline__ void load_spd_block(const uint8_t* row, int64_t j, in
   }
 }
 
+// LDS tiles of the fp32 vector-ALU kernels. Each of the 16 threads of a row
+// reads its own block of GB consecutive tile rows, so at any one read the
+// threads are GB rows apart. Tile row r is kept at LDS row r + r / GB with a
+// row stride of D + 4 floats: thread s then reads LDS row s (GB + 1) + k,
+// and for D = 8, 16, 32, 64 the 16 threads' 16-byte reads fall in distinct
+// bank groups. Without the padding and the gap they would all hit the same
+// banks.
+template <int D>
+constexpr int valu_row_stride() { return D + 4; }
+template <int R, int GB>
+constexpr int valu_tile_rows() { return R + R / GB; }
+template <int GB>
+__device__ __forceinline__ int valu_row(int r) { return r + r / GB; }
+
 // Rows r0 .. r0 + R - 1 of two row-major fp32 [nrows, D] tensors into LDS
-// tiles by NT threads, rows past nrows as zero, in 16-byte loads and stores.
-// x and y are 16-byte aligned: the entry points reject unaligned tensors, and
-// a head's rows start at a multiple of 16 bytes since D is a multiple of 4.
-template <int R, int D, int NT>
+// tiles (the layout above) by NT threads, rows past nrows as zero, in
+// 16-byte loads and stores. x and y are 16-byte aligned: the entry points
+// reject unaligned tensors, and a head's rows start at a multiple of 16
+// bytes since D is a multiple of 4.
+template <int R, int D, int GB, int NT>
 __device__ __forceinline__ void stage_rows_f32(const float* x, const float* y, int64_t r0, int64_t nrows,
-                                               float (*sx)[D], float (*sy)[D]) {
+                                               float (*sx)[valu_row_stride<D>()],
+                                               float (*sy)[valu_row_stride<D>()]) {
   static_assert(D % 4 == 0, "rows of whole 16-byte chunks");
   for (int t = (int)threadIdx.x; t < R * D / 4; t += NT) {
     const int r = t / (D / 4), c = (t % (D / 4)) * 4;
@@ -216,8 +232,8 @@ __device__ __forceinline__ void stage_rows_f32(const float* x, const float* y, i
       u = *reinterpret_cast<const float4*>(x + (r0 + r) * D + c);
       v = *reinterpret_cast<const float4*>(y + (r0 + r) * D + c);
     }
-    *reinterpret_cast<float4*>(&sx[r][c]) = u;
-    *reinterpret_cast<float4*>(&sy[r][c]) = v;
+    *reinterpret_cast<float4*>(&sx[valu_row<GB>(r)][c]) = u;
+    *reinterpret_cast<float4*>(&sy[valu_row<GB>(r)][c]) = v;
   }
 }
 }  // namespace gt

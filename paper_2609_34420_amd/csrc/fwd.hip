@@ -385,8 +385,9 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   constexpr int KB = 128 / kValuSplit; // keys per thread per LDS tile
   constexpr int TK = KB * kValuSplit;
   constexpr int RPB = 128 / kValuSplit;
-  __shared__ __attribute__((aligned(16))) float sK[TK][D];
-  __shared__ __attribute__((aligned(16))) float sV[TK][D];
+  constexpr int LR = valu_tile_rows<TK, KB>(), DP = valu_row_stride<D>();
+  __shared__ __attribute__((aligned(16))) float sK[LR][DP];
+  __shared__ __attribute__((aligned(16))) float sV[LR][DP];
   __shared__ float sT[256];
   const int tid = threadIdx.x;
   const int sp = tid % kValuSplit;   // this thread's key block of each tile
@@ -410,7 +411,7 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   float m = -INFINITY, l = 0.0f;     // running max (natural units) and sum relative to it
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
     __syncthreads();
-    stage_rows_f32<TK, D, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
+    stage_rows_f32<TK, D, KB, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
     __syncthreads();
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
     const int r0 = sp * KB;
@@ -425,7 +426,7 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
     for (int r = 0; r < KB; ++r) {
       float x = sT[(w[r >> 2] >> (8 * (r & 3))) & 0xffu];
 #pragma unroll
-      for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[r0 + r][c], x);
+      for (int c = 0; c < D; ++c) x = fmaf(qv[c], sK[valu_row<KB>(r0 + r)][c], x);
       sc[r] = (r0 + r < nk) ? x : -INFINITY;
       bm = fmaxf(bm, sc[r]);
     }
@@ -442,7 +443,7 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
       const float p = exp2_fast((sc[r] - m) * kLog2e);
       l += p;
 #pragma unroll
-      for (int c = 0; c < D; ++c) acc[c] = fmaf(p, sV[r0 + r][c], acc[c]);
+      for (int c = 0; c < D; ++c) acc[c] = fmaf(p, sV[valu_row<KB>(r0 + r)][c], acc[c]);
     }
   }
   // combine the states of the row (adjacent lanes): max, then each
