@@ -249,19 +249,27 @@ __global__ __launch_bounds__(128) void bwd_dq_valu_kernel(BwdArgs a) {
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
   const bool ok = i < a.Sq;
   float qv[D], dov[D], acc[D];
+  load_row_f32<D>(qg + hq, ok ? i : 0, ok, a.scale, qv);
+  load_row_f32<D>(dog + hq, ok ? i : 0, ok, 1.0f, dov);
 #pragma unroll
-  for (int c = 0; c < D; ++c) {
-    qv[c] = ok ? qg[hq + i * D + c] * a.scale : 0.0f;
-    dov[c] = ok ? dog[hq + i * D + c] : 0.0f;
-    acc[c] = 0.0f;
-  }
+  for (int c = 0; c < D; ++c) acc[c] = 0.0f;
   const float L = ok ? a.lse[(int64_t)h * a.Sq + i] : -INFINITY;
   const float dlt = ok ? a.dlt[(int64_t)h * a.Sq + i] : 0.0f;
   const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
+  // head dims up to 32: the next K/V tile is loaded into registers while
+  // this one is computed (the barriers order LDS only)
+  constexpr bool PF = D <= 32;
+  RowPrefetchF32<TK, D, KB, 128> pf;
+  if constexpr (PF) pf.load(kg + hk, vg + hk, 0, a.Sk);
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
-    __syncthreads();
-    stage_rows_f32<TK, D, KB, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
-    __syncthreads();
+    lds_barrier();
+    if constexpr (PF) {
+      pf.store(sK, sV);
+      if (j0 + TK < a.Sk) pf.load(kg + hk, vg + hk, j0 + TK, a.Sk);
+    } else {
+      stage_rows_f32<TK, D, KB, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
+    }
+    lds_barrier();
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
     const int r0 = sp * KB;
     if (!ok || L == -INFINITY || r0 >= nk) continue;
@@ -327,28 +335,65 @@ __global__ __launch_bounds__(128) void bwd_dkdv_valu_kernel(BwdArgs a) {
   const uint8_t* sbase = seq_spd(a, h) + a.row_off * a.ld_spd + a.col_off;
   const bool ok = j < a.Sk;
   float kv[D], vv[D], dk[D], dv[D];
+  load_row_f32<D>(reinterpret_cast<const float*>(a.k) + hk, ok ? j : 0, ok, a.scale, kv);
+  load_row_f32<D>(reinterpret_cast<const float*>(a.v) + hk, ok ? j : 0, ok, 1.0f, vv);
 #pragma unroll
   for (int c = 0; c < D; ++c) {
-    kv[c] = ok ? reinterpret_cast<const float*>(a.k)[hk + j * D + c] * a.scale : 0.0f;
-    vv[c] = ok ? reinterpret_cast<const float*>(a.v)[hk + j * D + c] : 0.0f;
     dk[c] = 0.0f;
     dv[c] = 0.0f;
   }
+  // A tile: Q and dO rows, LSE and Dlt, and the spd bytes of its queries x
+  // this workgroup's keys (issued together rather than one per score). At
+  // head dims up to 32 the next tile is loaded into registers while this one
+  // is computed (the barriers order LDS only).
+  const float* qf = reinterpret_cast<const float*>(a.q) + hq;
+  const float* of = reinterpret_cast<const float*>(a.d_o) + hq;
+  constexpr bool PF = D <= 32;
+  constexpr int NSB = TQ * RPB / 128;          // spd bytes per thread per tile
+  static_assert(TQ <= 128 && (TQ * RPB) % 128 == 0, "tile statistics and spd bytes per thread");
+  RowPrefetchF32<TQ, D, QB, 128> pf;
+  float pl = -INFINITY, pd = 0.0f;
+  uint8_t psb[NSB];
+  auto load_small = [&](int64_t i0) {
+    const bool in = tid < TQ && i0 + tid < a.Sq;
+    pl = in ? a.lse[(int64_t)h * a.Sq + i0 + tid] : -INFINITY;
+    pd = in ? a.dlt[(int64_t)h * a.Sq + i0 + tid] : 0.0f;
+#pragma unroll
+    for (int s = 0; s < NSB; ++s) {
+      const int t = tid + 128 * s, r = t / RPB, c = t % RPB;
+      psb[s] = (i0 + r < a.Sq && jb + c < a.Sk) ? sbase[(i0 + r) * a.ld_spd + jb + c] : (uint8_t)0;
+    }
+  };
+  auto store_small = [&]() {
+    if (tid < TQ) {
+      sL[tid] = pl;
+      sD[tid] = pd;
+    }
+#pragma unroll
+    for (int s = 0; s < NSB; ++s) {
+      const int t = tid + 128 * s;
+      sS[t / RPB][t % RPB] = psb[s];
+    }
+  };
+  if constexpr (PF) {
+    pf.load(qf, of, 0, a.Sq);
+    load_small(0);
+  }
   for (int64_t i0 = 0; i0 < a.Sq; i0 += TQ) {
-    __syncthreads();
-    stage_rows_f32<TQ, D, QB, 128>(reinterpret_cast<const float*>(a.q) + hq, reinterpret_cast<const float*>(a.d_o) + hq,
-                               i0, a.Sq, sQ, sO);
-    for (int t = tid; t < TQ; t += 128) {
-      const bool in = i0 + t < a.Sq;
-      sL[t] = in ? a.lse[(int64_t)h * a.Sq + i0 + t] : -INFINITY;
-      sD[t] = in ? a.dlt[(int64_t)h * a.Sq + i0 + t] : 0.0f;
+    lds_barrier();
+    if constexpr (PF) {
+      pf.store(sQ, sO);
+      store_small();
+      if (i0 + TQ < a.Sq) {
+        pf.load(qf, of, i0 + TQ, a.Sq);
+        load_small(i0 + TQ);
+      }
+    } else {
+      stage_rows_f32<TQ, D, QB, 128>(qf, of, i0, a.Sq, sQ, sO);
+      load_small(i0);
+      store_small();
     }
-    // the tile's spd bytes, issued together rather than one per score in the loop
-    for (int t = tid; t < TQ * RPB; t += 128) {
-      const int r = t / RPB, c = t % RPB;
-      sS[r][c] = (i0 + r < a.Sq && jb + c < a.Sk) ? sbase[(i0 + r) * a.ld_spd + jb + c] : (uint8_t)0;
-    }
-    __syncthreads();
+    lds_barrier();
     if (!ok) continue;
     const int nq = (int)((a.Sq - i0) < TQ ? (a.Sq - i0) : TQ);
     const int e = (sp + 1) * QB < nq ? (sp + 1) * QB : nq;

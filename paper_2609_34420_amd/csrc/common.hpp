@@ -236,4 +236,54 @@ __device__ __forceinline__ void stage_rows_f32(const float* x, const float* y, i
     *reinterpret_cast<float4*>(&sy[valu_row<GB>(r)][c]) = v;
   }
 }
+
+// The same tiles through registers: load() issues the 16-byte loads of a
+// tile, store() writes them to LDS, so the loads of the next tile are in
+// flight while the current one is computed (2 R D / NT floats per thread).
+template <int R, int D, int GB, int NT>
+struct RowPrefetchF32 {
+  static_assert(D % 4 == 0 && (R * D / 4) % NT == 0, "whole 16-byte chunks, evenly over the threads");
+  static constexpr int N = R * D / 4 / NT;
+  float4 u[N], v[N];
+  __device__ __forceinline__ void load(const float* x, const float* y, int64_t r0, int64_t nrows) {
+#pragma unroll
+    for (int s = 0; s < N; ++s) {
+      const int t = (int)threadIdx.x + s * NT;
+      const int r = t / (D / 4), c = (t % (D / 4)) * 4;
+      u[s] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      v[s] = u[s];
+      if (r0 + r < nrows) {
+        u[s] = *reinterpret_cast<const float4*>(x + (r0 + r) * D + c);
+        v[s] = *reinterpret_cast<const float4*>(y + (r0 + r) * D + c);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(float (*sx)[valu_row_stride<D>()], float (*sy)[valu_row_stride<D>()]) const {
+#pragma unroll
+    for (int s = 0; s < N; ++s) {
+      const int t = (int)threadIdx.x + s * NT;
+      const int r = t / (D / 4), c = (t % (D / 4)) * 4;
+      *reinterpret_cast<float4*>(&sx[valu_row<GB>(r)][c]) = u[s];
+      *reinterpret_cast<float4*>(&sy[valu_row<GB>(r)][c]) = v[s];
+    }
+  }
+};
+
+// Row `row` of a row-major fp32 [*, D] tensor (16-byte aligned rows) times
+// `mul` into registers, or zeros when !ok. The row is read unconditionally
+// (callers pass a valid row, clamped when !ok) in 16-byte loads that are
+// all in flight together, rather than one guarded load and wait per element.
+template <int D>
+__device__ __forceinline__ void load_row_f32(const float* base, int64_t row, bool ok, float mul, float (&out)[D]) {
+  const float4* p = reinterpret_cast<const float4*>(base + row * D);
+  const float f = ok ? mul : 0.0f;
+#pragma unroll
+  for (int c = 0; c < D / 4; ++c) {
+    const float4 x = p[c];
+    out[4 * c] = x.x * f;
+    out[4 * c + 1] = x.y * f;
+    out[4 * c + 2] = x.z * f;
+    out[4 * c + 3] = x.w * f;
+  }
+}
 }  // namespace gt

@@ -402,17 +402,25 @@ __global__ __launch_bounds__(128) void fwd_valu_kernel(FwdArgs a) {
   const int64_t hq = (int64_t)h * a.Sq * D, hk = (int64_t)h * a.Sk * D;
   const bool ok = i < a.Sq;
   float qv[D], acc[D];
+  load_row_f32<D>(qg + hq, ok ? i : 0, ok, a.scale, qv);
 #pragma unroll
-  for (int c = 0; c < D; ++c) {
-    qv[c] = ok ? qg[hq + i * D + c] * a.scale : 0.0f;
-    acc[c] = 0.0f;
-  }
+  for (int c = 0; c < D; ++c) acc[c] = 0.0f;
   const uint8_t* srow = ok ? seq_spd(a, h) + (a.row_off + i) * a.ld_spd + a.col_off : nullptr;
   float m = -INFINITY, l = 0.0f;     // running max (natural units) and sum relative to it
+  // head dims up to 32: the next K/V tile is loaded into registers while
+  // this one is computed (the barriers order LDS only)
+  constexpr bool PF = D <= 32;
+  RowPrefetchF32<TK, D, KB, 128> pf;
+  if constexpr (PF) pf.load(kg + hk, vg + hk, 0, a.Sk);
   for (int64_t j0 = 0; j0 < a.Sk; j0 += TK) {
-    __syncthreads();
-    stage_rows_f32<TK, D, KB, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
-    __syncthreads();
+    lds_barrier();
+    if constexpr (PF) {
+      pf.store(sK, sV);
+      if (j0 + TK < a.Sk) pf.load(kg + hk, vg + hk, j0 + TK, a.Sk);
+    } else {
+      stage_rows_f32<TK, D, KB, 128>(kg + hk, vg + hk, j0, a.Sk, sK, sV);
+    }
+    lds_barrier();
     const int nk = (int)((a.Sk - j0) < TK ? (a.Sk - j0) : TK);
     const int r0 = sp * KB;
     if (!ok || r0 >= nk) continue;
